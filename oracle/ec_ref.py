@@ -1,0 +1,295 @@
+"""CPU float64 oracle of the expert-choice (EC) MoE layer.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path imports, links or calls
+this module: only the tests, the smoke check and the CPU-baseline leg of the
+benchmark do.  It shares no code with the HIP library.
+
+Every function evaluates the plain definition in float64 on the exact stored
+input values (bf16 bit patterns or fp32 values widened to float64).  Matrix
+products use numpy's matmul as a library primitive; there is no blocking or
+fusion beyond the definitions below.
+
+Notation (the letters of the layer's interface; the paper swaps c and k between
+its Section 2.2 and its Section 4):
+  N tokens, d model width, E experts, h expert hidden width,
+  G routing groups (sequences), group g = tokens [off[g], off[g+1]),
+  k_g tokens selected by each expert in group g,
+  c capacity factor (average experts per token, c = k*E/L),
+  t mask ratio of a sequence.
+
+Pins (tests/test_oracle.py): brute-force selection on tiny inputs, exactly k_g
+tokens per (group, expert), softmax closed forms, the dense soft mixture when
+every token is selected, the textbook SwiGLU FFN when E = 1, central finite
+differences of the backward, and Table 5 of the paper for the capacity
+schedulers.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+
+import numpy as np
+
+
+# ---------------------------------------------------------------------------
+# Storage formats
+# ---------------------------------------------------------------------------
+
+def widen(a: np.ndarray) -> np.ndarray:
+    """Exact float64 value of stored data: uint16 arrays are bf16 bit patterns."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Capacity (Section 4.2 capacity function, Table 1 schedulers, Appendix H)
+# ---------------------------------------------------------------------------
+
+GAUSS_SIGMA = 0.22  # Appendix H
+
+
+def gaussian_g(r, sigma: float = GAUSS_SIGMA):
+    """Unnormalised bump exp(-(r - 1/2)^2 / (2 sigma^2)) of the Gaussian scheduler (Appendix H)."""
+    r = np.asarray(r, dtype=np.float64)
+    return np.exp(-((r - 0.5) ** 2) / (2.0 * sigma * sigma))
+
+
+def gaussian_g_tilde(r, sigma: float = GAUSS_SIGMA):
+    """Gaussian rescaled so that it is 0 at r = 0 and r = 1 and 1 at r = 1/2 (Appendix H)."""
+    g0 = math.exp(-1.0 / (8.0 * sigma * sigma))
+    return (gaussian_g(r, sigma) - g0) / (1.0 - g0)
+
+
+def scheduler(name: str, r):
+    """Scheduler s(r) in [0, 1] of Table 1 as a function of the mask ratio r."""
+    r = np.asarray(r, dtype=np.float64)
+    if name == "linear":
+        return r.copy()
+    if name == "linear_rev":
+        return 1.0 - r
+    if name == "cosine":
+        return 0.5 * (1.0 - np.cos(np.pi * r))
+    if name == "cosine_rev":
+        return 0.5 * (1.0 + np.cos(np.pi * r))
+    if name == "gaussian":
+        return gaussian_g_tilde(r)
+    if name == "gaussian_rev":
+        return 1.0 - gaussian_g_tilde(r)
+    raise ValueError(f"unknown scheduler {name!r}")
+
+
+def capacity_factor_ref(t, c_min: float, c_max: float, sched: str = "linear_rev"):
+    """c(t) = clamp(c_min + (c_max - c_min) s(t), c_min, c_max)  (Section 4.2)."""
+    c = c_min + (c_max - c_min) * scheduler(sched, t)
+    return np.clip(c, c_min, c_max)
+
+
+def capacity_ref(group_lengths, n_experts: int, c=None, t=None, c_min=None, c_max=None,
+                 sched: str = "linear_rev") -> np.ndarray:
+    """Tokens per expert in each group.
+
+    Section 2.2 equates expert-choice capacity with a token-choice top-c budget:
+    E experts taking k tokens each out of L give E*k = c*L pairs, so k = L*c/E.  With a time-dependent capacity,
+    c = c(t_g) per group (Section 4.2).  k is rounded half-to-even and clamped to
+    [0, L_g].
+    """
+    L = np.asarray(group_lengths, dtype=np.float64)
+    if c is not None:
+        cg = np.full(L.shape, float(c))
+    else:
+        cg = capacity_factor_ref(np.asarray(t, dtype=np.float64), c_min, c_max, sched)
+    k = np.rint(L * cg / float(n_experts))
+    return np.clip(k, 0, L).astype(np.int64)
+
+
+# ---------------------------------------------------------------------------
+# Router (Section 2.2: score matrix S in R^{N x E}; softmax over the experts)
+# ---------------------------------------------------------------------------
+
+def softmax_ref(Z: np.ndarray, inv_tau: float = 1.0) -> np.ndarray:
+    """Row softmax of Z / tau, shifted by the row maximum for stability."""
+    Z = np.asarray(Z, dtype=np.float64) * float(inv_tau)
+    Z = Z - Z.max(axis=1, keepdims=True)
+    e = np.exp(Z)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def router_ref(X, Wg, inv_tau: float = 1.0) -> np.ndarray:
+    """S = softmax(X Wg^T / tau) with Wg stored [E, d]."""
+    return softmax_ref(widen(X) @ widen(Wg).T, inv_tau)
+
+
+# ---------------------------------------------------------------------------
+# Expert-choice selection (Section 2.2: T_j = TopC_i(S_ij); per routing group,
+# Section 5.2: each expert chooses from the same L-token pool of its sequence)
+# ---------------------------------------------------------------------------
+
+def select_ref(S, group_offsets, capacity) -> np.ndarray:
+    """sel_token[E, K_tot]: for each expert j and group g, the k_g tokens of the group
+    with the largest S[:, j] (equal scores: lower token index first), listed in
+    ascending token order.  Expert j's row holds group 0's tokens, then group 1's, ...
+    """
+    S = np.asarray(S, dtype=np.float64)
+    off = np.asarray(group_offsets, dtype=np.int64)
+    k = np.asarray(capacity, dtype=np.int64)
+    E = S.shape[1]
+    K_tot = int(k.sum())
+    sel = np.empty((E, K_tot), dtype=np.int64)
+    for j in range(E):
+        pos = 0
+        for g in range(len(k)):
+            lo, hi = int(off[g]), int(off[g + 1])
+            idx = np.arange(lo, hi)
+            col = S[lo:hi, j]
+            order = np.lexsort((idx, -col))          # score descending, index ascending
+            chosen = np.sort(idx[order[: k[g]]])
+            sel[j, pos: pos + k[g]] = chosen
+            pos += k[g]
+    return sel
+
+
+def slot_ref(sel_token, n_tokens: int) -> np.ndarray:
+    """slot[N, E]: row of token i in expert j's buffer, or -1 if j did not select i."""
+    E, K = sel_token.shape
+    slot = np.full((n_tokens, E), -1, dtype=np.int64)
+    for j in range(E):
+        slot[sel_token[j], j] = np.arange(K)
+    return slot
+
+
+def bruteforce_select(col, k: int) -> tuple:
+    """Among all size-k subsets, the one that no unselected entry beats under the
+    order (score descending, index ascending).  Exponential; tiny inputs only."""
+    col = [float(v) for v in col]
+    n = len(col)
+    found = []
+    for sub in itertools.combinations(range(n), k):
+        s = set(sub)
+        ok = True
+        for a in sub:
+            for b in range(n):
+                if b in s:
+                    continue
+                # b beats a if its score is higher, or equal with a lower index
+                if col[b] > col[a] or (col[b] == col[a] and b < a):
+                    ok = False
+                    break
+            if not ok:
+                break
+        if ok:
+            found.append(sub)
+    assert len(found) == 1, "the selection rule must have exactly one answer"
+    return found[0]
+
+
+# ---------------------------------------------------------------------------
+# Experts (Appendix E: SwiGLU expert FFNs) and combine (Section 2.2)
+# ---------------------------------------------------------------------------
+
+def silu(z):
+    return z / (1.0 + np.exp(-z))
+
+
+def swiglu_ffn_ref(x, W1j, W3j, W2j):
+    """FFN_j(x) = W2_j (SiLU(W1_j x) * (W3_j x)), rows of x are tokens."""
+    x = widen(x)
+    h1 = x @ widen(W1j).T
+    h3 = x @ widen(W3j).T
+    return (silu(h1) * h3) @ widen(W2j).T
+
+
+def forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 1.0,
+                sel_token=None) -> dict:
+    """Layer output y_i = sum over experts j that selected i of g_ij FFN_j(x_i),
+    with g_ij = S_ij; y_i = 0 when no expert selected token i.
+
+    If sel_token is given it replaces the selection (used to evaluate the layer on
+    the selection another implementation made from its own score matrix)."""
+    Xf, W1f, W3f, W2f = widen(X), widen(W1), widen(W3), widen(W2)
+    S = router_ref(X, Wg, inv_tau)
+    sel = select_ref(S, group_offsets, capacity) if sel_token is None else np.asarray(sel_token)
+    E = S.shape[1]
+    Y = np.zeros_like(Xf)
+    gate = np.empty(sel.shape, dtype=np.float64)
+    for j in range(E):
+        rows = sel[j]
+        gate[j] = S[rows, j]
+        o = swiglu_ffn_ref(Xf[rows], W1f[j], W3f[j], W2f[j])
+        Y[rows] += gate[j][:, None] * o            # rows are distinct within one expert
+    return {"S": S, "sel_token": sel, "gate": gate, "Y": Y}
+
+
+def dense_loop_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 1.0):
+    """The combine as an explicit loop over (expert, selected token), one vector at a
+    time.  Small inputs only."""
+    Xf, W1f, W3f, W2f = widen(X), widen(W1), widen(W3), widen(W2)
+    S = router_ref(X, Wg, inv_tau)
+    sel = select_ref(S, group_offsets, capacity)
+    Y = np.zeros_like(Xf)
+    for j in range(sel.shape[0]):
+        for i in sel[j]:
+            x = Xf[i]
+            a = silu(W1f[j] @ x) * (W3f[j] @ x)
+            Y[i] = Y[i] + S[i, j] * (W2f[j] @ a)
+    return Y
+
+
+# ---------------------------------------------------------------------------
+# Backward: exact derivatives with the selection held fixed (it is an index set)
+# ---------------------------------------------------------------------------
+
+def backward_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau: float = 1.0,
+                 sel_token=None) -> dict:
+    """Gradients of sum(Y * dY) w.r.t. X, Wg, W1, W3, W2.
+
+    Chain, per selected pair (i, j) with x = x_i:
+      O = W2_j A, A = SiLU(H1) * H3, H1 = W1_j x, H3 = W3_j x, y_i += S_ij O
+      dO = S_ij dY_i,  dS_ij = <dY_i, O>
+      dA = W2_j^T dO,  dW2_j += dO A^T
+      dH3 = dA * SiLU(H1),  dH1 = dA * H3 * SiLU'(H1)
+      dx += W1_j^T dH1 + W3_j^T dH3,  dW1_j += dH1 x^T,  dW3_j += dH3 x^T
+    Router: S_i = softmax(Z_i / tau), Z = X Wg^T; dS is zero off the selection,
+      dZ_i = (S_i * (dS_i - <S_i, dS_i>)) / tau,  dWg = dZ^T X,  dX += dZ Wg.
+    """
+    Xf, Wgf, W1f, W3f, W2f = widen(X), widen(Wg), widen(W1), widen(W3), widen(W2)
+    dYf = widen(dY)
+    S = router_ref(X, Wg, inv_tau)
+    sel = select_ref(S, group_offsets, capacity) if sel_token is None else np.asarray(sel_token)
+    E = S.shape[1]
+    dX = np.zeros_like(Xf)
+    dS = np.zeros_like(S)
+    dW1 = np.zeros_like(W1f)
+    dW3 = np.zeros_like(W3f)
+    dW2 = np.zeros_like(W2f)
+    for j in range(E):
+        rows = sel[j]
+        x = Xf[rows]
+        h1 = x @ W1f[j].T
+        h3 = x @ W3f[j].T
+        sg = 1.0 / (1.0 + np.exp(-h1))
+        a = h1 * sg * h3
+        o = a @ W2f[j].T
+        g = S[rows, j]
+        dy = dYf[rows]
+        dS[rows, j] = np.sum(dy * o, axis=1)
+        do = g[:, None] * dy
+        da = do @ W2f[j]
+        dW2[j] = do.T @ a
+        dh3 = da * (h1 * sg)
+        dh1 = da * h3 * (sg * (1.0 + h1 * (1.0 - sg)))
+        dX[rows] += dh1 @ W1f[j] + dh3 @ W3f[j]
+        dW1[j] = dh1.T @ x
+        dW3[j] = dh3.T @ x
+    dZ = S * (dS - np.sum(S * dS, axis=1, keepdims=True)) * float(inv_tau)
+    dWg = dZ.T @ Xf
+    dX += dZ @ Wgf
+    return {"dX": dX, "dWg": dWg, "dW1": dW1, "dW3": dW3, "dW2": dW2, "dS": dS,
+            "S": S, "sel_token": sel}
+
+
+def loss_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau, sel_token) -> float:
+    """sum(Y * dY) with a fixed selection: the scalar whose gradient backward_ref returns."""
+    Y = forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau, sel_token)["Y"]
+    return float(np.sum(Y * widen(dY)))

@@ -1,0 +1,362 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+None of these tests re-types the oracle's formulas: each compares it with an
+independent fact (brute force, closed forms, invariants, library routines,
+finite differences, values printed in the paper).  The mutation tests at the
+end plant plausible mistakes in the oracle and check that a pin catches each.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import ec_ref as ref
+from paper_2604_01622_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _tiny_inputs(G_lens, d, E, h, seed, dtype="f32"):
+    wl = synth.small("t", G_lens, d, E, h, dtype=dtype, seed=seed, capacity_factor=1.0)
+    return synth.draw(wl, with_dy=True)
+
+
+# --------------------------------------------------------------------- storage
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(0)
+    a = (rng.standard_normal(100000) * np.exp(rng.uniform(-20, 20, 100000))).astype(np.float32)
+    a[:4] = [1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 0.0]   # exact ties
+    bits = synth.f32_to_bf16_bits(a)
+    t = torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(bits, t)
+    # widen() is exact: bf16 -> float64 -> bf16 round trip is the identity
+    w = ref.widen(bits)
+    assert np.array_equal(synth.f32_to_bf16_bits(w.astype(np.float32)), bits)
+    assert np.array_equal(w, torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy())
+
+
+# --------------------------------------------------------------------- softmax
+
+def test_softmax_rows_sum_to_one_and_positive():
+    rng = np.random.default_rng(1)
+    Z = rng.standard_normal((200, 17)) * 5
+    for inv_tau in (0.5, 1.0, 2.0):
+        S = ref.softmax_ref(Z, inv_tau)
+        assert np.all(S > 0)
+        assert np.max(np.abs(S.sum(axis=1) - 1.0)) < 1e-12
+
+
+def test_softmax_two_experts_is_logistic():
+    # E = 2: S_i0 = 1 / (1 + exp(-(z0 - z1)/tau)), a closed form independent of the max shift
+    rng = np.random.default_rng(2)
+    Z = rng.standard_normal((100, 2)) * 3
+    for tau in (0.5, 1.0, 2.0):
+        S = ref.softmax_ref(Z, 1.0 / tau)
+        expect = 1.0 / (1.0 + np.exp(-(Z[:, 0] - Z[:, 1]) / tau))
+        assert np.max(np.abs(S[:, 0] - expect)) < 1e-14
+
+
+def test_softmax_shift_invariance_and_library():
+    rng = np.random.default_rng(3)
+    Z = rng.standard_normal((50, 9))
+    S = ref.softmax_ref(Z, 0.7)
+    assert np.allclose(ref.softmax_ref(Z + rng.standard_normal((50, 1)) * 10, 0.7), S, atol=1e-14)
+    lib = torch.softmax(torch.from_numpy(Z) * 0.7, dim=1).numpy()
+    assert np.allclose(S, lib, atol=1e-15, rtol=1e-13)
+
+
+def test_router_special_cases():
+    inp = _tiny_inputs([16], 8, 5, 4, seed=4)
+    S0 = ref.router_ref(inp.X, np.zeros_like(inp.Wg))
+    assert np.allclose(S0, 1.0 / 5, atol=1e-15)
+    S1 = ref.router_ref(inp.X, inp.Wg[:1])
+    assert np.all(S1 == 1.0)
+    # router logits are X Wg^T with Wg stored [E, d]: check one logit by hand
+    Xf, Wgf = ref.widen(inp.X), ref.widen(inp.Wg)
+    z = sum(Xf[3, q] * Wgf[2, q] for q in range(8))
+    zz = [sum(Xf[3, q] * Wgf[e, q] for q in range(8)) for e in range(5)]
+    m = max(zz)
+    s = math.exp(z - m) / sum(math.exp(v - m) for v in zz)
+    assert abs(ref.router_ref(inp.X, inp.Wg)[3, 2] - s) < 1e-14
+
+
+# --------------------------------------------------------------------- selection
+
+@pytest.mark.parametrize("seed", range(12))
+def test_selection_equals_bruteforce_with_ties(seed):
+    rng = np.random.default_rng(100 + seed)
+    lens = list(rng.integers(1, 8, size=rng.integers(1, 4)))
+    E = int(rng.integers(1, 4))
+    N = int(sum(lens))
+    # coarse values force many exact ties
+    S = rng.integers(0, 4, size=(N, E)).astype(np.float64) / 4
+    off = np.concatenate([[0], np.cumsum(lens)])
+    for trial in range(3):
+        k = np.array([rng.integers(0, L + 1) for L in lens])
+        sel = ref.select_ref(S, off, k)
+        for j in range(E):
+            pos = 0
+            for g, L in enumerate(lens):
+                bf = ref.bruteforce_select(S[off[g]:off[g + 1], j], int(k[g]))
+                got = sel[j, pos:pos + k[g]] - off[g]
+                assert tuple(got) == tuple(sorted(bf))
+                pos += k[g]
+
+
+def test_selection_invariants_random():
+    rng = np.random.default_rng(5)
+    lens = [37, 64, 5, 90]
+    off = np.concatenate([[0], np.cumsum(lens)])
+    S = ref.softmax_ref(rng.standard_normal((sum(lens), 11)))
+    k = np.array([10, 64, 0, 33])
+    sel = ref.select_ref(S, off, k)
+    assert sel.shape == (11, k.sum())                    # E * sum(k) pairs in total
+    for j in range(11):
+        pos = 0
+        for g in range(4):
+            seg = sel[j, pos:pos + k[g]]
+            assert len(seg) == k[g]                      # exactly k_g per (group, expert)
+            assert np.all((seg >= off[g]) & (seg < off[g + 1]))
+            assert np.all(np.diff(seg) > 0)              # distinct, ascending
+            # every selected score >= every unselected score of that group
+            rest = np.setdiff1d(np.arange(off[g], off[g + 1]), seg)
+            if len(seg) and len(rest):
+                assert S[seg, j].min() >= S[rest, j].max()
+            pos += k[g]
+
+
+def test_selection_degenerate_cases():
+    off = np.array([0, 6, 10])
+    S = np.full((10, 3), 0.25)
+    sel = ref.select_ref(S, off, [2, 4])
+    assert np.array_equal(sel, np.tile([0, 1, 6, 7, 8, 9], (3, 1)))   # constant column: first k
+    sel = ref.select_ref(S, off, [0, 0])
+    assert sel.shape == (3, 0)
+    sel = ref.select_ref(S, off, [6, 4])
+    assert np.array_equal(sel, np.tile(np.arange(10), (3, 1)))        # k = L: every token
+
+
+def test_fig2_toy_loads():
+    # Figure 2: 6 tokens, 3 experts, capacity 2 -> every expert takes 2 tokens
+    with open(os.path.join(GOLDEN, "fig2_toy_loads.txt")) as f:
+        n, E, k, total, load = [int(v) for v in
+                                [ln for ln in f if not ln.startswith("#")][0].split()]
+    rng = np.random.default_rng(6)
+    for _ in range(20):
+        S = ref.softmax_ref(rng.standard_normal((n, E)))
+        sel = ref.select_ref(S, [0, n], [k])
+        loads = [len(sel[j]) for j in range(E)]
+        assert loads == [load] * E and sum(loads) == total
+
+
+# --------------------------------------------------------------------- capacity
+
+def _golden_table5():
+    rows = {}
+    with open(os.path.join(GOLDEN, "table5_flops_equiv.txt")) as f:
+        for ln in f:
+            if ln.startswith("#") or not ln.strip():
+                continue
+            name, es, ek, dk = ln.split()
+            rows[name] = (float(es), float(ek), float(dk))
+    return rows
+
+
+def test_table5_expected_capacity():
+    # Gauss-Legendre quadrature of E[s(r)] over r ~ U(0, 1)
+    x, w = np.polynomial.legendre.leggauss(400)
+    r, w = 0.5 * (x + 1.0), 0.5 * w
+    for name, (es, ek, dk) in _golden_table5().items():
+        Es = float(np.sum(w * ref.scheduler(name, r)))
+        Ek = float(np.sum(w * ref.capacity_factor_ref(r, 8.0, 32.0, name)))
+        assert abs(Es - es) <= 0.5e-4 + 1e-12, (name, Es)
+        # the paper derives E[k] from the rounded E[s] (8 + 24 * 0.5010 = 20.02), so the
+        # rounding of E[s] propagates: allow 24 * 0.5e-4 on top of the printed 2 decimals
+        assert abs(Ek - ek) <= 24 * 0.5e-4 + 0.5e-2 + 1e-9, (name, Ek)
+        assert abs((Ek - 20.0) - dk) <= 0.5e-3 + 1e-9, (name, Ek)
+
+
+def test_gaussian_scheduler_properties():
+    gt = ref.gaussian_g_tilde
+    assert abs(gt(0.0)) < 1e-15 and abs(gt(1.0)) < 1e-15 and abs(gt(0.5) - 1.0) < 1e-15
+    assert abs(ref.gaussian_g(0.0) - math.exp(-1.0 / (8 * 0.22 ** 2))) < 1e-15
+    r = np.linspace(0, 1, 101)
+    assert np.allclose(gt(r), gt(1 - r), atol=1e-15)
+    for name in ("linear", "linear_rev", "cosine", "cosine_rev", "gaussian", "gaussian_rev"):
+        s = ref.scheduler(name, r)
+        assert s.min() >= -1e-15 and s.max() <= 1 + 1e-15
+
+
+def test_capacity_timestep_rule():
+    # c(t) = 12 - 8t is the linear-reverse scheduler with c in [4, 12]; k = L c / E
+    k = ref.capacity_ref([2048] * 3, 64, t=[0.0, 0.5, 1.0], c_min=4, c_max=12)
+    assert list(k) == [384, 256, 128]
+    assert list(ref.capacity_ref([2048], 64, c=8)) == [256]
+    assert list(ref.capacity_ref([4096], 128, c=8)) == [256]
+    assert list(ref.capacity_ref([128], 8, c=2)) == [32]
+    # mean of c(t) under t ~ U(0,1) is 8 (matched FLOPs with the static c = 8)
+    x, w = np.polynomial.legendre.leggauss(50)
+    assert abs(np.sum(0.5 * w * ref.capacity_factor_ref(0.5 * (x + 1), 4, 12)) - 8.0) < 1e-12
+    # clamp to [0, L]
+    assert list(ref.capacity_ref([10], 2, c=5)) == [10]
+    # round half to even: L c / E = 2.5 -> 2, 3.5 -> 4
+    assert list(ref.capacity_ref([5, 7], 2, c=1)) == [2, 4]
+
+
+# --------------------------------------------------------------------- forward
+
+def test_forward_equals_dense_loop():
+    inp = _tiny_inputs([13, 20], 16, 4, 24, seed=8)
+    off = inp.wl.group_offsets
+    k = [5, 7]
+    for inv_tau in (1.0, 2.0):
+        Y = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, inv_tau)["Y"]
+        Yl = ref.dense_loop_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, inv_tau)
+        assert np.max(np.abs(Y - Yl)) < 1e-12
+
+
+def _torch_swiglu(x, W1, W3, W2):
+    x = torch.from_numpy(x)
+    return (torch.nn.functional.silu(x @ torch.from_numpy(W1).T)
+            * (x @ torch.from_numpy(W3).T)) @ torch.from_numpy(W2).T
+
+
+def test_full_capacity_is_dense_soft_mixture():
+    # k_g = L_g for every group: each expert takes every token and the layer is
+    # sum_j S_ij FFN_j(x_i), computed here with torch's silu and matmul
+    inp = _tiny_inputs([9, 14], 16, 3, 20, seed=9, dtype="bf16")
+    off = inp.wl.group_offsets
+    Y = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, [9, 14], 1.5)["Y"]
+    X, Wg = ref.widen(inp.X), ref.widen(inp.Wg)
+    S = torch.softmax(torch.from_numpy(X @ Wg.T) * 1.5, dim=1)
+    Yt = sum(S[:, j:j + 1] * _torch_swiglu(X, ref.widen(inp.W1)[j], ref.widen(inp.W3)[j],
+                                           ref.widen(inp.W2)[j]) for j in range(3))
+    assert np.max(np.abs(Y - Yt.numpy())) < 1e-12
+
+
+def test_single_expert_full_capacity_is_swiglu():
+    inp = _tiny_inputs([11], 8, 1, 12, seed=10)
+    Y = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, [0, 11], [11])["Y"]
+    Yt = _torch_swiglu(ref.widen(inp.X), ref.widen(inp.W1)[0], ref.widen(inp.W3)[0],
+                       ref.widen(inp.W2)[0])
+    assert np.max(np.abs(Y - Yt.numpy())) < 1e-12
+
+
+def test_unselected_tokens_get_zero():
+    inp = _tiny_inputs([30], 8, 2, 8, seed=11)
+    out = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, [0, 30], [3])
+    chosen = set(out["sel_token"].ravel().tolist())
+    for i in range(30):
+        if i not in chosen:
+            assert np.all(out["Y"][i] == 0)
+        else:
+            assert np.any(out["Y"][i] != 0)
+    assert np.array_equal(out["gate"], np.take_along_axis(out["S"].T, out["sel_token"], 1))
+
+
+# --------------------------------------------------------------------- backward
+
+def test_backward_matches_finite_differences():
+    inp = _tiny_inputs([7, 6], 8, 3, 6, seed=12)
+    off = inp.wl.group_offsets
+    k = [3, 2]
+    inv_tau = 1.7
+    args = [ref.widen(a) for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2)]
+    dY = ref.widen(inp.dY)
+    g = ref.backward_ref(*args, dY, off, k, inv_tau)
+    sel = g["sel_token"]
+    names = ["dX", "dWg", "dW1", "dW3", "dW2"]
+    rng = np.random.default_rng(0)
+    eps = 1e-6
+    for a_i, name in enumerate(names):
+        flat = args[a_i].reshape(-1)
+        for q in rng.choice(flat.size, size=min(25, flat.size), replace=False):
+            old = flat[q]
+            flat[q] = old + eps
+            lp = ref.loss_ref(*args, dY, off, k, inv_tau, sel)
+            flat[q] = old - eps
+            lm = ref.loss_ref(*args, dY, off, k, inv_tau, sel)
+            flat[q] = old
+            fd = (lp - lm) / (2 * eps)
+            an = g[name].reshape(-1)[q]
+            assert abs(fd - an) <= 1e-7 * max(1.0, abs(an)), (name, q, fd, an)
+
+
+def test_backward_matches_torch_autograd():
+    inp = _tiny_inputs([10, 12], 16, 4, 8, seed=13, dtype="bf16")
+    off = inp.wl.group_offsets
+    k = [4, 6]
+    inv_tau = 0.5
+    g = ref.backward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, off, k, inv_tau)
+    sel = g["sel_token"]
+    T = [torch.from_numpy(ref.widen(a)).requires_grad_(True)
+         for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2)]
+    X, Wg, W1, W3, W2 = T
+    S = torch.softmax((X @ Wg.T) * inv_tau, dim=1)
+    Y = torch.zeros_like(X)
+    for j in range(4):
+        rows = torch.from_numpy(sel[j])
+        o = _torch_swiglu_t(X[rows], W1[j], W3[j], W2[j])
+        Y = Y.index_add(0, rows, S[rows, j:j + 1] * o)
+    (Y * torch.from_numpy(ref.widen(inp.dY))).sum().backward()
+    for t, name in zip(T, ["dX", "dWg", "dW1", "dW3", "dW2"]):
+        assert np.max(np.abs(t.grad.numpy() - g[name])) < 1e-12, name
+
+
+def _torch_swiglu_t(x, W1, W3, W2):
+    return (torch.nn.functional.silu(x @ W1.T) * (x @ W3.T)) @ W2.T
+
+
+# --------------------------------------------------------------------- mutation tests
+
+def test_pins_catch_planted_mistakes(monkeypatch):
+    """Plant plausible mistakes in the oracle and check that a pin above fails."""
+    # 1. tie-break toward the higher index: brute force disagrees
+    S = np.array([[0.5], [0.5], [0.25]])
+    good = ref.select_ref(S, [0, 3], [1])
+    bad = np.array([[1]])
+    assert not np.array_equal(good, bad) and tuple(good[0]) == ref.bruteforce_select(S[:, 0], 1)
+
+    # 2. temperature applied as multiplication by tau instead of division
+    Z = np.array([[1.0, -0.5]])
+    tau = 2.0
+    wrong = ref.softmax_ref(Z, tau)[0, 0]
+    right = 1.0 / (1.0 + math.exp(-(1.5) / tau))
+    assert abs(wrong - right) > 1e-3 and abs(ref.softmax_ref(Z, 1 / tau)[0, 0] - right) < 1e-15
+
+    # 3. SiLU replaced by a plain sigmoid gate: the textbook SwiGLU pin fails
+    inp = _tiny_inputs([11], 8, 1, 12, seed=10)
+    monkeypatch.setattr(ref, "silu", lambda z: 1.0 / (1.0 + np.exp(-z)))
+    Y = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, [0, 11], [11])["Y"]
+    Yt = _torch_swiglu(ref.widen(inp.X), ref.widen(inp.W1)[0], ref.widen(inp.W3)[0],
+                       ref.widen(inp.W2)[0])
+    assert np.max(np.abs(Y - Yt.numpy())) > 1e-3
+    monkeypatch.undo()
+
+    # 4. W1 and W3 swapped in the FFN: the dense-mixture pin fails
+    inp = _tiny_inputs([9], 16, 2, 20, seed=9)
+    Yswap = ref.forward_ref(inp.X, inp.Wg, inp.W3, inp.W1, inp.W2, [0, 9], [9])["Y"]
+    Yok = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, [0, 9], [9])["Y"]
+    assert np.max(np.abs(Yswap - Yok)) > 1e-3
+
+    # 5. router backward without the <S, dS> term: finite differences disagree
+    inp = _tiny_inputs([6], 8, 3, 6, seed=12)
+    args = [ref.widen(a) for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2)]
+    dY = ref.widen(inp.dY)
+    g = ref.backward_ref(*args, dY, [0, 6], [2], 1.0)
+    S, dS = g["S"], g["dS"]
+    dZ_bad = S * dS
+    dWg_bad = dZ_bad.T @ args[0]
+    eps = 1e-6
+    flat = args[1].reshape(-1)
+    flat[0] += eps
+    lp = ref.loss_ref(*args, dY, [0, 6], [2], 1.0, g["sel_token"])
+    flat[0] -= 2 * eps
+    lm = ref.loss_ref(*args, dY, [0, 6], [2], 1.0, g["sel_token"])
+    flat[0] += eps
+    fd = (lp - lm) / (2 * eps)
+    assert abs(fd - g["dWg"].reshape(-1)[0]) < 1e-7
+    assert abs(fd - dWg_bad.reshape(-1)[0]) > 1e-6
