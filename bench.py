@@ -1,0 +1,227 @@
+"""Benchmark of the expert-choice MoE layer on one MI355X.
+
+A step is one pass of the whole layer over one batch: routing (router GEMM +
+softmax, column top-k), gather, SwiGLU expert grouped GEMMs, combine, and the
+full backward (gate gradient, grouped dgrad/wgrad GEMMs, router backward).
+Default workload: 8 sequences x 2048 tokens, d = 2048, 64 experts of hidden
+1024, per-sequence capacity c(t) = 12 - 8t (mask ratio t ~ U(0,1)), bf16
+storage, forward + backward.  Prints ONE JSON line on stdout.
+
+    python bench.py [--steps K] [--warmup W] [--workload train|static|timestep|fine|tiny]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "EC-MoE layer tokens/s fwd and fwd+bwd; grouped-GEMM MFMA util % and route GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+GEMM_STAGES = {"gemm_w13_swiglu", "gemm_w2", "gemm_dA_swiglu_bwd", "gemm_dW2", "gemm_dXe",
+               "gemm_dW13", "router_dx", "router_dwg"}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits):
+    """(algorithmic flops, algorithmic HBM bytes) of one launch of a stage."""
+    P = E * K
+    s = esz
+    table = {
+        "router": (2 * N * d * E, N * d * s + E * d * s + 2 * N * E * 4),
+        "topk": (0, 2 * E * N * 4 + P * 4),
+        "gather": (0, P * 4 + 2 * P * d * s),
+        "gemm_w13_swiglu": (4 * P * d * h, P * d * s + 2 * E * h * d * s + P * h * s
+                            + (2 * P * h * s if save_h else 0)),
+        "gemm_w2": (2 * P * d * h, P * h * s + E * d * h * s + P * d * s),
+        "combine": (0, 2 * E * N * 4 + P * d * s + N * d * s),
+        "bwd_gather": (0, 3 * P * 4 + 3 * P * d * s),
+        "gemm_dA_swiglu_bwd": (2 * P * d * h, P * d * s + E * d * h * s + 4 * P * h * s),
+        "gemm_dW2": (2 * P * d * h, P * d * s + P * h * s + E * d * h * s),
+        "gemm_dXe": (4 * P * d * h, 2 * P * h * s + 2 * E * h * d * s + P * d * s),
+        "gemm_dW13": (4 * P * d * h, 2 * P * h * s + P * d * s + 2 * E * h * d * s),
+        "router_dz": (0, 3 * N * E * 4 + P * 4 + N * EP * 2),
+        "router_dx": (2 * N * EP * d, N * EP * 2 + E * d * s + N * d * s),
+        "bwd_combine": (0, E * N * 4 + P * d * s + 2 * N * d * s),
+        "router_dwg": (2 * N * EP * d, N * EP * 2 + N * d * s + 2 * splits * E * d * 4),
+    }
+    return table[name]
+
+
+def cpu_baseline(inp, caps, inv_tau, backward):
+    """The float64 oracle on a bounded sample (the first routing group) on the host cores."""
+    from oracle import ec_ref as ref
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = len(os.sched_getaffinity(0))
+    wl = inp.wl
+    L0 = wl.group_lengths[0]
+    X = inp.X[:L0]
+    off = np.array([0, L0])
+    k = [int(caps[0])]
+    t0 = time.perf_counter()
+    fw = ref.forward_ref(X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, inv_tau)
+    if backward:
+        ref.backward_ref(X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY[:L0], off, k, inv_tau,
+                         sel_token=fw["sel_token"])
+    dt = time.perf_counter() - t0
+    return {"value": L0 / dt, "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
+            "sample": f"routing group 0 of {wl.n_groups} ({L0} tokens, k={k[0]}, all "
+                      f"{wl.n_experts} experts), {'fwd+bwd' if backward else 'fwd'}, "
+                      f"numpy float64, {dt:.1f} s",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="train",
+                    choices=["train", "static", "timestep", "fine", "tiny"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-forward-only", action="store_true")
+    a = ap.parse_args()
+    if a.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {a.gpus} is not supported (the layer's "
+              "multi-GPU sharding is a design, not part of this build)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2604_01622_amd as ec
+    from paper_2604_01622_amd import binding, synth
+
+    wl = {"train": synth.TRAIN_BF16, "static": synth.STATIC_BF16, "timestep": synth.TIMESTEP_BF16,
+          "fine": synth.FINE_BF16, "tiny": synth.TINY_F32}[a.workload]
+    backward = a.workload == "train"
+    inv_tau = wl.inv_temperatures[0]
+    torch.cuda.set_device(0)
+    log(f"[bench] drawing {wl.name}")
+    inp = synth.draw(wl, with_dy=backward)
+    L = np.asarray(wl.group_lengths)
+    if wl.time_dependent:
+        caps = ec.capacity(L, wl.n_experts, t=inp.t, c_min=wl.c_min, c_max=wl.c_max)
+    else:
+        caps = ec.capacity(L, wl.n_experts, c=wl.capacity_factor)
+
+    def dev(x):
+        if x.dtype == np.uint16:
+            return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(x).cuda()
+
+    X, Wg, W1, W3, W2 = (dev(x) for x in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2))
+    dY = dev(inp.dY) if backward else None
+    layer = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, training=backward)
+    N, d, E, h, K = wl.n_tokens, wl.d_model, wl.n_experts, wl.d_ff, layer.P.K
+    esz = 2 if wl.dtype == "bf16" else 4
+    EP = (E + 63) // 64 * 64
+    splits = max(1, min((512 + (d + 127) // 128 - 1) // ((d + 127) // 128), (N + 255) // 256))
+
+    def step():
+        layer.forward()
+        if backward:
+            layer.backward(dY)
+
+    log(f"[bench] warmup {a.warmup}")
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    fwd_ev = [binding.StageEvents(len(binding.FORWARD_STAGES)) for _ in range(a.steps)]
+    bwd_ev = [binding.StageEvents(len(binding.BACKWARD_STAGES)) for _ in range(a.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log(f"[bench] timing {a.steps} steps")
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(a.steps):
+        fwd_ev[i].arm()
+        layer.forward()
+        if backward:
+            bwd_ev[i].arm()
+            layer.backward(dY)
+    binding.StageEvents.disarm()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / a.steps
+    value = N / (ms * 1e-3)
+
+    stage_ms = {}
+    for n, col in zip(binding.FORWARD_STAGES, zip(*[e.durations_ms() for e in fwd_ev])):
+        stage_ms[n] = float(np.mean(col))
+    if backward:
+        for n, col in zip(binding.BACKWARD_STAGES, zip(*[e.durations_ms() for e in bwd_ev])):
+            stage_ms[n] = float(np.mean(col))
+    stages = {}
+    for n, t in stage_ms.items():
+        fl, by = stage_work(n, N, d, E, h, K, esz, EP, backward, splits)
+        st = {"ms": round(t, 4)}
+        if n in GEMM_STAGES:
+            st["tflops"] = round(fl / (t * 1e-3) / 1e12, 1)
+            st["mfma_frac"] = round(fl / (t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+        else:
+            st["gbs"] = round(by / (t * 1e-3) / 1e9, 1)
+            st["hbm_frac"] = round(by / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
+        stages[n] = st
+    dom = max(stage_ms, key=stage_ms.get)
+    fl, by = stage_work(dom, N, d, E, h, K, esz, EP, backward, splits)
+    t_dom = stage_ms[dom] * 1e-3
+    if dom in GEMM_STAGES:
+        peak = PEAK_BF16_TFLOPS if esz == 2 else PEAK_F32_TFLOPS
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(fl / t_dom / 1e12, 1),
+                "peak": peak, "unit": "TFLOP/s", "frac": round(fl / t_dom / 1e12 / peak, 4),
+                "traffic": None, "work_per_launch": fl, "avg_launch_ms": round(stage_ms[dom], 4)}
+    else:
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(by / t_dom / 1e9, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(by / t_dom / 1e9 / PEAK_HBM_GBS, 4),
+                "traffic": None, "work_per_launch": by, "avg_launch_ms": round(stage_ms[dom], 4)}
+    gemm_fl = sum(stage_work(n, N, d, E, h, K, esz, EP, backward, splits)[0]
+                  for n in stage_ms if n.startswith("gemm_"))
+    gemm_ms = sum(stage_ms[n] for n in stage_ms if n.startswith("gemm_"))
+
+    out = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+           "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": wl.dtype, "data": "synthetic (seeded normal inputs and random-init weights)",
+           "config": {"workload": wl.name, "pass": "fwd+bwd" if backward else "fwd",
+                      "tokens": N, "groups": wl.n_groups, "d_model": d, "experts": E,
+                      "d_ff": h, "k_per_group": [int(x) for x in caps], "K_tot": K},
+           "stages": stages, "roofline": roof,
+           "grouped_gemm": {"tflops": round(gemm_fl / (gemm_ms * 1e-3) / 1e12, 1),
+                            "mfma_frac": round(gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
+
+    if backward and not a.no_forward_only:
+        # forward alone, inference mode (no saved activations), same inputs
+        inf = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, training=False)
+        for _ in range(a.warmup):
+            inf.forward()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(a.steps):
+            inf.forward()
+        end.record()
+        torch.cuda.synchronize()
+        fms = start.elapsed_time(end) / a.steps
+        out["forward_only"] = {"tokens_per_s": round(N / (fms * 1e-3), 1), "ms": round(fms, 4)}
+        del inf
+
+    if not a.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle on a sample)")
+        out["cpu_baseline"] = cpu_baseline(inp, caps, inv_tau, backward)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,183 @@
+/*
+ * ec_moe.h - C interface of the expert-choice (EC) mixture-of-experts layer
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The layer (paper Section 2.2, "Expert-choice"; SwiGLU experts per Appendix E):
+ *   S   = softmax(X Wg^T / tau) over the E experts, one row per token;
+ *   T_gj = the k_g tokens of routing group g with the largest S[:, j]
+ *          (equal scores: the lower token index wins), for every expert j;
+ *   y_i = sum over experts j with i in T_gj of  S_ij * FFN_j(x_i),
+ *   FFN_j(x) = W2_j (SiLU(W1_j x) * (W3_j x)),   y_i = 0 if no expert chose i.
+ * A routing group is one sequence: every expert chooses from the tokens of the
+ * same sequence (Section 5.2), and its capacity k_g may depend on the
+ * sequence's mask ratio (Section 4.2): k_g = L_g c(t_g) / E, where c is the
+ * average number of experts per token (Section 2.2 relates the two: E k = c L).
+ *
+ * Conventions for every entry point
+ *  - Pointers are DEVICE pointers unless marked HOST.  Device buffers must be
+ *    16-byte aligned.  All arrays are dense row-major with the shapes given.
+ *  - Storage dtype (ec_problem.dtype) applies to X, Wg, W1, W3, W2, Y, dY, dX,
+ *    dW1, dW3, dW2.  S, gates and dWg are always fp32; accumulation is fp32.
+ *  - The caller owns every buffer (inputs, outputs, the saved activations and
+ *    the workspace).  The library allocates no device memory and keeps no
+ *    pointer after returning; its only mutable state is per calling thread
+ *    (the last error and the optional stage-timing events), so calls from
+ *    different threads are independent.
+ *  - Work is enqueued on `stream` and the call returns without waiting for it.
+ *    Capacities and group offsets are HOST arrays so that planning needs no
+ *    device synchronisation.
+ *  - Every argument is validated before anything is enqueued; an invalid call
+ *    returns a non-zero ec_status and enqueues nothing.  A failed launch
+ *    returns EC_ERR_HIP.  ec_last_error() gives the detail of the most recent
+ *    failure on the calling thread.  No function aborts or throws.
+ *  - Results are deterministic: no floating-point atomics are used, so two
+ *    calls with the same inputs give bitwise identical outputs.
+ */
+#ifndef EC_MOE_H
+#define EC_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EC_OK = 0,
+  EC_ERR_ARG = 1,        /* null pointer, bad enum, non-finite temperature      */
+  EC_ERR_SHAPE = 2,      /* sizes out of range or inconsistent                  */
+  EC_ERR_CAPACITY = 3,   /* some k_g < 0 or k_g > L_g                           */
+  EC_ERR_DTYPE = 4,      /* unknown storage dtype                               */
+  EC_ERR_ALIGN = 5,      /* a device pointer is not 16-byte aligned             */
+  EC_ERR_WORKSPACE = 6,  /* workspace or saved buffer smaller than required     */
+  EC_ERR_HIP = 7         /* a HIP launch or runtime call failed                 */
+} ec_status;
+
+typedef enum { EC_F32 = 0, EC_BF16 = 1 } ec_dtype;
+
+/* Capacity schedulers s(r) of the paper's Table 1 (Appendix H for the
+ * Gaussian, sigma = 0.22).  c(t) = clamp(c_min + (c_max - c_min) s(t), c_min, c_max). */
+typedef enum {
+  EC_SCHED_LINEAR = 0,        /* s(r) = r                    */
+  EC_SCHED_LINEAR_REV = 1,    /* s(r) = 1 - r                */
+  EC_SCHED_COSINE = 2,        /* s(r) = (1 - cos(pi r)) / 2  */
+  EC_SCHED_COSINE_REV = 3,    /* s(r) = (1 + cos(pi r)) / 2  */
+  EC_SCHED_GAUSSIAN = 4,      /* normalised Gaussian bump    */
+  EC_SCHED_GAUSSIAN_REV = 5   /* 1 - normalised Gaussian     */
+} ec_scheduler;
+
+/* Problem description.  Limits: 1 <= E <= 256; d and h multiples of 64 with
+ * 64 <= d, h <= 16384; 1 <= G; N = group_offsets[G] < 2^31; every expert
+ * buffer E * K_tot * max(d, h) < 2^31 elements.                               */
+typedef struct {
+  int64_t n_tokens;              /* N = sum of the group lengths                       */
+  int32_t d_model;               /* d                                                  */
+  int32_t n_experts;             /* E                                                  */
+  int32_t d_ff;                  /* h, hidden width of each SwiGLU expert              */
+  int32_t n_groups;              /* G routing groups (sequences)                       */
+  const int32_t *group_offsets;  /* HOST [G+1]: group g = tokens [off[g], off[g+1]),
+                                    off[0] = 0, non-decreasing, off[G] = N              */
+  const int32_t *capacity;       /* HOST [G]: k_g tokens per expert in group g,
+                                    0 <= k_g <= off[g+1] - off[g]                       */
+  float inv_temperature;         /* 1/tau > 0; S = softmax(logits * inv_temperature)   */
+  ec_dtype dtype;                /* storage dtype                                      */
+} ec_problem;
+
+/* Byte offsets of the forward activations inside the `saved` buffer that
+ * ec_moe_forward fills and ec_moe_backward reads (K = K_tot = sum_g k_g).
+ * Expert j's rows of every [E, K, .] buffer are [j K, (j+1) K); inside them
+ * group g's k_g tokens follow groups 0..g-1, in ascending token order.        */
+typedef struct {
+  size_t S;          /* fp32  [N, E]    router scores                          */
+  size_t sel_token;  /* int32 [E, K]    selected token of each expert row       */
+  size_t slot;       /* int32 [E, N]    [j, i]: row of token i in expert j's
+                        buffer, or -1 if expert j did not select token i        */
+  size_t Xe;         /* dtype [E, K, d] gathered tokens                         */
+  size_t H1;         /* dtype [E, K, h] W1 projection                           */
+  size_t H3;         /* dtype [E, K, h] W3 projection                           */
+  size_t A;          /* dtype [E, K, h] SiLU(H1) * H3                           */
+  size_t O;          /* dtype [E, K, d] expert outputs (not gate-scaled)        */
+  size_t total;      /* bytes of the whole buffer                               */
+} ec_saved_layout;
+
+/* Human-readable name of a status code (static string).                      */
+const char *ec_status_string(int status);
+
+/* Detail of the most recent failure on the calling thread ("" if none).      */
+const char *ec_last_error(void);
+
+/* K_tot = sum_g k_g after validating the problem; -1 on an invalid problem.  */
+int64_t ec_total_capacity(const ec_problem *p);
+
+/* Workspace bytes needed by ec_route (mode 0), ec_moe_forward (mode 1) or
+ * ec_moe_backward (mode 2).  0 on an invalid problem (see ec_last_error).    */
+size_t ec_workspace_size(const ec_problem *p, int mode);
+
+/* Layout of the saved buffer; returns an ec_status.                          */
+int ec_saved_layout_of(const ec_problem *p, ec_saved_layout *out /* HOST */);
+
+/* Capacity rule (Section 2.2 with Section 4.2's time-dependent capacity):
+ *   k_g = clamp(rint(L_g * c_g / E), 0, L_g)  (rint: half to even, in double),
+ *   c_g = c_fixed                                if t == NULL,
+ *   c_g = clamp(c_min + (c_max - c_min) s(t_g), c_min, c_max) otherwise.
+ * group_lengths, t and k_out are HOST arrays of length G.  Returns ec_status.  */
+int ec_capacity(int32_t n_groups, const int32_t *group_lengths, int32_t n_experts,
+                double c_fixed, const double *t, double c_min, double c_max,
+                int scheduler, int32_t *k_out);
+
+/* Routing only: the router GEMM + softmax and the per-(group, expert) column
+ * top-k (Section 2.2; tie-break toward the lower token index; Section 5.2's
+ * per-sequence pool).  Used for the retrofit's selection swap (Section 5).
+ *   X  [N, d] dtype, Wg [E, d] dtype (row j = expert j's router vector)
+ *   S  [N, E] fp32 out;  sel_token [E, K] int32 out;
+ *   sel_gate [E, K] fp32 out, may be NULL (= S at the selected entries);
+ *   slot [E, N] int32 out, may be NULL ([j, i] = row of token i in expert j's
+ *   buffer, -1 if not selected).
+ * ws: ec_workspace_size(p, 0) bytes.                                           */
+int ec_route(const ec_problem *p, const void *X, const void *Wg, float *S,
+             int32_t *sel_token, float *sel_gate, int32_t *slot,
+             void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Layer forward: routing, gather, SwiGLU experts as a grouped GEMM, and the
+ * gate-weighted combine (Section 2.2, Appendix E).
+ *   W1, W3 [E, h, d] dtype;  W2 [E, d, h] dtype;  Y [N, d] dtype out.
+ * saved: NULL for inference, else ec_saved_layout.total bytes that receive the
+ * activations the backward needs.  ws: ec_workspace_size(p, 1) bytes.         */
+int ec_moe_forward(const ec_problem *p, const void *X, const void *Wg,
+                   const void *W1, const void *W3, const void *W2, void *Y,
+                   void *saved, size_t saved_bytes,
+                   void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Layer backward: gradients of sum(Y * dY) with the selection held fixed (the
+ * selection is an index set; gradient reaches the router through the gate
+ * values S_ij of the selected pairs and the softmax).
+ *   dY [N, d] dtype;  saved: filled by ec_moe_forward with the same inputs;
+ *   dX [N, d] dtype out;  dWg [E, d] fp32 out;  dW1, dW3 [E, h, d] and
+ *   dW2 [E, d, h] dtype out (overwritten, not accumulated).
+ * ws: ec_workspace_size(p, 2) bytes.                                           */
+int ec_moe_backward(const ec_problem *p, const void *X, const void *Wg,
+                    const void *W1, const void *W3, const void *W2,
+                    const void *dY, const void *saved, size_t saved_bytes,
+                    void *dX, float *dWg, void *dW1, void *dW3, void *dW2,
+                    void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Stage timing for profiling.  After this call, every entry point called on
+ * the same thread records events[0] on its stream before its first kernel and
+ * events[s+1] after stage s, for s < n_events - 1, so that
+ * hipEventElapsedTime(events[s], events[s+1]) is the duration of stage s.
+ * The caller creates and owns the events; pass NULL / 0 to stop recording.
+ * Stages of ec_moe_forward: 0 router+softmax, 1 top-k, 2 gather,
+ *   3 W1/W3 grouped GEMM + SwiGLU, 4 W2 grouped GEMM, 5 combine.
+ * Stages of ec_moe_backward: 0 dY gather + gate gradient, 1 dA grouped GEMM +
+ *   SwiGLU backward, 2 dW2, 3 dXe, 4 dW1/dW3, 5 router dZ, 6 router dX,
+ *   7 combine of dXe, 8 dWg.
+ * Stages of ec_route: 0 router+softmax, 1 top-k.                              */
+int ec_set_stage_events(hipEvent_t *events /* HOST array */, int n_events);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EC_MOE_H */

@@ -293,3 +293,81 @@ def loss_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau, sel_token)
     """sum(Y * dY) with a fixed selection: the scalar whose gradient backward_ref returns."""
     Y = forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau, sel_token)["Y"]
     return float(np.sum(Y * widen(dY)))
+
+
+# ---------------------------------------------------------------------------
+# Restrictions of the definitions above to a few tokens or one expert, for
+# large inputs where the full evaluation is too slow in float64.  Each is
+# checked against forward_ref / backward_ref on small inputs.
+# ---------------------------------------------------------------------------
+
+def forward_rows_ref(X, Wg, W1, W3, W2, sel_token, rows, inv_tau: float = 1.0) -> np.ndarray:
+    """y_i for the listed tokens only, with the selection given."""
+    rows = np.asarray(rows, dtype=np.int64)
+    slot = slot_ref(np.asarray(sel_token), np.asarray(X).shape[0])[rows]
+    Xr = widen(np.asarray(X)[rows])
+    S = softmax_ref(Xr @ widen(Wg).T, inv_tau)
+    Y = np.zeros_like(Xr)
+    for j in range(S.shape[1]):
+        q = np.nonzero(slot[:, j] >= 0)[0]          # listed tokens that expert j selected
+        if len(q):
+            Y[q] += S[q, j][:, None] * swiglu_ffn_ref(Xr[q], W1[j], W3[j], W2[j])
+    return Y
+
+
+def _pair_terms(x, W1j, W3j, W2j):
+    """H1, H3, sigmoid(H1), A and O for rows x of one expert."""
+    h1 = x @ widen(W1j).T
+    h3 = x @ widen(W3j).T
+    sg = 1.0 / (1.0 + np.exp(-h1))
+    a = h1 * sg * h3
+    return h1, h3, sg, a, a @ widen(W2j).T
+
+
+def backward_rows_ref(X, Wg, W1, W3, W2, dY, sel_token, rows, inv_tau: float = 1.0) -> np.ndarray:
+    """dX_i for the listed tokens only (expert and router terms), selection given."""
+    rows = np.asarray(rows, dtype=np.int64)
+    slot = slot_ref(np.asarray(sel_token), np.asarray(X).shape[0])[rows]
+    Xr, dYr, Wgf = widen(np.asarray(X)[rows]), widen(np.asarray(dY)[rows]), widen(Wg)
+    S = softmax_ref(Xr @ Wgf.T, inv_tau)
+    dX = np.zeros_like(Xr)
+    dS = np.zeros_like(S)
+    for j in range(S.shape[1]):
+        q = np.nonzero(slot[:, j] >= 0)[0]
+        if not len(q):
+            continue
+        h1, h3, sg, a, o = _pair_terms(Xr[q], W1[j], W3[j], W2[j])
+        dS[q, j] = np.sum(dYr[q] * o, axis=1)
+        da = (S[q, j][:, None] * dYr[q]) @ widen(W2[j])
+        dh3 = da * (h1 * sg)
+        dh1 = da * h3 * (sg * (1.0 + h1 * (1.0 - sg)))
+        dX[q] += dh1 @ widen(W1[j]) + dh3 @ widen(W3[j])
+    dZ = S * (dS - np.sum(S * dS, axis=1, keepdims=True)) * float(inv_tau)
+    return dX + dZ @ Wgf
+
+
+def expert_grads_ref(X, Wg, W1, W3, W2, dY, sel_token, j: int, inv_tau: float = 1.0):
+    """(dW1_j, dW3_j, dW2_j) of one expert, selection given."""
+    rows = np.asarray(sel_token)[j]
+    x = widen(np.asarray(X)[rows])
+    g = softmax_ref(x @ widen(Wg).T, inv_tau)[:, j]
+    h1, h3, sg, a, o = _pair_terms(x, W1[j], W3[j], W2[j])
+    do = g[:, None] * widen(np.asarray(dY)[rows])
+    da = do @ widen(W2[j])
+    dh3 = da * (h1 * sg)
+    dh1 = da * h3 * (sg * (1.0 + h1 * (1.0 - sg)))
+    return dh1.T @ x, dh3.T @ x, do.T @ a
+
+
+def router_grad_ref(X, Wg, W1, W3, W2, dY, sel_token, inv_tau: float = 1.0) -> np.ndarray:
+    """dWg [E, d] with the selection given (needs every selected pair's output)."""
+    Xf, dYf = widen(X), widen(dY)
+    S = router_ref(X, Wg, inv_tau)
+    sel = np.asarray(sel_token)
+    dS = np.zeros_like(S)
+    for j in range(S.shape[1]):
+        rows = sel[j]
+        o = _pair_terms(Xf[rows], W1[j], W3[j], W2[j])[4]
+        dS[rows, j] = np.sum(dYf[rows] * o, axis=1)
+    dZ = S * (dS - np.sum(S * dS, axis=1, keepdims=True)) * float(inv_tau)
+    return dZ.T @ Xf

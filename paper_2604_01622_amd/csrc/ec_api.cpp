@@ -1,0 +1,464 @@
+// Host side of the C interface declared in include/ec_moe.h: argument
+// validation, the capacity rule, the layout of the saved activations and of
+// the workspace, and the launch sequence of each entry point on the caller's
+// stream.  Nothing here allocates device memory or synchronises.
+#include "../../include/ec_moe.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "ec_kernels.h"
+
+
+namespace {
+
+thread_local std::string g_last_error;
+thread_local hipEvent_t* g_events = nullptr;  // stage timing (ec_set_stage_events)
+thread_local int g_n_events = 0;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Plan {
+  int N = 0, d = 0, E = 0, h = 0, G = 0, EP = 0;
+  long K = 0;          // K_tot
+  int dtype = 0;
+  size_t esz = 0;      // storage bytes per element
+};
+
+int validate(const ec_problem* p, Plan* out) {
+  g_last_error.clear();
+  if (!p) return fail(EC_ERR_ARG, "problem is NULL");
+  if (p->dtype != EC_F32 && p->dtype != EC_BF16)
+    return fail(EC_ERR_DTYPE, "unknown dtype %d", (int)p->dtype);
+  if (p->n_groups < 1) return fail(EC_ERR_SHAPE, "n_groups must be >= 1 (got %d)", p->n_groups);
+  if (!p->group_offsets || !p->capacity)
+    return fail(EC_ERR_ARG, "group_offsets and capacity must be host arrays");
+  if (p->n_experts < 1 || p->n_experts > 256)
+    return fail(EC_ERR_SHAPE, "n_experts must be in [1, 256] (got %d)", p->n_experts);
+  if (p->d_model < 64 || p->d_model > 16384 || p->d_model % 64)
+    return fail(EC_ERR_SHAPE, "d_model must be a multiple of 64 in [64, 16384] (got %d)",
+                p->d_model);
+  if (p->d_ff < 64 || p->d_ff > 16384 || p->d_ff % 64)
+    return fail(EC_ERR_SHAPE, "d_ff must be a multiple of 64 in [64, 16384] (got %d)", p->d_ff);
+  if (!std::isfinite(p->inv_temperature) || !(p->inv_temperature > 0.f))
+    return fail(EC_ERR_ARG, "inv_temperature must be finite and > 0");
+  if (p->n_tokens < 0 || p->n_tokens >= (int64_t)1 << 31)
+    return fail(EC_ERR_SHAPE, "n_tokens out of range");
+  const int32_t* off = p->group_offsets;
+  if (off[0] != 0) return fail(EC_ERR_SHAPE, "group_offsets[0] must be 0");
+  long K = 0;
+  for (int g = 0; g < p->n_groups; ++g) {
+    if (off[g + 1] < off[g]) return fail(EC_ERR_SHAPE, "group_offsets must be non-decreasing");
+    const int L = off[g + 1] - off[g];
+    const int k = p->capacity[g];
+    if (k < 0 || k > L)
+      return fail(EC_ERR_CAPACITY, "capacity[%d] = %d outside [0, %d]", g, k, L);
+    K += k;
+  }
+  if ((int64_t)off[p->n_groups] != p->n_tokens)
+    return fail(EC_ERR_SHAPE, "group_offsets[G] = %d != n_tokens = %lld", off[p->n_groups],
+                (long long)p->n_tokens);
+  const int64_t maxw = p->d_model > p->d_ff ? p->d_model : p->d_ff;
+  if ((int64_t)p->n_experts * K * 2 * maxw >= ((int64_t)1 << 31) ||
+      (int64_t)p->n_experts * p->n_tokens >= ((int64_t)1 << 31))
+    return fail(EC_ERR_SHAPE, "problem too large for 32-bit element indices");
+  Plan& P = *out;
+  P.N = (int)p->n_tokens;
+  P.d = p->d_model;
+  P.E = p->n_experts;
+  P.h = p->d_ff;
+  P.G = p->n_groups;
+  P.K = K;
+  P.EP = (P.E + 63) / 64 * 64;
+  P.dtype = p->dtype;
+  P.esz = p->dtype == EC_F32 ? 4 : 2;
+  return EC_OK;
+}
+
+// Sub-allocator over a caller buffer; with base == nullptr it only measures.
+struct Carve {
+  char* base;
+  size_t used = 0;
+  explicit Carve(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    void* r = base ? base + used : nullptr;
+    used += align_up(bytes);
+    return r;
+  }
+};
+
+struct Saved {
+  float* S;
+  int32_t* sel;
+  int32_t* slot;
+  void* Xe;
+  void* H1;
+  void* H3;
+  void* A;
+  void* O;
+};
+
+Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
+  Saved s;
+  s.S = (float*)c.take((size_t)P.N * P.E * 4);
+  s.sel = (int32_t*)c.take((size_t)P.E * P.K * 4);
+  s.slot = (int32_t*)c.take((size_t)P.E * P.N * 4);
+  s.Xe = c.take((size_t)P.E * P.K * P.d * P.esz);
+  s.H1 = with_h ? c.take((size_t)P.E * P.K * P.h * P.esz) : nullptr;
+  s.H3 = with_h ? c.take((size_t)P.E * P.K * P.h * P.esz) : nullptr;
+  s.A = c.take((size_t)P.E * P.K * P.h * P.esz);
+  s.O = c.take((size_t)P.E * P.K * P.d * P.esz);
+  return s;
+}
+
+struct BwdWs {
+  void* dO;       // [E, K, d]; reused for dXe once dO is dead
+  float* dSp;     // [E, K]
+  void* dH;       // [E, K, 2h]
+  float* dZ;      // [N, E]
+  uint16_t* dZb;  // [N, EP] (bf16 only)
+  float* part;    // [splits, E, d]
+  int splits;
+};
+
+BwdWs carve_bwd(Carve& c, const Plan& P) {
+  BwdWs w;
+  w.dO = c.take((size_t)P.E * P.K * P.d * P.esz);
+  w.dSp = (float*)c.take((size_t)P.E * P.K * 4);
+  w.dH = c.take((size_t)P.E * P.K * 2 * P.h * P.esz);
+  w.dZ = (float*)c.take((size_t)P.N * P.E * 4);
+  w.dZb = P.dtype == EC_BF16 ? (uint16_t*)c.take((size_t)P.N * P.EP * 2) : nullptr;
+  w.splits = ec::router_dwg_splits(P.N, P.E, P.d);
+  w.part = (float*)c.take((size_t)w.splits * P.E * P.d * 4);
+  return w;
+}
+
+size_t route_ws(const Plan& P, bool need_slot) {
+  Carve c(nullptr);
+  c.take((size_t)P.E * P.N * 4);                   // ST
+  if (need_slot) c.take((size_t)P.E * P.N * 4);    // slot when the caller passes none
+  return c.used;
+}
+
+size_t forward_ws(const Plan& P) {
+  Carve c(nullptr);
+  c.take((size_t)P.E * P.N * 4);  // ST
+  carve_saved(c, P, false);       // activations when no saved buffer is given
+  return c.used;
+}
+
+size_t backward_ws(const Plan& P) {
+  Carve c(nullptr);
+  carve_bwd(c, P);
+  return c.used;
+}
+
+size_t saved_bytes(const Plan& P) {
+  Carve c(nullptr);
+  carve_saved(c, P, true);
+  return c.used;
+}
+
+int check_ptr(const void* ptr, const char* name, bool optional = false) {
+  if (!ptr) {
+    if (optional) return EC_OK;
+    return fail(EC_ERR_ARG, "%s is NULL", name);
+  }
+  if ((uintptr_t)ptr % 16) return fail(EC_ERR_ALIGN, "%s is not 16-byte aligned", name);
+  return EC_OK;
+}
+
+#define EC_TRY(expr)                           \
+  do {                                         \
+    int _s = (expr);                           \
+    if (_s != EC_OK) return _s;                \
+  } while (0)
+
+#define EC_HIP(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t _e = (expr);                                                            \
+    if (_e != hipSuccess)                                                              \
+      return fail(EC_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(_e));          \
+  } while (0)
+
+// Records stage event `i` (0 = before the first stage) if timing is enabled.
+hipError_t mark(int i, hipStream_t st) {
+  if (g_events && i < g_n_events) return hipEventRecord(g_events[i], st);
+  return hipSuccess;
+}
+
+int enqueue_route(const ec_problem* p, const Plan& P, const void* X, const void* Wg, float* S,
+                  float* ST, int32_t* sel, float* gate, int32_t* slot, hipStream_t st) {
+  EC_HIP(mark(0, st));
+  EC_HIP(ec::launch_router_softmax(P.dtype, X, Wg, S, ST, P.N, P.d, P.E, p->inv_temperature, st));
+  EC_HIP(mark(1, st));
+  ec::GroupTable tab;
+  int seg = 0;
+  for (int g0 = 0; g0 < P.G; g0 += ec::TOPK_MAX_GROUPS) {
+    tab.n = 0;
+    for (int g = g0; g < P.G && g < g0 + ec::TOPK_MAX_GROUPS; ++g) {
+      tab.off[tab.n] = p->group_offsets[g];
+      tab.len[tab.n] = p->group_offsets[g + 1] - p->group_offsets[g];
+      tab.k[tab.n] = p->capacity[g];
+      tab.seg[tab.n] = seg;
+      seg += p->capacity[g];
+      ++tab.n;
+    }
+    EC_HIP(ec::launch_topk(ST, P.N, P.E, (int)P.K, tab, sel, gate, slot, st));
+  }
+  EC_HIP(mark(2, st));
+  return EC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ec_status_string(int status) {
+  switch (status) {
+    case EC_OK: return "EC_OK";
+    case EC_ERR_ARG: return "EC_ERR_ARG: invalid argument";
+    case EC_ERR_SHAPE: return "EC_ERR_SHAPE: invalid or inconsistent sizes";
+    case EC_ERR_CAPACITY: return "EC_ERR_CAPACITY: capacity outside [0, group length]";
+    case EC_ERR_DTYPE: return "EC_ERR_DTYPE: unknown storage dtype";
+    case EC_ERR_ALIGN: return "EC_ERR_ALIGN: device pointer not 16-byte aligned";
+    case EC_ERR_WORKSPACE: return "EC_ERR_WORKSPACE: buffer too small";
+    case EC_ERR_HIP: return "EC_ERR_HIP: HIP runtime error";
+    default: return "unknown ec_status";
+  }
+}
+
+const char* ec_last_error(void) { return g_last_error.c_str(); }
+
+int ec_set_stage_events(hipEvent_t* events, int n_events) {
+  g_last_error.clear();
+  if (n_events < 0 || (n_events > 0 && !events)) return fail(EC_ERR_ARG, "bad event array");
+  g_events = n_events > 0 ? events : nullptr;
+  g_n_events = n_events;
+  return EC_OK;
+}
+
+int64_t ec_total_capacity(const ec_problem* p) {
+  Plan P;
+  if (validate(p, &P) != EC_OK) return -1;
+  return P.K;
+}
+
+size_t ec_workspace_size(const ec_problem* p, int mode) {
+  Plan P;
+  if (validate(p, &P) != EC_OK) return 0;
+  switch (mode) {
+    case 0: return route_ws(P, true);
+    case 1: return forward_ws(P);
+    case 2: return backward_ws(P);
+    default: fail(EC_ERR_ARG, "unknown workspace mode %d", mode); return 0;
+  }
+}
+
+int ec_saved_layout_of(const ec_problem* p, ec_saved_layout* out) {
+  Plan P;
+  EC_TRY(validate(p, &P));
+  if (!out) return fail(EC_ERR_ARG, "out is NULL");
+  // carve an imaginary buffer at address 0 and read the offsets back
+  Carve m(nullptr);
+  size_t offs[8];
+  int n = 0;
+  const size_t sizes[8] = {(size_t)P.N * P.E * 4, (size_t)P.E * P.K * 4, (size_t)P.E * P.N * 4,
+                           (size_t)P.E * P.K * P.d * P.esz, (size_t)P.E * P.K * P.h * P.esz,
+                           (size_t)P.E * P.K * P.h * P.esz, (size_t)P.E * P.K * P.h * P.esz,
+                           (size_t)P.E * P.K * P.d * P.esz};
+  for (size_t b : sizes) {
+    offs[n++] = m.used;
+    m.take(b);
+  }
+  out->S = offs[0];
+  out->sel_token = offs[1];
+  out->slot = offs[2];
+  out->Xe = offs[3];
+  out->H1 = offs[4];
+  out->H3 = offs[5];
+  out->A = offs[6];
+  out->O = offs[7];
+  out->total = m.used;
+  return EC_OK;
+}
+
+int ec_capacity(int32_t n_groups, const int32_t* group_lengths, int32_t n_experts, double c_fixed,
+                const double* t, double c_min, double c_max, int scheduler, int32_t* k_out) {
+  g_last_error.clear();
+  if (n_groups < 0 || !group_lengths || !k_out) return fail(EC_ERR_ARG, "bad arguments");
+  if (n_experts < 1) return fail(EC_ERR_SHAPE, "n_experts must be >= 1");
+  if (t && (scheduler < EC_SCHED_LINEAR || scheduler > EC_SCHED_GAUSSIAN_REV))
+    return fail(EC_ERR_ARG, "unknown scheduler %d", scheduler);
+  if (t && !(c_min <= c_max)) return fail(EC_ERR_ARG, "c_min must be <= c_max");
+  const double pi = 3.14159265358979323846;
+  const double sigma = 0.22;
+  const double g0 = std::exp(-1.0 / (8.0 * sigma * sigma));
+  for (int g = 0; g < n_groups; ++g) {
+    const int L = group_lengths[g];
+    if (L < 0) return fail(EC_ERR_SHAPE, "group length %d < 0", L);
+    double c = c_fixed;
+    if (t) {
+      const double r = t[g];
+      double s;
+      switch (scheduler) {
+        case EC_SCHED_LINEAR: s = r; break;
+        case EC_SCHED_LINEAR_REV: s = 1.0 - r; break;
+        case EC_SCHED_COSINE: s = 0.5 * (1.0 - std::cos(pi * r)); break;
+        case EC_SCHED_COSINE_REV: s = 0.5 * (1.0 + std::cos(pi * r)); break;
+        default: {
+          const double gg = std::exp(-(r - 0.5) * (r - 0.5) / (2.0 * sigma * sigma));
+          const double gt = (gg - g0) / (1.0 - g0);
+          s = scheduler == EC_SCHED_GAUSSIAN ? gt : 1.0 - gt;
+        }
+      }
+      c = c_min + (c_max - c_min) * s;
+      c = c < c_min ? c_min : (c > c_max ? c_max : c);
+    }
+    if (!std::isfinite(c) || c < 0) return fail(EC_ERR_ARG, "capacity factor must be >= 0");
+    double k = std::nearbyint((double)L * c / (double)n_experts);  // ties to even
+    if (k < 0) k = 0;
+    if (k > L) k = L;
+    k_out[g] = (int32_t)k;
+  }
+  return EC_OK;
+}
+
+int ec_route(const ec_problem* p, const void* X, const void* Wg, float* S, int32_t* sel_token,
+             float* sel_gate, int32_t* slot, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Plan P;
+  EC_TRY(validate(p, &P));
+  EC_TRY(check_ptr(X, "X"));
+  EC_TRY(check_ptr(Wg, "Wg"));
+  EC_TRY(check_ptr(S, "S"));
+  EC_TRY(check_ptr(sel_token, "sel_token", P.K == 0));
+  EC_TRY(check_ptr(sel_gate, "sel_gate", true));
+  EC_TRY(check_ptr(slot, "slot", true));
+  const size_t need = route_ws(P, slot == nullptr);
+  EC_TRY(check_ptr(ws, "workspace", need == 0));
+  if (ws_bytes < need)
+    return fail(EC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+  if (P.N == 0) return EC_OK;
+  Carve c(ws);
+  float* ST = (float*)c.take((size_t)P.E * P.N * 4);
+  int32_t* sl = slot ? slot : (int32_t*)c.take((size_t)P.E * P.N * 4);
+  return enqueue_route(p, P, X, Wg, S, ST, sel_token, sel_gate, sl, stream);
+}
+
+int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const void* W1,
+                   const void* W3, const void* W2, void* Y, void* saved, size_t saved_bytes_in,
+                   void* ws, size_t ws_bytes, hipStream_t stream) {
+  Plan P;
+  EC_TRY(validate(p, &P));
+  EC_TRY(check_ptr(X, "X"));
+  EC_TRY(check_ptr(Wg, "Wg"));
+  EC_TRY(check_ptr(W1, "W1"));
+  EC_TRY(check_ptr(W3, "W3"));
+  EC_TRY(check_ptr(W2, "W2"));
+  EC_TRY(check_ptr(Y, "Y"));
+  EC_TRY(check_ptr(saved, "saved", true));
+  if (saved && saved_bytes_in < saved_bytes(P))
+    return fail(EC_ERR_WORKSPACE, "saved buffer %zu bytes < %zu required", saved_bytes_in,
+                saved_bytes(P));
+  const size_t need = forward_ws(P);
+  EC_TRY(check_ptr(ws, "workspace"));
+  if (ws_bytes < need)
+    return fail(EC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+  if (P.N == 0) return EC_OK;
+
+  Carve c(ws);
+  float* ST = (float*)c.take((size_t)P.E * P.N * 4);
+  Saved s;
+  if (saved) {
+    Carve cs(saved);
+    s = carve_saved(cs, P, true);
+  } else {
+    s = carve_saved(c, P, false);
+  }
+  EC_TRY(enqueue_route(p, P, X, Wg, s.S, ST, s.sel, nullptr, s.slot, stream));
+  const int M = (int)P.K;
+  EC_HIP(ec::launch_gather(P.dtype, X, s.sel, s.Xe, (long)P.E * M, P.d, P.N, stream));
+  EC_HIP(mark(3, stream));
+  EC_HIP(ec::launch_gemm_w13(P.dtype, s.Xe, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream));
+  EC_HIP(mark(4, stream));
+  EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream));
+  EC_HIP(mark(5, stream));
+  EC_HIP(ec::launch_combine(P.dtype, s.O, s.S, s.slot, Y, P.N, P.E, M, P.d, stream));
+  EC_HIP(mark(6, stream));
+  return EC_OK;
+}
+
+int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const void* W1,
+                    const void* W3, const void* W2, const void* dY, const void* saved,
+                    size_t saved_bytes_in, void* dX, float* dWg, void* dW1, void* dW3, void* dW2,
+                    void* ws, size_t ws_bytes, hipStream_t stream) {
+  Plan P;
+  EC_TRY(validate(p, &P));
+  EC_TRY(check_ptr(X, "X"));
+  EC_TRY(check_ptr(Wg, "Wg"));
+  EC_TRY(check_ptr(W1, "W1"));
+  EC_TRY(check_ptr(W3, "W3"));
+  EC_TRY(check_ptr(W2, "W2"));
+  EC_TRY(check_ptr(dY, "dY"));
+  EC_TRY(check_ptr(saved, "saved"));
+  EC_TRY(check_ptr(dX, "dX"));
+  EC_TRY(check_ptr(dWg, "dWg"));
+  EC_TRY(check_ptr(dW1, "dW1"));
+  EC_TRY(check_ptr(dW3, "dW3"));
+  EC_TRY(check_ptr(dW2, "dW2"));
+  if (saved_bytes_in < saved_bytes(P))
+    return fail(EC_ERR_WORKSPACE, "saved buffer %zu bytes < %zu required", saved_bytes_in,
+                saved_bytes(P));
+  const size_t need = backward_ws(P);
+  EC_TRY(check_ptr(ws, "workspace"));
+  if (ws_bytes < need)
+    return fail(EC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+
+  Carve cs((void*)saved);
+  const Saved s = carve_saved(cs, P, true);
+  Carve c(ws);
+  const BwdWs w = carve_bwd(c, P);
+  const int M = (int)P.K;
+  const int E = P.E, d = P.d, h = P.h, N = P.N;
+  void* dXe = w.dO;  // dO is dead once dW2 is formed
+  EC_HIP(mark(0, stream));
+  EC_HIP(ec::launch_bwd_gather(P.dtype, dY, s.O, s.S, s.sel, w.dO, w.dSp, N, E, M, d, stream));
+  EC_HIP(mark(1, stream));
+  EC_HIP(ec::launch_gemm_dA(P.dtype, w.dO, W2, s.H1, s.H3, w.dH, E, M, d, h, stream));
+  EC_HIP(mark(2, stream));
+  EC_HIP(ec::launch_gemm_dW2(P.dtype, w.dO, s.A, dW2, E, M, d, h, stream));
+  EC_HIP(mark(3, stream));
+  EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream));
+  EC_HIP(mark(4, stream));
+  EC_HIP(ec::launch_gemm_dW13(P.dtype, w.dH, s.Xe, dW1, dW3, E, M, d, h, stream));
+  EC_HIP(mark(5, stream));
+  EC_HIP(ec::launch_router_dz(s.S, w.dSp, s.slot, w.dZ, w.dZb, N, E, P.EP, M,
+                              p->inv_temperature, stream));
+  EC_HIP(mark(6, stream));
+  const void* dZop = P.dtype == EC_BF16 ? (const void*)w.dZb : (const void*)w.dZ;
+  EC_HIP(ec::launch_router_dx(P.dtype, dZop, Wg, dX, N, E, P.EP, d, stream));
+  EC_HIP(mark(7, stream));
+  EC_HIP(ec::launch_bwd_combine(P.dtype, dXe, s.slot, dX, dX, N, E, M, d, stream));
+  EC_HIP(mark(8, stream));
+  EC_HIP(ec::launch_router_dwg(P.dtype, dZop, X, dWg, w.part, w.splits, N, E, P.EP, d, stream));
+  EC_HIP(mark(9, stream));
+  return EC_OK;
+}
+
+}  // extern "C"

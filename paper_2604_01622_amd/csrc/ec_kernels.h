@@ -1,0 +1,90 @@
+// Internal launchers of the expert-choice MoE kernels.  Each returns the
+// hipError_t of its launch(es); all work goes on the given stream.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ec {
+
+enum { DT_F32 = 0, DT_BF16 = 1 };
+
+// Groups handled by one top-k launch (the table travels as a kernel argument).
+constexpr int TOPK_MAX_GROUPS = 128;
+
+struct GroupTable {
+  int n;                            // groups in this launch
+  int off[TOPK_MAX_GROUPS];         // first token of the group
+  int len[TOPK_MAX_GROUPS];         // tokens in the group
+  int k[TOPK_MAX_GROUPS];           // tokens each expert takes from the group
+  int seg[TOPK_MAX_GROUPS];         // first row of the group's segment in an expert buffer
+};
+
+// S [N,E] and ST [E,N] fp32 from X [N,d] and Wg [E,d].
+hipError_t launch_router_softmax(int dtype, const void* X, const void* Wg, float* S, float* ST,
+                                 int N, int d, int E, float inv_tau, hipStream_t st);
+
+// Column top-k of ST per (group, expert): sel_token/sel_gate [E,K], slotT [E,N].
+hipError_t launch_topk(const float* ST, int N, int E, int K, const GroupTable& tab,
+                       int32_t* sel_token, float* sel_gate, int32_t* slotT, hipStream_t st);
+
+// Xe[r, :] = X[sel_token[r], :] for all E*K rows.
+hipError_t launch_gather(int dtype, const void* X, const int32_t* sel_token, void* Xe,
+                         long rows, int d, int N, hipStream_t st);
+
+// Y[i, :] = sum_j S[i,j] O[j, slotT[j,i], :] over experts j with slotT[j,i] >= 0.
+hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_t* slotT,
+                          void* Y, int N, int E, int K, int d, hipStream_t st);
+
+// Backward gather: dO[j,r,:] = S[i,j] dY[i,:] and dS[i,j] = <dY[i,:], O[j,r,:]>,
+// i = sel_token[j,r]; dS [N,E] fp32 is zero for unselected pairs.
+hipError_t launch_bwd_gather(int dtype, const void* dY, const void* O, const float* S,
+                             const int32_t* sel_token, void* dO, float* dS, int N, int E, int K,
+                             int d, hipStream_t st);
+
+// Backward combine: dX[i,:] = Xr[i,:] + sum_j dXe[j, slotT[j,i], :]  (Xr may alias dX).
+hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, const void* Xr,
+                              void* dX, int N, int E, int K, int d, hipStream_t st);
+
+// Router backward, part 1: dZ = S * (dS - <S, dS>) / tau  [N,E] fp32, with
+// dS_ij = dSp[j, slot_ij] on the selection and 0 elsewhere; dZb (optional) is a
+// bf16 copy [N, EP] with zero columns E..EP-1.
+hipError_t launch_router_dz(const float* S, const float* dSp, const int32_t* slotT, float* dZ,
+                            uint16_t* dZb, int N, int E, int EP, int K, float inv_tau,
+                            hipStream_t st);
+
+// Router backward, part 2: dX = dZ Wg  (bf16: dZ is the padded bf16 copy).
+hipError_t launch_router_dx(int dtype, const void* dZ, const void* Wg, void* dX, int N, int E,
+                            int EP, int d, hipStream_t st);
+
+// Router backward, part 3: dWg [E,d] fp32 = dZ^T X, split over the tokens into
+// `splits` partial sums (part [splits,E,d] fp32) added in a fixed order.
+hipError_t launch_router_dwg(int dtype, const void* dZ, const void* X, float* dWg, float* part,
+                             int splits, int N, int E, int EP, int d, hipStream_t st);
+int router_dwg_splits(int N, int E, int d);
+
+// ---- grouped GEMMs over E experts (M = K rows per expert) ----
+
+// H = Xe W1^T, Xe W3^T -> A = SiLU(H1) * H3 (and H1, H3 if non-null).
+hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
+                           void* H1, void* H3, int E, int M, int d, int h, hipStream_t st);
+// O = A W2^T.
+hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
+                          int h, hipStream_t st);
+// dA = dO W2 and the SwiGLU backward: dH[:, 0:h] = dH1, dH[:, h:2h] = dH3 ([E,M,2h]).
+hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
+                          const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st);
+// dXe = dH1 W1 + dH3 W3  ([E,M,d]).
+hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
+                           int E, int M, int d, int h, hipStream_t st);
+// dW2 = dO^T A  ([E,d,h]).
+hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
+                           int d, int h, hipStream_t st);
+// dW1 = dH1^T Xe, dW3 = dH3^T Xe  ([E,h,d] each).
+hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1, void* dW3,
+                            int E, int M, int d, int h, hipStream_t st);
+
+// Fill n int32/fp32/bytes with zero (a kernel, not a memset node).
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);
+
+}  // namespace ec

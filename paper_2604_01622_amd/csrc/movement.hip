@@ -1,0 +1,289 @@
+// Bandwidth-bound stages of the layer: the gather of selected tokens into
+// expert-contiguous buffers, the gate-weighted combine (Section 2.2,
+// y_i = sum_j g_ij FFN_j(x_i) with g_ij = S_ij), and their backward
+// counterparts.  No floating-point atomics: every output row is produced by
+// one wave that sums its expert contributions in ascending expert order.
+#include "ec_common.h"
+#include "ec_kernels.h"
+
+namespace ec {
+
+namespace {
+
+// ---------------------------------------------------------------- gather
+// One wave per expert row; 16-byte vectors, all loads of a row issued before
+// its stores.
+template <int U>
+__global__ __launch_bounds__(256) void gather_kernel(const uint4* __restrict__ X,
+                                                     const int32_t* __restrict__ sel,
+                                                     uint4* __restrict__ Xe, long rows, int vpr,
+                                                     int N) {
+  const int lane = threadIdx.x & 63;
+  const long r = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const int i = sel[r];
+  if ((unsigned)i >= (unsigned)N) return;  // never for a valid selection
+  const uint4* src = X + (size_t)i * vpr;
+  uint4* dst = Xe + (size_t)r * vpr;
+  for (int v0 = 0; v0 < vpr; v0 += 64 * U) {
+    uint4 t[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = v0 + u * 64 + lane;
+      if (v < vpr) t[u] = src[v];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = v0 + u * 64 + lane;
+      if (v < vpr) dst[v] = t[u];
+    }
+  }
+}
+
+// ---------------------------------------------------------------- combine
+constexpr int CB_TOK = 16;   // tokens per workgroup (4 per wave)
+constexpr int CB_Q = 4;      // 8-element chunks per lane per column block
+constexpr int CB_MAXE = 256;
+
+// Builds, for one token, the ascending list of (expert, row, gate) it was
+// selected by; returns the list length.  list is wave-private LDS.
+__device__ __forceinline__ int token_expert_list(const int32_t* sslot, const float* sgate,
+                                                 int t, int E, int K, int2* list, float* lgate) {
+  const int lane = threadIdx.x & 63;
+  int n = 0;
+  for (int j0 = 0; j0 < E; j0 += 64) {
+    const int j = j0 + lane;
+    int r = (j < E) ? sslot[j * CB_TOK + t] : -1;
+    r = (r < K) ? r : -1;  // never for a valid selection
+    const uint64_t m = __ballot(r >= 0);
+    const int before = __popcll(m & ((1ull << lane) - 1ull));
+    if (r >= 0) {
+      list[n + before] = make_int2(j, r);
+      lgate[n + before] = sgate ? sgate[t * CB_MAXE + j] : 1.0f;
+    }
+    n += __popcll(m);
+  }
+  __builtin_amdgcn_wave_barrier();
+  return n;
+}
+
+// Y[i] = (Xr[i] if Xr) + sum_j g_ij Src[j, slot_ij]; with S == nullptr the
+// gates are 1 (backward combine of dXe).
+template <typename T>
+__global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
+                                                      const float* __restrict__ S,
+                                                      const int32_t* __restrict__ slotT,
+                                                      const T* Xr, T* Y, int N, int E, int K,
+                                                      int d) {
+  __shared__ int32_t sslot[CB_MAXE * CB_TOK];
+  __shared__ float sgate[CB_TOK * CB_MAXE];
+  __shared__ int2 slist[4][CB_MAXE];
+  __shared__ float sglist[4][CB_MAXE];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i0 = blockIdx.x * CB_TOK;
+  for (int c = tid; c < E * CB_TOK; c += 256) {
+    const int j = c / CB_TOK, t = c % CB_TOK;
+    sslot[c] = (i0 + t < N) ? slotT[(size_t)j * N + i0 + t] : -1;
+  }
+  if (S) {
+    for (int c = tid; c < CB_TOK * E; c += 256) {
+      const int t = c / E, j = c % E;
+      sgate[t * CB_MAXE + j] = (i0 + t < N) ? S[(size_t)(i0 + t) * E + j] : 0.f;
+    }
+  }
+  __syncthreads();
+  const int nch = d >> 3;
+  for (int t = wave; t < CB_TOK; t += 4) {
+    const int i = i0 + t;
+    if (i >= N) break;
+    const int n = token_expert_list(sslot, S ? sgate : nullptr, t, E, K, slist[wave],
+                                      sglist[wave]);
+    for (int c0 = 0; c0 < nch; c0 += 64 * CB_Q) {
+      float acc[CB_Q][8];
+#pragma unroll
+      for (int q = 0; q < CB_Q; ++q) {
+        const int c = c0 + q * 64 + lane;
+        if (Xr && c < nch) {
+          Elem<T>::load8(Xr + (size_t)i * d + c * 8, acc[q]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
+        }
+      }
+      for (int p = 0; p < n; ++p) {
+        const int2 jr = slist[wave][p];
+        const float g = sglist[wave][p];
+        const T* src = Src + ((size_t)jr.x * K + jr.y) * d;
+        float v[CB_Q][8];
+#pragma unroll
+        for (int q = 0; q < CB_Q; ++q) {
+          const int c = c0 + q * 64 + lane;
+          if (c < nch) Elem<T>::load8(src + c * 8, v[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < CB_Q; ++q) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[q][e] = fmaf(g, v[q][e], acc[q][e]);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < CB_Q; ++q) {
+        const int c = c0 + q * 64 + lane;
+        if (c < nch) Elem<T>::store8(Y + (size_t)i * d + c * 8, acc[q]);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// ---------------------------------------------------------------- backward gather
+// One wave per expert row (j, r), token i = sel[j, r]:
+//   dO[j, r] = S[i, j] dY[i],  dSp[j, r] = <dY[i], O[j, r]>.
+template <typename T>
+__global__ __launch_bounds__(256) void bwd_gather_kernel(const T* __restrict__ dY,
+                                                         const T* __restrict__ O,
+                                                         const float* __restrict__ S,
+                                                         const int32_t* __restrict__ sel,
+                                                         T* __restrict__ dO,
+                                                         float* __restrict__ dSp, int N, int E,
+                                                         int K, int d) {
+  const int lane = threadIdx.x & 63;
+  const long r = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const long rows = (long)E * K;
+  if (r >= rows) return;
+  const int j = (int)(r / K);
+  const int i = sel[r];
+  if ((unsigned)i >= (unsigned)N) return;  // never for a valid selection
+  const float g = S[(size_t)i * E + j];
+  const T* y = dY + (size_t)i * d;
+  const T* o = O + (size_t)r * d;
+  T* out = dO + (size_t)r * d;
+  const int nch = d >> 3;
+  float dot = 0.f;
+  for (int c = lane; c < nch; c += 64) {
+    float vy[8], vo[8];
+    Elem<T>::load8(y + c * 8, vy);
+    Elem<T>::load8(o + c * 8, vo);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      dot = fmaf(vy[e], vo[e], dot);
+      vy[e] *= g;
+    }
+    Elem<T>::store8(out + c * 8, vy);
+  }
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) dot += __shfl_xor(dot, s, 64);
+  if (lane == 0) dSp[r] = dot;
+}
+
+// ---------------------------------------------------------------- router dZ
+// dZ[i, :] = S_i * (dS_i - <S_i, dS_i>) / tau with dS_ij = dSp[j, slot_ij] on
+// the selection and 0 elsewhere.  Writes fp32 dZ [N, E] and, if dZb is given,
+// a bf16 copy [N, EP] whose columns E..EP-1 are zero.
+__global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict__ S,
+                                                        const float* __restrict__ dSp,
+                                                        const int32_t* __restrict__ slotT,
+                                                        float* __restrict__ dZ,
+                                                        bf16_t* __restrict__ dZb, int N, int E,
+                                                        int EP, int K, float inv_tau) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= N) return;
+  const float* s = S + (size_t)i * E;
+  float dot = 0.f;
+  for (int j = 0; j < E; ++j) {
+    const int r = slotT[(size_t)j * N + i];
+    const float ds = (r >= 0 && r < K) ? dSp[(size_t)j * K + r] : 0.f;
+    dot = fmaf(s[j], ds, dot);
+  }
+  for (int j = 0; j < EP; ++j) {
+    float z = 0.f;
+    if (j < E) {
+      const int r = slotT[(size_t)j * N + i];
+      const float ds = (r >= 0 && r < K) ? dSp[(size_t)j * K + r] : 0.f;
+      z = s[j] * (ds - dot) * inv_tau;
+      dZ[(size_t)i * E + j] = z;
+    }
+    if (dZb) dZb[(size_t)i * EP + j] = (bf16_t)f32_to_bf16(z);
+  }
+}
+
+__global__ void zero_kernel(uint4* p, size_t n16, unsigned char* tail, size_t ntail) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+    p[i] = make_uint4(0, 0, 0, 0);
+  if (blockIdx.x == 0 && threadIdx.x < ntail) tail[threadIdx.x] = 0;
+}
+
+}  // namespace
+
+hipError_t launch_gather(int dtype, const void* X, const int32_t* sel_token, void* Xe, long rows,
+                         int d, int N, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  const int vpr = d * (dtype == DT_F32 ? 4 : 2) / 16;
+  const long grid = (rows + 3) / 4;
+  gather_kernel<4><<<dim3((unsigned)grid), 256, 0, st>>>((const uint4*)X, sel_token, (uint4*)Xe,
+                                                         rows, vpr, N);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_t* slotT, void* Y,
+                          int N, int E, int K, int d, hipStream_t st) {
+  if (N == 0) return hipSuccess;
+  const int grid = (N + CB_TOK - 1) / CB_TOK;
+  if (dtype == DT_F32)
+    combine_kernel<float><<<grid, 256, 0, st>>>((const float*)O, S, slotT, nullptr, (float*)Y, N,
+                                                E, K, d);
+  else
+    combine_kernel<bf16_t><<<grid, 256, 0, st>>>((const bf16_t*)O, S, slotT, nullptr, (bf16_t*)Y,
+                                                 N, E, K, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, const void* Xr,
+                              void* dX, int N, int E, int K, int d, hipStream_t st) {
+  if (N == 0) return hipSuccess;
+  const int grid = (N + CB_TOK - 1) / CB_TOK;
+  if (dtype == DT_F32)
+    combine_kernel<float><<<grid, 256, 0, st>>>((const float*)dXe, nullptr, slotT,
+                                                (const float*)Xr, (float*)dX, N, E, K, d);
+  else
+    combine_kernel<bf16_t><<<grid, 256, 0, st>>>((const bf16_t*)dXe, nullptr, slotT,
+                                                 (const bf16_t*)Xr, (bf16_t*)dX, N, E, K, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_gather(int dtype, const void* dY, const void* O, const float* S,
+                             const int32_t* sel_token, void* dO, float* dSp, int N, int E, int K,
+                             int d, hipStream_t st) {
+  const long rows = (long)E * K;
+  if (rows == 0) return hipSuccess;
+  const long grid = (rows + 3) / 4;
+  if (dtype == DT_F32)
+    bwd_gather_kernel<float><<<dim3((unsigned)grid), 256, 0, st>>>(
+        (const float*)dY, (const float*)O, S, sel_token, (float*)dO, dSp, N, E, K, d);
+  else
+    bwd_gather_kernel<bf16_t><<<dim3((unsigned)grid), 256, 0, st>>>(
+        (const bf16_t*)dY, (const bf16_t*)O, S, sel_token, (bf16_t*)dO, dSp, N, E, K, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_router_dz(const float* S, const float* dSp, const int32_t* slotT, float* dZ,
+                            bf16_t* dZb, int N, int E, int EP, int K, float inv_tau,
+                            hipStream_t st) {
+  if (N == 0) return hipSuccess;
+  router_dz_kernel<<<(N + 255) / 256, 256, 0, st>>>(S, dSp, slotT, dZ, dZb, N, E, EP, K, inv_tau);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return hipSuccess;
+  const size_t n16 = bytes / 16;
+  const size_t ntail = bytes - n16 * 16;
+  size_t blocks = (n16 + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks == 0) blocks = 1;
+  zero_kernel<<<(unsigned)blocks, 256, 0, st>>>((uint4*)p, n16, (unsigned char*)p + n16 * 16, ntail);
+  return hipGetLastError();
+}
+
+}  // namespace ec

@@ -1,0 +1,124 @@
+"""Host-side checks of the C interface (no GPU needed): the library loads and
+exports every function the header declares, argument validation rejects bad
+calls before anything is enqueued, and the host capacity rule agrees with the
+oracle's."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import ec_ref as ref
+import paper_2604_01622_amd as ec
+from paper_2604_01622_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ec_moe.h")
+
+EC_OK, EC_ERR_ARG, EC_ERR_SHAPE, EC_ERR_CAPACITY, EC_ERR_DTYPE, EC_ERR_ALIGN, EC_ERR_WORKSPACE = range(7)
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ec_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    L = ec.lib()
+    names = header_functions()
+    assert set(names) == set(binding.EXPORTS), names
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.ec_status_string(EC_ERR_CAPACITY).decode().startswith("EC_ERR_CAPACITY")
+
+
+def _problem(**kw):
+    args = dict(n_tokens=256, d_model=128, n_experts=8, d_ff=64, group_offsets=[0, 100, 256],
+                capacity=[10, 20], inv_temperature=1.0, dtype=torch.bfloat16)
+    args.update(kw)
+    return binding.Problem(**args)
+
+
+FAKE = ctypes.c_void_p(1 << 20)       # aligned, never dereferenced: validation fails first
+MISALIGNED = ctypes.c_void_p((1 << 20) + 8)
+
+
+def _route(P, X=FAKE, ws_bytes=1 << 30):
+    L = ec.lib()
+    return L.ec_route(P.ref, X, FAKE, FAKE, FAKE, None, None, FAKE, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(capacity=[101, 20]), EC_ERR_CAPACITY),
+    (dict(capacity=[-1, 20]), EC_ERR_CAPACITY),
+    (dict(n_tokens=255), EC_ERR_SHAPE),                       # N != off[G]
+    (dict(group_offsets=[0, 300, 256]), EC_ERR_SHAPE),        # decreasing offsets
+    (dict(group_offsets=[1, 100, 256]), EC_ERR_SHAPE),
+    (dict(d_model=100), EC_ERR_SHAPE),
+    (dict(d_ff=32), EC_ERR_SHAPE),
+    (dict(n_experts=0), EC_ERR_SHAPE),
+    (dict(n_experts=257), EC_ERR_SHAPE),
+    (dict(inv_temperature=0.0), EC_ERR_ARG),
+    (dict(inv_temperature=float("nan")), EC_ERR_ARG),
+])
+def test_invalid_problems_rejected(kw, status):
+    P = _problem(**kw)
+    assert _route(P) == status
+    assert ec.lib().ec_last_error().decode() != ""
+    assert ec.lib().ec_workspace_size(P.ref, 1) == 0
+    assert ec.lib().ec_total_capacity(P.ref) == -1
+
+
+def test_bad_dtype_and_pointers():
+    P = _problem()
+    P.c.dtype = 7
+    assert _route(P) == EC_ERR_DTYPE
+    P = _problem()
+    assert _route(P, X=None) == EC_ERR_ARG
+    assert _route(P, X=MISALIGNED) == EC_ERR_ALIGN
+    assert _route(P, ws_bytes=16) == EC_ERR_WORKSPACE
+    L = ec.lib()
+    # forward: saved buffer too small, workspace too small
+    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 1 << 40, None)
+    assert st == EC_ERR_WORKSPACE
+    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, FAKE, 64, None)
+    assert st == EC_ERR_WORKSPACE
+    # backward needs the saved buffer
+    st = L.ec_moe_backward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, FAKE, FAKE, FAKE,
+                           FAKE, FAKE, FAKE, 1 << 40, None)
+    assert st == EC_ERR_ARG
+    assert L.ec_workspace_size(P.ref, 9) == 0
+
+
+def test_workspace_and_saved_layout():
+    P = _problem()
+    assert P.K == 30
+    lay = P.saved_layout()
+    order = ["S", "sel_token", "slot", "Xe", "H1", "H3", "A", "O", "total"]
+    offs = [lay[k] for k in order]
+    assert offs == sorted(offs) and all(o % 256 == 0 for o in offs)
+    N, E, K, d, h = 256, 8, 30, 128, 64
+    assert lay["sel_token"] - lay["S"] >= N * E * 4
+    assert lay["Xe"] - lay["slot"] >= E * N * 4
+    assert lay["H1"] - lay["Xe"] >= E * K * d * 2
+    assert lay["total"] - lay["O"] >= E * K * d * 2
+    for mode in (0, 1, 2):
+        assert P.workspace_size(mode) > 0
+
+
+@pytest.mark.parametrize("sched", list(binding.SCHEDULERS))
+def test_capacity_rule_matches_oracle(sched):
+    rng = np.random.default_rng(3)
+    lens = rng.integers(0, 5000, size=64)
+    t = rng.uniform(0, 1, size=64)
+    t[:4] = [0.0, 1.0, 0.5, 0.25]
+    got = ec.capacity(lens, 64, t=t, c_min=4.0, c_max=12.0, scheduler=sched)
+    exp = ref.capacity_ref(lens, 64, t=t, c_min=4.0, c_max=12.0, sched=sched)
+    assert np.array_equal(got, exp)
+    got = ec.capacity(lens, 64, c=8.0)
+    assert np.array_equal(got, ref.capacity_ref(lens, 64, c=8.0))
+    # half-to-even on exact ties: L c / E = 2.5 -> 2 and 3.5 -> 4
+    assert list(ec.capacity([5, 7], 2, c=1.0)) == [2, 4]

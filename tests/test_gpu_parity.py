@@ -1,0 +1,280 @@
+"""Parity of the HIP path (through the C interface) with the CPU float64 oracle.
+
+Tolerances (stated by the layer's specification, derived for fp32 storage):
+  * scores S: max |S_gpu - S_ref| / S_ref <= 1e-5 (fp32 scores, fp32 accumulation);
+  * selection: bit-exact against the oracle's selection run on the GPU's own S;
+  * outputs and gradients: relative L2 <= 2e-2 for bf16 storage (fp32
+    accumulation), <= 1e-4 for fp32 storage (fp32 sums of up to a few
+    thousand terms, unit roundoff 6e-8).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ec_ref as ref
+import paper_2604_01622_amd as ec
+from paper_2604_01622_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+S_TOL = 1e-5
+
+
+def out_tol(dtype):
+    return 2e-2 if dtype == "bf16" else 1e-4
+
+
+def dev(a):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def rel_l2(got, exp):
+    got, exp = ref.widen(got), np.asarray(exp, dtype=np.float64)
+    den = np.linalg.norm(exp)
+    return float(np.linalg.norm(got - exp) / (den if den > 0 else 1.0))
+
+
+def caps_for(wl, inp):
+    """(library capacities, oracle capacities) for a workload; they must agree."""
+    L = np.asarray(wl.group_lengths)
+    if wl.time_dependent:
+        k_lib = ec.capacity(L, wl.n_experts, t=inp.t, c_min=wl.c_min, c_max=wl.c_max)
+        k_ref = ref.capacity_ref(L, wl.n_experts, t=inp.t, c_min=wl.c_min, c_max=wl.c_max)
+    else:
+        k_lib = ec.capacity(L, wl.n_experts, c=wl.capacity_factor)
+        k_ref = ref.capacity_ref(L, wl.n_experts, c=wl.capacity_factor)
+    assert np.array_equal(k_lib, k_ref)
+    return k_lib
+
+
+def check_route(inp, caps, inv_tau, S_rows=None):
+    """Runs ec_route; checks S against the oracle (all rows or a sample) and the
+    selection bit-exactly against the oracle run on the GPU's S."""
+    wl = inp.wl
+    off = wl.group_offsets
+    X, Wg = dev(inp.X), dev(inp.Wg)
+    S, sel, gate, slot = ec.route(X, Wg, off, caps, inv_tau, d_ff=wl.d_ff)
+    torch.cuda.synchronize()
+    S_h, sel_h, gate_h, slot_h = S.cpu().numpy(), sel.cpu().numpy(), gate.cpu().numpy(), slot.cpu().numpy()
+    rows = np.arange(wl.n_tokens) if S_rows is None else S_rows
+    S_ref = ref.router_ref(np.asarray(inp.X)[rows], inp.Wg, inv_tau)
+    err = np.max(np.abs(S_h[rows].astype(np.float64) - S_ref) / S_ref) if len(rows) else 0.0
+    assert err <= S_TOL, f"score error {err:.3g}"
+    sel_ref = ref.select_ref(S_h.astype(np.float64), off, caps)
+    assert sel_h.shape == sel_ref.shape
+    assert np.array_equal(sel_h, sel_ref), "selection differs from the oracle on the GPU's scores"
+    slot_exp = ref.slot_ref(sel_ref, wl.n_tokens).T
+    assert np.array_equal(slot_h, slot_exp)
+    if sel_h.size:
+        assert np.array_equal(gate_h, np.take_along_axis(S_h.T, sel_h.astype(np.int64), 1))
+    return S_h, sel_h
+
+
+def run_layer(inp, caps, inv_tau, backward=False):
+    wl = inp.wl
+    X, Wg, W1, W3, W2 = (dev(a) for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2))
+    Y, saved = ec.forward(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, save=True)
+    out = {"Y": host(Y), "saved": saved}
+    if backward:
+        g = ec.backward(X, Wg, W1, W3, W2, dev(inp.dY), saved, wl.group_offsets, caps, inv_tau)
+        for n, t in zip(("dX", "dWg", "dW1", "dW3", "dW2"), g):
+            out[n] = host(t)
+    torch.cuda.synchronize()
+    P = ec.Problem.of(X, Wg, wl.d_ff, wl.group_offsets, caps, inv_tau)
+    out["views"] = {k: v for k, v in ec.saved_views(saved, P).items()}
+    return out
+
+
+def full_case(wl, inv_tau=None, backward=None, inp=None):
+    inv_tau = wl.inv_temperatures[0] if inv_tau is None else inv_tau
+    backward = wl.backward if backward is None else backward
+    print(f"[case] {wl.name} inv_tau={inv_tau} backward={backward}", flush=True)
+    inp = inp or synth.draw(wl, with_dy=backward)
+    caps = caps_for(wl, inp)
+    S_h, sel = check_route(inp, caps, inv_tau)
+    out = run_layer(inp, caps, inv_tau, backward)
+    # the forward's routing equals ec_route's (same kernels, deterministic)
+    assert np.array_equal(out["views"]["sel_token"].cpu().numpy(), sel)
+    assert np.array_equal(out["views"]["S"].cpu().numpy(), S_h)
+    tol = out_tol(wl.dtype)
+    args = (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2)
+    if not backward:
+        Y_ref = ref.forward_ref(*args, wl.group_offsets, caps, inv_tau, sel_token=sel)["Y"]
+        assert rel_l2(out["Y"], Y_ref) <= tol, rel_l2(out["Y"], Y_ref)
+        return out
+    g = ref.backward_ref(*args, inp.dY, wl.group_offsets, caps, inv_tau, sel_token=sel)
+    Y_ref = ref.forward_ref(*args, wl.group_offsets, caps, inv_tau, sel_token=sel)["Y"]
+    errs = {"Y": rel_l2(out["Y"], Y_ref)}
+    for n in ("dX", "dWg", "dW1", "dW3", "dW2"):
+        errs[n] = rel_l2(out[n], g[n])
+    print("[errs]", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    assert all(v <= tol for v in errs.values()), errs
+    return out
+
+
+# ------------------------------------------------------------------ small cases
+
+def test_tiny_f32_forward_backward():
+    wl = synth.TINY_F32
+    full_case(wl, backward=True, inp=synth.draw(wl, with_dy=True))
+
+
+RAGGED = dict(group_lengths=[700, 384, 530], d=256, E=16, h=320)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_ragged_multitile_forward_backward(dtype):
+    wl = synth.small(f"ragged_{dtype}", RAGGED["group_lengths"], RAGGED["d"], RAGGED["E"],
+                     RAGGED["h"], dtype=dtype, seed=11, c_min=4.0, c_max=12.0, backward=True)
+    full_case(wl)
+
+
+@pytest.mark.parametrize("inv_tau", [0.5, 2.0])
+def test_temperature(inv_tau):
+    wl = synth.small("temp", [512, 300], 128, 32, 128, seed=12, capacity_factor=3.0)
+    full_case(wl, inv_tau=inv_tau)
+
+
+@pytest.mark.parametrize("E", [1, 5, 17, 200])
+def test_expert_counts(E):
+    wl = synth.small(f"E{E}", [256, 129], 128, E, 64, seed=13, capacity_factor=min(2.0, E))
+    full_case(wl)
+
+
+def test_zero_capacity_everywhere():
+    wl = synth.small("k0", [100, 50], 64, 8, 64, seed=14, capacity_factor=0.0, backward=True)
+    out = full_case(wl)
+    assert np.all(out["Y"] == 0) and np.all(out["dW1"] == 0) and np.all(out["dWg"] == 0)
+
+
+def test_full_capacity_everywhere():
+    # k = L: every expert takes every token of the group (dense soft mixture)
+    wl = synth.small("kL", [96, 64], 128, 4, 128, seed=15, capacity_factor=4.0, backward=True)
+    full_case(wl)
+
+
+def test_empty_and_singleton_groups():
+    wl = synth.small("empty", [0, 1, 300, 0, 77], 64, 8, 64, seed=16, capacity_factor=2.5,
+                     backward=True)
+    full_case(wl)
+
+
+def test_many_groups():
+    rng = np.random.default_rng(17)
+    lens = rng.integers(5, 40, size=300)          # > one launch's group table
+    wl = synth.small("many", lens, 64, 8, 64, seed=17, c_min=1.0, c_max=6.0)
+    full_case(wl)
+
+
+def test_long_group_route_only():
+    # a column longer than the LDS-cached top-k path
+    wl = synth.small("long", [20000, 777], 64, 4, 64, seed=18, capacity_factor=1.5)
+    inp = synth.draw(wl)
+    caps = caps_for(wl, inp)
+    check_route(inp, caps, 1.0)
+
+
+def test_ties_zero_router():
+    # Wg = 0: every score is exactly 1/E and each expert takes the first k tokens
+    wl = synth.small("ties", [64, 40], 64, 8, 64, seed=19, capacity_factor=2.0)
+    inp = synth.draw(wl)
+    inp.Wg[:] = 0
+    caps = caps_for(wl, inp)
+    S_h, sel = check_route(inp, caps, 1.0)
+    assert np.all(S_h == np.float32(1.0 / 8))
+    exp = np.concatenate([np.arange(caps[0]), 64 + np.arange(caps[1])])
+    assert np.array_equal(sel, np.tile(exp, (8, 1)))
+
+
+def test_ties_repeated_tokens():
+    # tokens drawn from 10 integer-valued prototypes: whole groups of tokens have
+    # bitwise-equal scores, so every column's threshold falls inside a tie
+    wl = synth.small("qties", [333, 200], 64, 8, 64, seed=20, capacity_factor=2.0)
+    inp = synth.draw(wl)
+    rng = np.random.default_rng(20)
+    protos = rng.integers(-1, 2, size=(10, 64)).astype(np.float32)
+    inp.X[:] = synth.f32_to_bf16_bits(protos[rng.integers(0, 10, size=wl.n_tokens)])
+    inp.Wg[:] = synth.f32_to_bf16_bits(
+        (rng.integers(-2, 3, size=inp.Wg.shape) / 8).astype(np.float32))
+    caps = caps_for(wl, inp)
+    S_h, sel = check_route(inp, caps, 1.0)
+    assert len(np.unique(S_h[:, 0])) <= 10     # the ties are really there
+
+
+def test_deterministic():
+    wl = synth.small("det", [512, 512], 256, 16, 192, seed=21, capacity_factor=4.0, backward=True)
+    inp = synth.draw(wl, with_dy=True)
+    caps = caps_for(wl, inp)
+    a = run_layer(inp, caps, 1.0, backward=True)
+    b = run_layer(inp, caps, 1.0, backward=True)
+    for n in ("Y", "dX", "dWg", "dW1", "dW3", "dW2"):
+        assert np.array_equal(a[n], b[n]), n
+
+
+# ------------------------------------------------------------------ full-size workloads
+# Same launch configuration as the benchmark; the oracle checks the selection
+# everywhere, the scores on sampled rows and the outputs on sampled tokens.
+
+def _full_forward(wl, inv_tau, n_rows=32, seed=0):
+    print(f"[case] {wl.name} inv_tau={inv_tau}", flush=True)
+    inp = synth.draw(wl)
+    caps = caps_for(wl, inp)
+    rng = np.random.default_rng(seed)
+    rows = np.sort(rng.choice(wl.n_tokens, size=256, replace=False))
+    S_h, sel = check_route(inp, caps, inv_tau, S_rows=rows)
+    out = run_layer(inp, caps, inv_tau)
+    assert np.array_equal(out["views"]["sel_token"].cpu().numpy(), sel)
+    # pick sampled tokens among the selected ones (and one unselected, if any)
+    chosen = np.unique(sel)
+    yrows = np.sort(rng.choice(chosen, size=min(n_rows, len(chosen)), replace=False))
+    Y_ref = ref.forward_rows_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, sel, yrows, inv_tau)
+    err = rel_l2(out["Y"][yrows], Y_ref)
+    print(f"[errs] Y(sampled {len(yrows)}) {err:.2e}", flush=True)
+    assert err <= 2e-2
+    unsel = np.setdiff1d(np.arange(wl.n_tokens), chosen)
+    if len(unsel):
+        assert np.all(out["Y"][unsel[:64]] == 0)
+
+
+def test_full_static_bf16():
+    _full_forward(synth.STATIC_BF16, 1.0)
+
+
+def test_full_timestep_bf16():
+    _full_forward(synth.TIMESTEP_BF16, 1.0)
+
+
+@pytest.mark.parametrize("inv_tau", synth.FINE_BF16.inv_temperatures)
+def test_full_fine_bf16(inv_tau):
+    _full_forward(synth.FINE_BF16, inv_tau, n_rows=16)
+
+
+def test_full_train_bf16():
+    wl = synth.TRAIN_BF16
+    print(f"[case] {wl.name} backward", flush=True)
+    inp = synth.draw(wl, with_dy=True)
+    caps = caps_for(wl, inp)
+    rng = np.random.default_rng(4)
+    rows = np.sort(rng.choice(wl.n_tokens, size=256, replace=False))
+    S_h, sel = check_route(inp, caps, 1.0, S_rows=rows)
+    out = run_layer(inp, caps, 1.0, backward=True)
+    args = (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, sel)
+    chosen = np.unique(sel)
+    xrows = np.sort(rng.choice(chosen, size=8, replace=False))
+    errs = {"dX": rel_l2(out["dX"][xrows], ref.backward_rows_ref(*args, xrows, 1.0))}
+    for j in (0, wl.n_experts - 1):
+        g1, g3, g2 = ref.expert_grads_ref(*args, j, 1.0)
+        errs[f"dW1[{j}]"] = rel_l2(out["dW1"][j], g1)
+        errs[f"dW3[{j}]"] = rel_l2(out["dW3"][j], g3)
+        errs[f"dW2[{j}]"] = rel_l2(out["dW2"][j], g2)
+    errs["dWg"] = rel_l2(out["dWg"], ref.router_grad_ref(*args, 1.0))
+    print("[errs]", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    assert all(v <= 2e-2 for v in errs.values()), errs

@@ -360,3 +360,28 @@ def test_pins_catch_planted_mistakes(monkeypatch):
     fd = (lp - lm) / (2 * eps)
     assert abs(fd - g["dWg"].reshape(-1)[0]) < 1e-7
     assert abs(fd - dWg_bad.reshape(-1)[0]) > 1e-6
+
+
+# --------------------------------------------------------------------- restricted forms
+
+def test_restricted_forms_equal_full_definitions():
+    inp = _tiny_inputs([19, 23, 9], 16, 5, 24, seed=21, dtype="bf16")
+    off = inp.wl.group_offsets
+    k = [6, 4, 9]
+    inv_tau = 0.7
+    full = ref.backward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, off, k, inv_tau)
+    sel = full["sel_token"]
+    Y = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, inv_tau)["Y"]
+    rows = [0, 5, 18, 19, 40, 50]
+    assert np.max(np.abs(ref.forward_rows_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, sel, rows,
+                                              inv_tau) - Y[rows])) < 1e-12
+    assert np.max(np.abs(ref.backward_rows_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, sel,
+                                               rows, inv_tau) - full["dX"][rows])) < 1e-12
+    for j in range(5):
+        g1, g3, g2 = ref.expert_grads_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, sel, j,
+                                          inv_tau)
+        assert np.max(np.abs(g1 - full["dW1"][j])) < 1e-12
+        assert np.max(np.abs(g3 - full["dW3"][j])) < 1e-12
+        assert np.max(np.abs(g2 - full["dW2"][j])) < 1e-12
+    dWg = ref.router_grad_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, sel, inv_tau)
+    assert np.max(np.abs(dWg - full["dWg"])) < 1e-12
