@@ -284,6 +284,8 @@ class StageEvents:
 
     def __init__(self, n_stages: int):
         self.events = [torch.cuda.Event(enable_timing=True) for _ in range(n_stages + 1)]
+        for e in self.events:   # torch creates the underlying HIP event on first record
+            e.record()
         self._arr = (ctypes.c_void_p * len(self.events))()
 
     def arm(self):

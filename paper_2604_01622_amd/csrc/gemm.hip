@@ -289,7 +289,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmParams p) {
   // ---- epilogue: stage 32-row slices of the wave tile through LDS ----
   constexpr int SLD = WN + 4;
   float* stage = reinterpret_cast<float*>(smem) + wave * 32 * SLD;
-#pragma unroll 1
+#pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
 #pragma unroll
     for (int ni = 0; ni < NB; ++ni)
