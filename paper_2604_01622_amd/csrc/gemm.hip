@@ -57,75 +57,74 @@ struct GemmParams {
 
 // ------------------------------------------------------------------ bf16 MFMA
 
-__device__ __forceinline__ void transpose8x8(const uint4 in[8], uint4 out[8]) {
+__device__ __forceinline__ void transpose8x8(const u32x4 in[8], u32x4 out[8]) {
   // in[kq] holds 8 bf16 along m for k = kq; out[mm] holds 8 bf16 along k for m = mm
-  const uint32_t* w = reinterpret_cast<const uint32_t*>(in);
-  uint32_t* o = reinterpret_cast<uint32_t*>(out);
 #pragma unroll
   for (int p = 0; p < 4; ++p) {       // source dword p holds m = 2p, 2p+1
 #pragma unroll
     for (int q = 0; q < 4; ++q) {     // dest dword q holds k = 2q, 2q+1
-      const uint32_t lo = w[(2 * q) * 4 + p], hi = w[(2 * q + 1) * 4 + p];
-      o[(2 * p) * 4 + q] = (lo & 0xffffu) | (hi << 16);
-      o[(2 * p + 1) * 4 + q] = (lo >> 16) | (hi & 0xffff0000u);
+      const uint32_t lo = in[2 * q][p], hi = in[2 * q + 1][p];
+      out[2 * p][q] = (lo & 0xffffu) | (hi << 16);
+      out[2 * p + 1][q] = (lo >> 16) | (hi & 0xffff0000u);
     }
   }
 }
 
-template <int R, bool KC>
+template <int R, bool KC, int NT>
 struct TileRegs {
-  static constexpr int N = KC ? (R * 8 + 255) / 256 : 8 * ((R + 255) / 256);
+  static constexpr int N = KC ? (R * 8 + NT - 1) / NT : 8 * ((R + NT - 1) / NT);
 };
 
 // Loads one 64-wide K step of an operand tile of R rows into registers.
 //   KC:  row r (0..R) -> pointer row_ptr(r) (K-contiguous), chunk of 8 k.
 //   !KC: element (r, k) at col_base + k*ld + r, rows r >= r_valid zero.
-template <int R>
-__device__ __forceinline__ void load_kc(uint4* regs, const bf16_t* const* rowp, int k0, int kv) {
+// K-contiguous operand: chunk c = tid + q*NT covers row c/8, k-chunk c%8.  The
+// K extent of such operands is a multiple of 64, so no K predicate is needed.
+template <int R, int NT>
+__device__ __forceinline__ void load_kc(u32x4* regs, const bf16_t* const* rowp, int k0) {
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < TileRegs<R, true>::N; ++q) {
-    const int c = tid + q * 256;
-    const int ch = c & 7;
-    const int k = k0 + ch * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (c < R * 8 && k < kv) v = *reinterpret_cast<const uint4*>(rowp[q] + k);
-    regs[q] = v;
+  for (int q = 0; q < TileRegs<R, true, NT>::N; ++q) {
+    const int c = tid + q * NT;
+    if (R * 8 % NT == 0 || c < R * 8)
+      regs[q] = *reinterpret_cast<const u32x4*>(rowp[q] + k0 + (c & 7) * 8);
   }
 }
 
-template <int R>
-__device__ __forceinline__ void store_kc(bf16_t* s, const uint4* regs) {
+template <int R, int NT>
+__device__ __forceinline__ void store_kc(bf16_t* s, const u32x4* regs) {
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < TileRegs<R, true>::N; ++q) {
-    const int c = tid + q * 256;
-    if (c < R * 8) *reinterpret_cast<uint4*>(s + (c >> 3) * GLDK + (c & 7) * 8) = regs[q];
+  for (int q = 0; q < TileRegs<R, true, NT>::N; ++q) {
+    const int c = tid + q * NT;
+    if (R * 8 % NT == 0 || c < R * 8)
+      *reinterpret_cast<u32x4*>(s + (c >> 3) * GLDK + (c & 7) * 8) = regs[q];
   }
 }
 
-template <int R>
-__device__ __forceinline__ void store_mn(bf16_t* s, const uint4* regs) {
+template <int R, int NT>
+__device__ __forceinline__ void store_mn(bf16_t* s, const u32x4* regs) {
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < (R + 255) / 256; ++q) {
-    const int b = tid + q * 256;
+  for (int q = 0; q < (R + NT - 1) / NT; ++q) {
+    const int b = tid + q * NT;
     if (b < R) {
       const int kb = b & 7, rc = b >> 3;
-      uint4 t[8];
+      u32x4 t[8];
       transpose8x8(regs + 8 * q, t);
 #pragma unroll
       for (int mm = 0; mm < 8; ++mm)
-        *reinterpret_cast<uint4*>(s + (rc * 8 + mm) * GLDK + kb * 8) = t[mm];
+        *reinterpret_cast<u32x4*>(s + (rc * 8 + mm) * GLDK + kb * 8) = t[mm];
     }
   }
 }
 
-template <int BM, int BN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmParams p) {
-  constexpr int WM = BM / 2, WN = BN / 2;
+template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_kernel(GemmParams p) {
+  constexpr int NT = 64 * WGM * WGN;   // threads
+  constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int MB = WM / 32, NB = WN / 32;
-  constexpr int A_N = TileRegs<BM, A_KC>::N, B_N = TileRegs<BN, B_KC>::N;
+  constexpr int A_N = TileRegs<BM, A_KC, NT>::N, B_N = TileRegs<BN, B_KC, NT>::N;
   static_assert(EPI != EPI_SWIGLU || (NB % 2 == 0), "SwiGLU needs W1 and W3 blocks per wave");
   __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * GLDK];
   bf16_t* As = smem;
@@ -142,7 +141,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmParams p) {
   const int n0 = (EPI == EPI_SWIGLU) ? nt * (BN / 2) : nt * BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % WGM, wn = wave / WGM;
 
   const bf16_t* Ab = reinterpret_cast<const bf16_t*>(p.A) + (size_t)e * p.a_bs;
   const bf16_t* Bb = reinterpret_cast<const bf16_t*>(p.B) + (size_t)e * p.b_bs;
@@ -154,7 +153,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmParams p) {
   if constexpr (A_KC) {
 #pragma unroll
     for (int q = 0; q < A_N; ++q) {
-      int r = m0 + ((tid + q * 256) >> 3);
+      int r = m0 + ((tid + q * NT) >> 3);
       r = r < p.M ? r : p.M - 1;
       arow[q] = Ab + (size_t)r * p.lda;
     }
@@ -162,7 +161,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmParams p) {
   if constexpr (B_KC) {
 #pragma unroll
     for (int q = 0; q < B_N; ++q) {
-      const int lr = (tid + q * 256) >> 3;
+      const int lr = (tid + q * NT) >> 3;
       if constexpr (EPI == EPI_SWIGLU) {
         const int half = lr / (BN / 2);
         int r = n0 + lr % (BN / 2);
@@ -176,62 +175,58 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmParams p) {
     }
   }
 
-  auto load_a = [&](int k0, uint4* regs) {
+  // M/N-contiguous operand: 8 x 8 block b = tid + q*NT covers k-rows kb*8.. and
+  // columns rc*8..; rows past kv (the ragged K tail) and columns past `cols` read 0.
+  auto load_mn = [&](u32x4* regs, auto src_row, int R, int r0, int cols, int k0, int kv) {
+#pragma unroll
+    for (int q = 0; q < 8 * ((R + NT - 1) / NT) / 8; ++q) {
+      const int b = tid + q * NT;
+      const int kb = b & 7, rc = b >> 3;
+      const int c = r0 + rc * 8;
+      const bool full = (k0 + GBK <= kv);
+#pragma unroll
+      for (int kq = 0; kq < 8; ++kq) {
+        const int k = k0 + kb * 8 + kq;
+        u32x4 v = u32x4{0u, 0u, 0u, 0u};
+        if ((R % NT == 0 || b < R) && (full || k < kv) && c < cols)
+          v = *reinterpret_cast<const u32x4*>(src_row(k) + c);
+        regs[8 * q + kq] = v;
+      }
+    }
+  };
+  auto load_a = [&](int k0, u32x4* regs) {
     if constexpr (A_KC) {
-      load_kc<BM>(regs, arow, k0, p.kv_a);
+      load_kc<BM, NT>(regs, arow, k0);
     } else {
-#pragma unroll
-      for (int q = 0; q < (BM + 255) / 256; ++q) {
-        const int b = tid + q * 256;
-        const int kb = b & 7, rc = b >> 3;
-        const int m = m0 + rc * 8;
-#pragma unroll
-        for (int kq = 0; kq < 8; ++kq) {
-          const int k = k0 + kb * 8 + kq;
-          uint4 v = make_uint4(0, 0, 0, 0);
-          if (b < BM && k < p.kv_a && m < p.M)
-            v = *reinterpret_cast<const uint4*>(Ab + (size_t)k * p.lda + m);
-          regs[8 * q + kq] = v;
-        }
-      }
+      load_mn(regs, [&](int k) { return Ab + (size_t)k * p.lda; }, BM, m0, p.M, k0, p.kv_a);
     }
   };
-  auto load_b = [&](int k0, uint4* regs) {
+  auto load_b = [&](int k0, u32x4* regs) {
     if constexpr (B_KC) {
-      load_kc<BN>(regs, brow, k0, p.kv_b);
+      load_kc<BN, NT>(regs, brow, k0);
     } else {
-#pragma unroll
-      for (int q = 0; q < (BN + 255) / 256; ++q) {
-        const int b = tid + q * 256;
-        const int kb = b & 7, rc = b >> 3;
-        const int n = n0 + rc * 8;
-#pragma unroll
-        for (int kq = 0; kq < 8; ++kq) {
-          const int k = k0 + kb * 8 + kq;
-          uint4 v = make_uint4(0, 0, 0, 0);
-          if (b < BN && k < p.kv_b && n < p.N) {
-            const bf16_t* src = (k < p.k_split) ? Bb + (size_t)k * p.ldb
-                                                : B2b + (size_t)(k - p.k_split) * p.ldb;
-            v = *reinterpret_cast<const uint4*>(src + n);
-          }
-          regs[8 * q + kq] = v;
-        }
-      }
+      load_mn(regs,
+              [&](int k) {
+                return (k < p.k_split) ? Bb + (size_t)k * p.ldb
+                                       : B2b + (size_t)(k - p.k_split) * p.ldb;
+              },
+              BN, n0, p.N, k0, p.kv_b);
     }
   };
-  auto store_a = [&](int buf, const uint4* regs) {
-    if constexpr (A_KC) store_kc<BM>(As + buf * BM * GLDK, regs);
-    else store_mn<BM>(As + buf * BM * GLDK, regs);
+  auto store_a = [&](int buf, const u32x4* regs) {
+    if constexpr (A_KC) store_kc<BM, NT>(As + buf * BM * GLDK, regs);
+    else store_mn<BM, NT>(As + buf * BM * GLDK, regs);
   };
-  auto store_b = [&](int buf, const uint4* regs) {
-    if constexpr (B_KC) store_kc<BN>(Bs + buf * BN * GLDK, regs);
-    else store_mn<BN>(Bs + buf * BN * GLDK, regs);
+  auto store_b = [&](int buf, const u32x4* regs) {
+    if constexpr (B_KC) store_kc<BN, NT>(Bs + buf * BN * GLDK, regs);
+    else store_mn<BN, NT>(Bs + buf * BN * GLDK, regs);
   };
 
   // LDS row of this wave's B block ni
   auto b_lds_row = [&](int ni) -> int {
     if constexpr (EPI == EPI_SWIGLU) {
-      return (ni < NB / 2) ? wn * (BN / 4) + ni * 32 : BN / 2 + wn * (BN / 4) + (ni - NB / 2) * 32;
+      constexpr int HWN = BN / 2 / WGN;  // W1 (and W3) columns per wave
+      return (ni < NB / 2) ? wn * HWN + ni * 32 : BN / 2 + wn * HWN + (ni - NB / 2) * 32;
     } else {
       return wn * WN + ni * 32;
     }
@@ -245,7 +240,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
 
-  uint4 ra[A_N], rb[B_N];
+  u32x4 ra[A_N], rb[B_N];
   load_a(0, ra);
   load_b(0, rb);
   store_a(0, ra);
@@ -380,14 +375,297 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmParams p) {
   }
 }
 
-template <int BM, int BN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
+// ------------------------------------------------------------------ bf16 MFMA, pipelined
+// Both operands K-contiguous (the forward products).  K advances 32 at a time
+// through a ring of STAGES LDS buffers filled directly from global memory by
+// global_load_lds_dwordx4 (no VGPR staging), STAGES-1 K steps ahead of the
+// MFMAs.  Each 64-byte LDS row holds one operand row's 32 k values as four
+// 16-byte chunks, XOR-swizzled by row so that the 32-lane fragment reads are
+// free of bank conflicts.
+
+constexpr int DBK = 32;
+
+__device__ __forceinline__ int dma_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane.
+// (The builtin exists only for the device; the host pass must not see it or it
+// drops the kernel's launch stub.)
+__device__ __forceinline__ void dma16(const void* g, void* lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+#endif
+}
+
+constexpr int vmcnt_imm(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
+
+template <int BM, int BN, int WGM, int WGN, int STAGES, int KSTEP, int EPI>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmParams p) {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN;
+  constexpr int MB = WM / 32, NB = WN / 32;
+  constexpr int KK = KSTEP / 16;                // MFMA k-steps per stage
+  constexpr int CPR = KSTEP / 8;                // 16-byte chunks per LDS row
+  constexpr int ROWB = KSTEP * 2;               // bytes per LDS row
+  constexpr int ROWS = BM + BN;                 // LDS rows per stage (A then B)
+  constexpr int STAGE_BYTES = ROWS * ROWB;
+  constexpr int RPL = 1024 / ROWB;              // rows per 1 KiB load block
+  constexpr int LOADS = ROWS * CPR / NT;        // 16-byte chunks per thread per stage
+  constexpr int SLD = WN + 4;
+  constexpr int STAGE_EPI = NT / 64 * 32 * SLD * 4;
+  constexpr int SMEM = STAGES * STAGE_BYTES > STAGE_EPI ? STAGES * STAGE_BYTES : STAGE_EPI;
+  static_assert(ROWS * CPR % NT == 0, "whole 16-byte chunks per thread");
+  static_assert(KSTEP == 32 || KSTEP == 64, "K step");
+  static_assert(EPI != EPI_SWIGLU || (NB % 2 == 0), "SwiGLU needs W1 and W3 blocks per wave");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+
+  const int ntile = p.batches * p.MT * p.NT;
+  const int t = xcd_tile_id(blockIdx.x, gridDim.x);
+  if (t >= ntile) return;
+  const int per_b = p.MT * p.NT;
+  const int e = t / per_b;
+  const int rem = t - e * per_b;
+  const int mt = rem % p.MT, nt = rem / p.MT;
+  const int m0 = mt * BM;
+  const int n0 = (EPI == EPI_SWIGLU) ? nt * (BN / 2) : nt * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave % WGM, wn = wave / WGM;
+  const bf16_t* Ab = reinterpret_cast<const bf16_t*>(p.A) + (size_t)e * p.a_bs;
+  const bf16_t* Bb = reinterpret_cast<const bf16_t*>(p.B) + (size_t)e * p.b_bs;
+  const bf16_t* B2b = p.B2 ? reinterpret_cast<const bf16_t*>(p.B2) + (size_t)e * p.b_bs : nullptr;
+
+  // swizzle: physical chunk = logical chunk ^ swz(row), conflict-free 32-lane
+  // fragment reads for 32 and 64 LDS banks
+  auto swz = [](int row) -> int {
+    if constexpr (KSTEP == 32) return ((row >> 1) ^ (row >> 3)) & 3;
+    else return (row ^ (row >> 3)) & 7;
+  };
+
+  // The q-th load of this thread fills 1 KiB block (wave * LOADS + q) of a stage.
+  const bf16_t* src[LOADS];
+#pragma unroll
+  for (int q = 0; q < LOADS; ++q) {
+    const int row = (wave * LOADS + q) * RPL + lane / CPR;
+    const int lc = (lane % CPR) ^ swz(row);
+    const bf16_t* rp;
+    if (row < BM) {
+      int r = m0 + row;
+      r = r < p.M ? r : p.M - 1;
+      rp = Ab + (size_t)r * p.lda;
+    } else {
+      const int lr = row - BM;
+      if constexpr (EPI == EPI_SWIGLU) {
+        int r = n0 + lr % (BN / 2);
+        r = r < p.N ? r : p.N - 1;
+        rp = (lr < BN / 2 ? Bb : B2b) + (size_t)r * p.ldb;
+      } else {
+        int r = n0 + lr;
+        r = r < p.N ? r : p.N - 1;
+        rp = Bb + (size_t)r * p.ldb;
+      }
+    }
+    src[q] = rp + lc * 8;
+  }
+  auto issue = [&](int kt, int stage) {
+    char* base = smem + stage * STAGE_BYTES + wave * LOADS * 1024;
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) dma16(src[q] + kt * KSTEP, base + q * 1024);
+  };
+
+  auto b_lds_row = [&](int ni) -> int {
+    if constexpr (EPI == EPI_SWIGLU) {
+      constexpr int HWN = BN / 2 / WGN;
+      return (ni < NB / 2) ? wn * HWN + ni * 32 : BN / 2 + wn * HWN + (ni - NB / 2) * 32;
+    } else {
+      return wn * WN + ni * 32;
+    }
+  };
+  int aoff[MB], boff[NB], aswz[MB], bswz[NB];
+#pragma unroll
+  for (int mi = 0; mi < MB; ++mi) {
+    const int row = wm * WM + mi * 32 + (lane & 31);
+    aoff[mi] = row * ROWB;
+    aswz[mi] = swz(row);
+  }
+#pragma unroll
+  for (int ni = 0; ni < NB; ++ni) {
+    const int row = BM + b_lds_row(ni) + (lane & 31);
+    boff[ni] = row * ROWB;
+    bswz[ni] = swz(row);
+  }
+  bf16x8 af[2][MB], bfr[2][NB];
+  auto load_frags = [&](int buf, int stage, int kk) {
+    const char* sb = smem + stage * STAGE_BYTES;
+    const int lc = kk * 2 + (lane >> 5);
+#pragma unroll
+    for (int mi = 0; mi < MB; ++mi)
+      af[buf][mi] = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(sb + aoff[mi] + ((lc ^ aswz[mi]) << 4)));
+#pragma unroll
+    for (int ni = 0; ni < NB; ++ni)
+      bfr[buf][ni] = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(sb + boff[ni] + ((lc ^ bswz[ni]) << 4)));
+  };
+
+  f32x16 acc[MB][NB];
+#pragma unroll
+  for (int mi = 0; mi < MB; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < NB; ++ni)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
+
+  // Waits until this wave's loads of K step `kt` have landed, given how many
+  // younger steps have been issued after it.
+  auto wait_step = [&](int kt, int KT) {
+    const int younger = KT - 1 - kt < STAGES - 2 ? KT - 1 - kt : STAGES - 2;
+    static_assert(STAGES <= 5, "wait cases");
+    if (younger >= 3) __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * LOADS));
+    else if (younger == 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));
+    else if (younger == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  };
+
+  // Ring: steps 0..STAGES-1 are issued up front; the end of step kt refills
+  // stage kt % STAGES with step kt + STAGES once every wave has read it.  When
+  // waiting for step j, the steps issued after it number
+  // min(STAGES-1, KT-1-j) for j = 0 and min(STAGES-2, KT-1-j) afterwards.
+  const int KT = p.K / KSTEP;
+#pragma unroll
+  for (int s = 0; s < STAGES; ++s)
+    if (s < KT) issue(s, s);
+  if (KT > 0) {
+    const int younger = KT - 1 < STAGES - 1 ? KT - 1 : STAGES - 1;
+    if (younger >= 3) __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * LOADS));
+    else if (younger == 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));
+    else if (younger == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __builtin_amdgcn_s_barrier();
+    load_frags(0, 0, 0);
+  }
+  // Each k-step: the first half of its MFMAs, then the next k-step's fragment
+  // reads (at a stage end: the barrier, the refill of this stage and the next
+  // stage's first fragments), then the second half, so that the LDS latency
+  // is covered by MFMAs already in flight.
+  constexpr int NMF = MB * NB;
+  auto mfma_range = [&](int cur, int lo, int hi) {
+#pragma unroll
+    for (int q = 0; q < NMF; ++q) {
+      if (q < lo || q >= hi) continue;
+      const int mi = q / NB, ni = q % NB;
+      acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][mi], bfr[cur][ni],
+                                                              acc[mi][ni], 0, 0, 0);
+    }
+  };
+  for (int kt = 0; kt < KT; ++kt) {
+    const int stage = kt % STAGES;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int cur = kk & 1;
+      mfma_range(cur, 0, NMF / 2);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kk + 1 < KK) {
+        load_frags(cur ^ 1, stage, kk + 1);
+      } else {
+        // after the final step this reads a stale stage, harmlessly, which
+        // keeps the loop body uniform
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): this wave's reads are done
+        if (kt + 1 < KT) wait_step(kt + 1, KT);
+        __builtin_amdgcn_s_barrier();
+        if (kt + STAGES < KT) issue(kt + STAGES, stage);
+        load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_range(cur, NMF / 2, NMF);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  __syncthreads();
+
+  // ---- epilogue (same as gemm_bf16_kernel) ----
+  float* stage_f = reinterpret_cast<float*>(smem) + wave * 32 * SLD;
+#pragma unroll
+  for (int mi = 0; mi < MB; ++mi) {
+#pragma unroll
+    for (int ni = 0; ni < NB; ++ni)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        stage_f[row * SLD + ni * 32 + (lane & 31)] = acc[mi][ni][r];
+      }
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+    const int mbase = m0 + wm * WM + mi * 32;
+    if constexpr (EPI == EPI_STORE) {
+      constexpr int CPR = WN / 8;
+#pragma unroll
+      for (int q = 0; q < (32 * CPR) / 64; ++q) {
+        const int c = lane + q * 64;
+        const int row = c / CPR, cc = c % CPR;
+        const int m = mbase + row;
+        const int n = n0 + wn * WN + cc * 8;
+        if (m < p.M && n < p.N) {
+          const float* v = stage_f + row * SLD + cc * 8;
+          float vv[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) vv[u] = v[u];
+          Elem<bf16_t>::store8((bf16_t*)p.C + (size_t)e * p.c_bs + (size_t)m * p.ldc + n, vv);
+        }
+      }
+    } else {
+      constexpr int HW = WN / 2;
+      constexpr int CPR = HW / 8;
+#pragma unroll
+      for (int q = 0; q < (32 * CPR + 63) / 64; ++q) {
+        const int c = lane + q * 64;
+        const int row = c / CPR, cc = c % CPR;
+        const int m = mbase + row;
+        const int n = n0 + wn * HW + cc * 8;
+        if (c < 32 * CPR && m < p.M && n < p.N) {
+          const float* v1 = stage_f + row * SLD + cc * 8;
+          const float* v3 = v1 + HW;
+          float a[8], h1[8], h3[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            h1[u] = v1[u];
+            h3[u] = v3[u];
+            a[u] = silu_f(h1[u]) * h3[u];
+          }
+          Elem<bf16_t>::store8((bf16_t*)p.C + (size_t)e * p.c_bs + (size_t)m * p.ldc + n, a);
+          if (p.H1) {
+            const size_t ho = (size_t)e * p.h_bs + (size_t)m * p.ldh + n;
+            Elem<bf16_t>::store8((bf16_t*)p.H1 + ho, h1);
+            Elem<bf16_t>::store8((bf16_t*)p.H3 + ho, h3);
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+template <int BM, int BN, int WGM, int WGN, int STAGES, int KSTEP, int EPI>
+hipError_t run_nt_dma(GemmParams p, hipStream_t st) {
+  p.MT = (p.M + BM - 1) / BM;
+  p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
+  const long ntile = (long)p.batches * p.MT * p.NT;
+  if (ntile == 0) return hipSuccess;
+  const long grid = (ntile + 7) / 8 * 8;
+  gemm_nt_dma_kernel<BM, BN, WGM, WGN, STAGES, KSTEP, EPI>
+      <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
 hipError_t run_bf16(GemmParams p, hipStream_t st) {
   p.MT = (p.M + BM - 1) / BM;
   p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
   const long ntile = (long)p.batches * p.MT * p.NT;
   if (ntile == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
-  gemm_bf16_kernel<BM, BN, A_KC, B_KC, EPI, OUT_F32><<<dim3((unsigned)grid), 256, 0, st>>>(p);
+  gemm_bf16_kernel<BM, BN, WGM, WGN, A_KC, B_KC, EPI, OUT_F32>
+      <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
   return hipGetLastError();
 }
 
@@ -517,7 +795,7 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
   p.H1 = H1; p.H3 = H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU>(p, 1, 1, st);
-  return run_bf16<256, 128, true, true, EPI_SWIGLU, false>(p, st);
+  return run_nt_dma<256, 256, 4, 2, 2, 64, EPI_SWIGLU>(p, st);
 }
 
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
@@ -529,7 +807,7 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
   p.C = O; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
-  return run_bf16<256, 128, true, true, EPI_STORE, false>(p, st);
+  return run_nt_dma<256, 256, 4, 2, 2, 64, EPI_STORE>(p, st);
 }
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
@@ -544,7 +822,7 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
   p.H1 = (void*)H1; p.H3 = (void*)H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
-  return run_bf16<256, 128, true, false, EPI_SWIGLU_BWD, false>(p, st);
+  return run_bf16<256, 256, 4, 2, true, false, EPI_SWIGLU_BWD, false>(p, st);
 }
 
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
@@ -557,7 +835,7 @@ hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void
   p.C = dXe; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 0, st);
-  return run_bf16<256, 128, true, false, EPI_STORE, false>(p, st);
+  return run_bf16<256, 256, 4, 2, true, false, EPI_STORE, false>(p, st);
 }
 
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
@@ -569,7 +847,7 @@ hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, 
   p.M = d; p.N = h; p.K = M; p.kv_a = M; p.kv_b = M; p.batches = E;
   p.C = dW2; p.c_bs = (long)d * h; p.ldc = h;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 0, 0, st);
-  return run_bf16<256, 128, false, false, EPI_STORE, false>(p, st);
+  return run_bf16<256, 128, 4, 2, false, false, EPI_STORE, false>(p, st);
 }
 
 hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1, void* dW3,
@@ -581,7 +859,7 @@ hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1
   p.M = 2 * h; p.N = d; p.K = M; p.kv_a = M; p.kv_b = M; p.batches = E;
   p.C = dW1; p.C2 = dW3; p.c_split = h; p.c_bs = (long)h * d; p.ldc = d;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 0, 0, st);
-  return run_bf16<256, 128, false, false, EPI_STORE, false>(p, st);
+  return run_bf16<256, 128, 4, 2, false, false, EPI_STORE, false>(p, st);
 }
 
 hipError_t launch_router_dx(int dtype, const void* dZ, const void* Wg, void* dX, int N, int E,
@@ -594,7 +872,7 @@ hipError_t launch_router_dx(int dtype, const void* dZ, const void* Wg, void* dX,
   p.C = dX; p.c_bs = 0; p.ldc = d;
   if (N == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 0, st);
-  return run_bf16<256, 128, true, false, EPI_STORE, false>(p, st);
+  return run_bf16<256, 128, 2, 2, true, false, EPI_STORE, false>(p, st);
 }
 
 int router_dwg_splits(int N, int E, int d) {
@@ -624,12 +902,12 @@ hipError_t launch_router_dwg(int dtype, const void* dZ, const void* X, float* dW
   if (last == chunk) {
     p.kv_a = chunk; p.kv_b = chunk;
     if (dtype == DT_F32) err = run_f32<EPI_STORE>(p, 0, 0, st);
-    else err = run_bf16<256, 128, false, false, EPI_STORE, true>(p, st);
+    else err = run_bf16<256, 128, 2, 2, false, false, EPI_STORE, true>(p, st);
   } else {
     GemmParams p1 = p;
     p1.batches = splits - 1; p1.kv_a = chunk; p1.kv_b = chunk;
     err = (splits > 1) ? ((dtype == DT_F32) ? run_f32<EPI_STORE>(p1, 0, 0, st)
-                                            : run_bf16<256, 128, false, false, EPI_STORE, true>(p1, st))
+                                            : run_bf16<256, 128, 2, 2, false, false, EPI_STORE, true>(p1, st))
                        : hipSuccess;
     if (err != hipSuccess) return err;
     GemmParams p2 = p;
@@ -639,7 +917,7 @@ hipError_t launch_router_dwg(int dtype, const void* dZ, const void* X, float* dW
     p2.C = part + (size_t)(splits - 1) * E * d;
     p2.batches = 1; p2.kv_a = last; p2.kv_b = last;
     err = (dtype == DT_F32) ? run_f32<EPI_STORE>(p2, 0, 0, st)
-                            : run_bf16<256, 128, false, false, EPI_STORE, true>(p2, st);
+                            : run_bf16<256, 128, 2, 2, false, false, EPI_STORE, true>(p2, st);
   }
   if (err != hipSuccess) return err;
   const long n = (long)E * d;
