@@ -3,13 +3,17 @@
 // (Section 2.2: each expert processes exactly its capacity), so the group is
 // a uniform batch of E problems; ragged per-group capacities only change M.
 //
-// bf16: v_mfma_f32_32x32x16_bf16, fp32 accumulation.  A workgroup of 4 waves
-// (2 x 2) computes a BM x BN tile; K advances in 64-wide steps through two LDS
-// buffers (padded rows, conflict-free 16-byte fragment reads) while the next
-// step's global loads are in flight.  Operands stored K-contiguous are copied
-// as 16-byte rows; operands stored M/N-contiguous (the backward's transposed
-// products) are loaded as 8 x 8 blocks and transposed in registers on their
-// way into LDS, so every MFMA fragment is one 16-byte LDS read.  Tiles are
+// bf16: one pipelined kernel (gemm_dma_kernel) for every product of the
+// forward and backward.  v_mfma_f32_32x32x16_bf16 with fp32 accumulation; a
+// 256 x 256 output tile per workgroup of 8 waves (2 per SIMD, 64 x 128 each);
+// K advances 64 at a time through a 2-stage LDS ring filled straight from
+// global memory by global_load_lds_dwordx4 (no VGPR staging).  K-contiguous
+// operands sit in LDS as 128-byte rows with XOR-swizzled 16-byte chunks
+// (conflict-free fragment reads); K-major operands (the backward's transposed
+// products) stay K-major in LDS and are read with the transposing
+// ds_read_b64_tr_b16.  Each k-step issues half its MFMAs, then the next
+// step's fragment reads (and at a stage end the barrier and the refill), then
+// the other half, so LDS latency hides behind MFMAs in flight.  Tiles are
 // numbered so that consecutive ones share an expert and stay on one XCD.
 //
 // fp32: a plain LDS-tiled FMA kernel with the same operand conventions.
@@ -19,9 +23,6 @@
 namespace ec {
 
 namespace {
-
-constexpr int GBK = 64;
-constexpr int GLDK = GBK + 8;  // padded LDS row in bf16 elements (144 bytes)
 
 enum { EPI_STORE = 0, EPI_SWIGLU = 1, EPI_SWIGLU_BWD = 2 };
 
@@ -55,337 +56,7 @@ struct GemmParams {
   int ldh;
 };
 
-// ------------------------------------------------------------------ bf16 MFMA
-
-__device__ __forceinline__ void transpose8x8(const u32x4 in[8], u32x4 out[8]) {
-  // in[kq] holds 8 bf16 along m for k = kq; out[mm] holds 8 bf16 along k for m = mm
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {       // source dword p holds m = 2p, 2p+1
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {     // dest dword q holds k = 2q, 2q+1
-      const uint32_t lo = in[2 * q][p], hi = in[2 * q + 1][p];
-      out[2 * p][q] = (lo & 0xffffu) | (hi << 16);
-      out[2 * p + 1][q] = (lo >> 16) | (hi & 0xffff0000u);
-    }
-  }
-}
-
-template <int R, bool KC, int NT>
-struct TileRegs {
-  static constexpr int N = KC ? (R * 8 + NT - 1) / NT : 8 * ((R + NT - 1) / NT);
-};
-
-// Loads one 64-wide K step of an operand tile of R rows into registers.
-//   KC:  row r (0..R) -> pointer row_ptr(r) (K-contiguous), chunk of 8 k.
-//   !KC: element (r, k) at col_base + k*ld + r, rows r >= r_valid zero.
-// K-contiguous operand: chunk c = tid + q*NT covers row c/8, k-chunk c%8.  The
-// K extent of such operands is a multiple of 64, so no K predicate is needed.
-template <int R, int NT>
-__device__ __forceinline__ void load_kc(u32x4* regs, const bf16_t* const* rowp, int k0) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int q = 0; q < TileRegs<R, true, NT>::N; ++q) {
-    const int c = tid + q * NT;
-    if (R * 8 % NT == 0 || c < R * 8)
-      regs[q] = *reinterpret_cast<const u32x4*>(rowp[q] + k0 + (c & 7) * 8);
-  }
-}
-
-template <int R, int NT>
-__device__ __forceinline__ void store_kc(bf16_t* s, const u32x4* regs) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int q = 0; q < TileRegs<R, true, NT>::N; ++q) {
-    const int c = tid + q * NT;
-    if (R * 8 % NT == 0 || c < R * 8)
-      *reinterpret_cast<u32x4*>(s + (c >> 3) * GLDK + (c & 7) * 8) = regs[q];
-  }
-}
-
-template <int R, int NT>
-__device__ __forceinline__ void store_mn(bf16_t* s, const u32x4* regs) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int q = 0; q < (R + NT - 1) / NT; ++q) {
-    const int b = tid + q * NT;
-    if (b < R) {
-      const int kb = b & 7, rc = b >> 3;
-      u32x4 t[8];
-      transpose8x8(regs + 8 * q, t);
-#pragma unroll
-      for (int mm = 0; mm < 8; ++mm)
-        *reinterpret_cast<u32x4*>(s + (rc * 8 + mm) * GLDK + kb * 8) = t[mm];
-    }
-  }
-}
-
-template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_bf16_kernel(GemmParams p) {
-  constexpr int NT = 64 * WGM * WGN;   // threads
-  constexpr int WM = BM / WGM, WN = BN / WGN;
-  constexpr int MB = WM / 32, NB = WN / 32;
-  constexpr int A_N = TileRegs<BM, A_KC, NT>::N, B_N = TileRegs<BN, B_KC, NT>::N;
-  static_assert(EPI != EPI_SWIGLU || (NB % 2 == 0), "SwiGLU needs W1 and W3 blocks per wave");
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * GLDK];
-  bf16_t* As = smem;
-  bf16_t* Bs = smem + 2 * BM * GLDK;
-
-  const int ntile = p.batches * p.MT * p.NT;
-  const int t = xcd_tile_id(blockIdx.x, gridDim.x);
-  if (t >= ntile) return;
-  const int per_b = p.MT * p.NT;
-  const int e = t / per_b;
-  const int rem = t - e * per_b;
-  const int mt = rem % p.MT, nt = rem / p.MT;
-  const int m0 = mt * BM;
-  const int n0 = (EPI == EPI_SWIGLU) ? nt * (BN / 2) : nt * BN;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave % WGM, wn = wave / WGM;
-
-  const bf16_t* Ab = reinterpret_cast<const bf16_t*>(p.A) + (size_t)e * p.a_bs;
-  const bf16_t* Bb = reinterpret_cast<const bf16_t*>(p.B) + (size_t)e * p.b_bs;
-  const bf16_t* B2b = p.B2 ? reinterpret_cast<const bf16_t*>(p.B2) + (size_t)e * p.b_bs : nullptr;
-
-  // per-thread row pointers of the K-contiguous operands (fixed over K)
-  const bf16_t* arow[A_KC ? A_N : 1];
-  const bf16_t* brow[B_KC ? B_N : 1];
-  if constexpr (A_KC) {
-#pragma unroll
-    for (int q = 0; q < A_N; ++q) {
-      int r = m0 + ((tid + q * NT) >> 3);
-      r = r < p.M ? r : p.M - 1;
-      arow[q] = Ab + (size_t)r * p.lda;
-    }
-  }
-  if constexpr (B_KC) {
-#pragma unroll
-    for (int q = 0; q < B_N; ++q) {
-      const int lr = (tid + q * NT) >> 3;
-      if constexpr (EPI == EPI_SWIGLU) {
-        const int half = lr / (BN / 2);
-        int r = n0 + lr % (BN / 2);
-        r = r < p.N ? r : p.N - 1;
-        brow[q] = (half ? B2b : Bb) + (size_t)r * p.ldb;
-      } else {
-        int r = n0 + lr;
-        r = r < p.N ? r : p.N - 1;
-        brow[q] = Bb + (size_t)r * p.ldb;
-      }
-    }
-  }
-
-  // M/N-contiguous operand: 8 x 8 block b = tid + q*NT covers k-rows kb*8.. and
-  // columns rc*8..; rows past kv (the ragged K tail) and columns past `cols` read 0.
-  auto load_mn = [&](u32x4* regs, auto src_row, int R, int r0, int cols, int k0, int kv) {
-#pragma unroll
-    for (int q = 0; q < 8 * ((R + NT - 1) / NT) / 8; ++q) {
-      const int b = tid + q * NT;
-      const int kb = b & 7, rc = b >> 3;
-      const int c = r0 + rc * 8;
-      const bool full = (k0 + GBK <= kv);
-#pragma unroll
-      for (int kq = 0; kq < 8; ++kq) {
-        const int k = k0 + kb * 8 + kq;
-        u32x4 v = u32x4{0u, 0u, 0u, 0u};
-        if ((R % NT == 0 || b < R) && (full || k < kv) && c < cols)
-          v = *reinterpret_cast<const u32x4*>(src_row(k) + c);
-        regs[8 * q + kq] = v;
-      }
-    }
-  };
-  auto load_a = [&](int k0, u32x4* regs) {
-    if constexpr (A_KC) {
-      load_kc<BM, NT>(regs, arow, k0);
-    } else {
-      load_mn(regs, [&](int k) { return Ab + (size_t)k * p.lda; }, BM, m0, p.M, k0, p.kv_a);
-    }
-  };
-  auto load_b = [&](int k0, u32x4* regs) {
-    if constexpr (B_KC) {
-      load_kc<BN, NT>(regs, brow, k0);
-    } else {
-      load_mn(regs,
-              [&](int k) {
-                return (k < p.k_split) ? Bb + (size_t)k * p.ldb
-                                       : B2b + (size_t)(k - p.k_split) * p.ldb;
-              },
-              BN, n0, p.N, k0, p.kv_b);
-    }
-  };
-  auto store_a = [&](int buf, const u32x4* regs) {
-    if constexpr (A_KC) store_kc<BM, NT>(As + buf * BM * GLDK, regs);
-    else store_mn<BM, NT>(As + buf * BM * GLDK, regs);
-  };
-  auto store_b = [&](int buf, const u32x4* regs) {
-    if constexpr (B_KC) store_kc<BN, NT>(Bs + buf * BN * GLDK, regs);
-    else store_mn<BN, NT>(Bs + buf * BN * GLDK, regs);
-  };
-
-  // LDS row of this wave's B block ni
-  auto b_lds_row = [&](int ni) -> int {
-    if constexpr (EPI == EPI_SWIGLU) {
-      constexpr int HWN = BN / 2 / WGN;  // W1 (and W3) columns per wave
-      return (ni < NB / 2) ? wn * HWN + ni * 32 : BN / 2 + wn * HWN + (ni - NB / 2) * 32;
-    } else {
-      return wn * WN + ni * 32;
-    }
-  };
-
-  f32x16 acc[MB][NB];
-#pragma unroll
-  for (int mi = 0; mi < MB; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < NB; ++ni)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
-
-  u32x4 ra[A_N], rb[B_N];
-  load_a(0, ra);
-  load_b(0, rb);
-  store_a(0, ra);
-  store_b(0, rb);
-  __syncthreads();
-
-  const int KT = (p.K + GBK - 1) / GBK;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) {
-      load_a((kt + 1) * GBK, ra);
-      load_b((kt + 1) * GBK, rb);
-    }
-    const bf16_t* as = As + buf * BM * GLDK;
-    const bf16_t* bs = Bs + buf * BN * GLDK;
-#pragma unroll
-    for (int kk = 0; kk < GBK / 16; ++kk) {
-      const int ko = kk * 16 + (lane >> 5) * 8;
-      bf16x8 af[MB], bfr[NB];
-#pragma unroll
-      for (int mi = 0; mi < MB; ++mi)
-        af[mi] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(as + (wm * WM + mi * 32 + (lane & 31)) * GLDK + ko));
-#pragma unroll
-      for (int ni = 0; ni < NB; ++ni)
-        bfr[ni] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(bs + (b_lds_row(ni) + (lane & 31)) * GLDK + ko));
-#pragma unroll
-      for (int mi = 0; mi < MB; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < NB; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
-    }
-    if (kt + 1 < KT) {
-      store_a(buf ^ 1, ra);
-      store_b(buf ^ 1, rb);
-    }
-    __syncthreads();
-  }
-
-  // ---- epilogue: stage 32-row slices of the wave tile through LDS ----
-  constexpr int SLD = WN + 4;
-  float* stage = reinterpret_cast<float*>(smem) + wave * 32 * SLD;
-#pragma unroll
-  for (int mi = 0; mi < MB; ++mi) {
-#pragma unroll
-    for (int ni = 0; ni < NB; ++ni)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        stage[row * SLD + ni * 32 + (lane & 31)] = acc[mi][ni][r];
-      }
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): staged values visible to the wave
-    __builtin_amdgcn_wave_barrier();
-    const int mbase = m0 + wm * WM + mi * 32;
-    if constexpr (EPI == EPI_STORE) {
-      constexpr int CPR = WN / 8;  // 8-wide chunks per staged row
-#pragma unroll
-      for (int q = 0; q < (32 * CPR) / 64; ++q) {
-        const int c = lane + q * 64;
-        const int row = c / CPR, cc = c % CPR;
-        const int m = mbase + row;
-        const int n = n0 + wn * WN + cc * 8;
-        if (m < p.M && n < p.N) {
-          const float* v = stage + row * SLD + cc * 8;
-          float vv[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) vv[u] = v[u];
-          const bool second = m >= p.c_split;
-          const int mm = second ? m - p.c_split : m;
-          const size_t off = (size_t)e * p.c_bs + (size_t)mm * p.ldc + n;
-          if constexpr (OUT_F32) Elem<float>::store8((float*)(second ? p.C2 : p.C) + off, vv);
-          else Elem<bf16_t>::store8((bf16_t*)(second ? p.C2 : p.C) + off, vv);
-        }
-      }
-    } else if constexpr (EPI == EPI_SWIGLU) {
-      constexpr int HW = WN / 2;    // h1 columns staged, then h3 columns
-      constexpr int CPR = HW / 8;
-#pragma unroll
-      for (int q = 0; q < (32 * CPR + 63) / 64; ++q) {
-        const int c = lane + q * 64;
-        const int row = c / CPR, cc = c % CPR;
-        const int m = mbase + row;
-        const int n = n0 + wn * HW + cc * 8;
-        if (c < 32 * CPR && m < p.M && n < p.N) {
-          const float* v1 = stage + row * SLD + cc * 8;
-          const float* v3 = v1 + HW;
-          float a[8], h1[8], h3[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            h1[u] = v1[u];
-            h3[u] = v3[u];
-            a[u] = silu_f(h1[u]) * h3[u];
-          }
-          const size_t off = (size_t)e * p.c_bs + (size_t)m * p.ldc + n;
-          Elem<bf16_t>::store8((bf16_t*)p.C + off, a);
-          if (p.H1) {
-            const size_t ho = (size_t)e * p.h_bs + (size_t)m * p.ldh + n;
-            Elem<bf16_t>::store8((bf16_t*)p.H1 + ho, h1);
-            Elem<bf16_t>::store8((bf16_t*)p.H3 + ho, h3);
-          }
-        }
-      }
-    } else {  // EPI_SWIGLU_BWD: acc = dA; dH1 -> C, dH3 -> C2
-      constexpr int CPR = WN / 8;
-#pragma unroll
-      for (int q = 0; q < (32 * CPR) / 64; ++q) {
-        const int c = lane + q * 64;
-        const int row = c / CPR, cc = c % CPR;
-        const int m = mbase + row;
-        const int n = n0 + wn * WN + cc * 8;
-        if (m < p.M && n < p.N) {
-          const float* v = stage + row * SLD + cc * 8;
-          const size_t ho = (size_t)e * p.h_bs + (size_t)m * p.ldh + n;
-          float h1[8], h3[8], d1[8], d3[8];
-          Elem<bf16_t>::load8((const bf16_t*)p.H1 + ho, h1);
-          Elem<bf16_t>::load8((const bf16_t*)p.H3 + ho, h3);
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const float da = v[u];
-            const float sg = sigmoid_f(h1[u]);
-            d3[u] = da * h1[u] * sg;
-            d1[u] = da * h3[u] * sg * (1.0f + h1[u] * (1.0f - sg));
-          }
-          const size_t off = (size_t)e * p.c_bs + (size_t)m * p.ldc + n;
-          Elem<bf16_t>::store8((bf16_t*)p.C + off, d1);
-          Elem<bf16_t>::store8((bf16_t*)p.C2 + off, d3);
-        }
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
-  }
-}
-
 // ------------------------------------------------------------------ bf16 MFMA, pipelined
-// Both operands K-contiguous (the forward products).  K advances 32 at a time
-// through a ring of STAGES LDS buffers filled directly from global memory by
-// global_load_lds_dwordx4 (no VGPR staging), STAGES-1 K steps ahead of the
-// MFMAs.  Each 64-byte LDS row holds one operand row's 32 k values as four
-// 16-byte chunks, XOR-swizzled by row so that the 32-lane fragment reads are
-// free of bank conflicts.
-
-constexpr int DBK = 32;
-
-__device__ __forceinline__ int dma_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
 
 // 16 bytes per lane from global memory straight into LDS at lds + 16 * lane.
 // (The builtin exists only for the device; the host pass must not see it or it
@@ -398,24 +69,55 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) {
 
 constexpr int vmcnt_imm(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
 
-template <int BM, int BN, int WGM, int WGN, int STAGES, int KSTEP, int EPI>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmParams p) {
+// Each operand is K-contiguous (stored [rows][K]) or K-major (stored
+// [K][rows], the backward's transposed products).  A K-major tile is kept K-major in LDS (64 rows of k, its
+// columns contiguous, 16-byte chunks XOR-swizzled by k) and read with the
+// transposing ds_read_b64_tr_b16: in each 16-lane group, lane j addresses the
+// 4 consecutive columns 4*(j%4).. of row kbase + j/4, and lane i receives
+// column i of rows kbase..kbase+3 -- two such reads make one MFMA fragment.
+// Rows past the valid K (ragged tail) and columns past the operand's width are
+// fetched from a zero block, so the MFMAs see exact zeros there.
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+__device__ __attribute__((aligned(16))) bf16_t g_zero_block[4096];  // stays zero
+
+__device__ __forceinline__ v4i16 ds_read_tr16(const char* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
+#else
+  return v4i16{0, 0, 0, 0};
+#endif
+}
+
+template <int R, bool KC, int NT>
+struct DmaOperand {
+  static constexpr int BYTES = KC ? R * 128 : 64 * R * 2;   // per stage
+  static constexpr int LOADS = R * 8 / NT;                  // 16-byte chunks per thread
+  static constexpr int CPR = R / 8;                         // chunks per K-major row
+  static_assert(R * 8 % NT == 0, "whole chunks per thread");
+  static_assert(KC || (R % 128 == 0), "K-major tiles are multiples of 128 wide");
+};
+
+__device__ __forceinline__ int kc_swz(int row) { return (row ^ (row >> 3)) & 7; }
+__device__ __forceinline__ int km_swz(int k) { return (k & 3) << 2; }
+
+template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams p) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int MB = WM / 32, NB = WN / 32;
-  constexpr int KK = KSTEP / 16;                // MFMA k-steps per stage
-  constexpr int CPR = KSTEP / 8;                // 16-byte chunks per LDS row
-  constexpr int ROWB = KSTEP * 2;               // bytes per LDS row
-  constexpr int ROWS = BM + BN;                 // LDS rows per stage (A then B)
-  constexpr int STAGE_BYTES = ROWS * ROWB;
-  constexpr int RPL = 1024 / ROWB;              // rows per 1 KiB load block
-  constexpr int LOADS = ROWS * CPR / NT;        // 16-byte chunks per thread per stage
+  constexpr int KSTEP = 64, STAGES = 2, KK = KSTEP / 16;
+  using OA = DmaOperand<BM, A_KC, NT>;
+  using OB = DmaOperand<BN, B_KC, NT>;
+  constexpr int STAGE_BYTES = OA::BYTES + OB::BYTES;
+  constexpr int LOADS = OA::LOADS + OB::LOADS;
   constexpr int SLD = WN + 4;
   constexpr int STAGE_EPI = NT / 64 * 32 * SLD * 4;
   constexpr int SMEM = STAGES * STAGE_BYTES > STAGE_EPI ? STAGES * STAGE_BYTES : STAGE_EPI;
-  static_assert(ROWS * CPR % NT == 0, "whole 16-byte chunks per thread");
-  static_assert(KSTEP == 32 || KSTEP == 64, "K step");
   static_assert(EPI != EPI_SWIGLU || (NB % 2 == 0), "SwiGLU needs W1 and W3 blocks per wave");
+  static_assert(EPI != EPI_SWIGLU || B_KC, "SwiGLU forward has K-contiguous weights");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int ntile = p.batches * p.MT * p.NT;
@@ -434,45 +136,77 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmPara
   const bf16_t* Bb = reinterpret_cast<const bf16_t*>(p.B) + (size_t)e * p.b_bs;
   const bf16_t* B2b = p.B2 ? reinterpret_cast<const bf16_t*>(p.B2) + (size_t)e * p.b_bs : nullptr;
 
-  // swizzle: physical chunk = logical chunk ^ swz(row), conflict-free 32-lane
-  // fragment reads for 32 and 64 LDS banks
-  auto swz = [](int row) -> int {
-    if constexpr (KSTEP == 32) return ((row >> 1) ^ (row >> 3)) & 3;
-    else return (row ^ (row >> 3)) & 7;
-  };
-
-  // The q-th load of this thread fills 1 KiB block (wave * LOADS + q) of a stage.
-  const bf16_t* src[LOADS];
+  // ---- DMA sources.  Load q of a thread fills 1 KiB block (wave*L + q) of
+  // the operand's stage area: 64 chunks, lane -> chunk.
+  const bf16_t* a_src[OA::LOADS];   // K-contiguous: fixed row pointer
+  int a_col[OA::LOADS], a_row[OA::LOADS];
+  const bf16_t* b_src[OB::LOADS];
+  int b_col[OB::LOADS], b_row[OB::LOADS];
 #pragma unroll
-  for (int q = 0; q < LOADS; ++q) {
-    const int row = (wave * LOADS + q) * RPL + lane / CPR;
-    const int lc = (lane % CPR) ^ swz(row);
-    const bf16_t* rp;
-    if (row < BM) {
+  for (int q = 0; q < OA::LOADS; ++q) {
+    const int id = (wave * OA::LOADS + q) * 64 + lane;
+    if constexpr (A_KC) {
+      const int row = id >> 3, lc = (id & 7) ^ kc_swz(row);
       int r = m0 + row;
       r = r < p.M ? r : p.M - 1;
-      rp = Ab + (size_t)r * p.lda;
+      a_src[q] = Ab + (size_t)r * p.lda + lc * 8;
     } else {
-      const int lr = row - BM;
+      const int row = id / OA::CPR, lc = (id % OA::CPR) ^ km_swz(row);
+      a_row[q] = row;                 // k within the step
+      a_col[q] = m0 + lc * 8;         // first column of the chunk
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < OB::LOADS; ++q) {
+    const int id = (wave * OB::LOADS + q) * 64 + lane;
+    if constexpr (B_KC) {
+      const int row = id >> 3, lc = (id & 7) ^ kc_swz(row);
+      const bf16_t* rp;
       if constexpr (EPI == EPI_SWIGLU) {
-        int r = n0 + lr % (BN / 2);
+        int r = n0 + row % (BN / 2);
         r = r < p.N ? r : p.N - 1;
-        rp = (lr < BN / 2 ? Bb : B2b) + (size_t)r * p.ldb;
+        rp = (row < BN / 2 ? Bb : B2b) + (size_t)r * p.ldb;
       } else {
-        int r = n0 + lr;
+        int r = n0 + row;
         r = r < p.N ? r : p.N - 1;
         rp = Bb + (size_t)r * p.ldb;
       }
+      b_src[q] = rp + lc * 8;
+    } else {
+      const int row = id / OB::CPR, lc = (id % OB::CPR) ^ km_swz(row);
+      b_row[q] = row;
+      b_col[q] = n0 + lc * 8;
     }
-    src[q] = rp + lc * 8;
   }
   auto issue = [&](int kt, int stage) {
-    char* base = smem + stage * STAGE_BYTES + wave * LOADS * 1024;
+    char* base = smem + stage * STAGE_BYTES;
 #pragma unroll
-    for (int q = 0; q < LOADS; ++q) dma16(src[q] + kt * KSTEP, base + q * 1024);
+    for (int q = 0; q < OA::LOADS; ++q) {
+      const bf16_t* g;
+      if constexpr (A_KC) {
+        g = a_src[q] + kt * KSTEP;
+      } else {
+        const int k = kt * KSTEP + a_row[q];
+        g = (k < p.kv_a && a_col[q] < p.M) ? Ab + (size_t)k * p.lda + a_col[q] : g_zero_block;
+      }
+      dma16(g, base + (wave * OA::LOADS + q) * 1024);
+    }
+#pragma unroll
+    for (int q = 0; q < OB::LOADS; ++q) {
+      const bf16_t* g;
+      if constexpr (B_KC) {
+        g = b_src[q] + kt * KSTEP;
+      } else {
+        const int k = kt * KSTEP + b_row[q];
+        const bf16_t* rowp = (k < p.k_split) ? Bb + (size_t)k * p.ldb
+                                             : B2b + (size_t)(k - p.k_split) * p.ldb;
+        g = (k < p.kv_b && b_col[q] < p.N) ? rowp + b_col[q] : g_zero_block;
+      }
+      dma16(g, base + OA::BYTES + (wave * OB::LOADS + q) * 1024);
+    }
   };
 
-  auto b_lds_row = [&](int ni) -> int {
+  auto b_lds_col = [&](int ni) -> int {
     if constexpr (EPI == EPI_SWIGLU) {
       constexpr int HWN = BN / 2 / WGN;
       return (ni < NB / 2) ? wn * HWN + ni * 32 : BN / 2 + wn * HWN + (ni - NB / 2) * 32;
@@ -480,31 +214,65 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmPara
       return wn * WN + ni * 32;
     }
   };
-  int aoff[MB], boff[NB], aswz[MB], bswz[NB];
+  // Fragment addressing.  K-contiguous: byte offset of the lane's row and its
+  // swizzle.  K-major: byte offset of the lane's column chunk (before the
+  // k-dependent swizzle) and the k row it starts at.
+  const int g16 = lane >> 4, j16 = lane & 15;
+  int a_off[MB], a_sw[MB], b_off[NB], b_sw[NB];
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
-    const int row = wm * WM + mi * 32 + (lane & 31);
-    aoff[mi] = row * ROWB;
-    aswz[mi] = swz(row);
+    if constexpr (A_KC) {
+      const int row = wm * WM + mi * 32 + (lane & 31);
+      a_off[mi] = row * 128;
+      a_sw[mi] = kc_swz(row);
+    } else {
+      const int col = wm * WM + mi * 32 + 16 * (g16 & 1) + 4 * (j16 & 3);
+      a_off[mi] = col >> 3;           // logical chunk
+      a_sw[mi] = (col & 7) * 2;       // byte offset inside the chunk
+    }
   }
 #pragma unroll
   for (int ni = 0; ni < NB; ++ni) {
-    const int row = BM + b_lds_row(ni) + (lane & 31);
-    boff[ni] = row * ROWB;
-    bswz[ni] = swz(row);
+    if constexpr (B_KC) {
+      const int row = b_lds_col(ni) + (lane & 31);
+      b_off[ni] = row * 128;
+      b_sw[ni] = kc_swz(row);
+    } else {
+      const int col = b_lds_col(ni) + 16 * (g16 & 1) + 4 * (j16 & 3);
+      b_off[ni] = col >> 3;
+      b_sw[ni] = (col & 7) * 2;
+    }
   }
+  const int km_k = 8 * (g16 >> 1) + (j16 >> 2);   // k row (within a 16-step) of a K-major read
+
   bf16x8 af[2][MB], bfr[2][NB];
+  auto km_frag = [&](const char* tile, int rowbytes, int chunk, int inner, int kk) -> bf16x8 {
+    const int k0 = kk * 16 + km_k, k1 = k0 + 4;
+    const v4i16 lo = ds_read_tr16(tile + k0 * rowbytes + ((chunk ^ km_swz(k0)) << 4) + inner);
+    const v4i16 hi = ds_read_tr16(tile + k1 * rowbytes + ((chunk ^ km_swz(k1)) << 4) + inner);
+    const v4i16 both[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8, both);
+  };
   auto load_frags = [&](int buf, int stage, int kk) {
-    const char* sb = smem + stage * STAGE_BYTES;
+    const char* sa = smem + stage * STAGE_BYTES;
+    const char* sbb = sa + OA::BYTES;
     const int lc = kk * 2 + (lane >> 5);
 #pragma unroll
-    for (int mi = 0; mi < MB; ++mi)
-      af[buf][mi] = __builtin_bit_cast(
-          bf16x8, *reinterpret_cast<const u32x4*>(sb + aoff[mi] + ((lc ^ aswz[mi]) << 4)));
+    for (int mi = 0; mi < MB; ++mi) {
+      if constexpr (A_KC)
+        af[buf][mi] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(sa + a_off[mi] + ((lc ^ a_sw[mi]) << 4)));
+      else
+        af[buf][mi] = km_frag(sa, BM * 2, a_off[mi], a_sw[mi], kk);
+    }
 #pragma unroll
-    for (int ni = 0; ni < NB; ++ni)
-      bfr[buf][ni] = __builtin_bit_cast(
-          bf16x8, *reinterpret_cast<const u32x4*>(sb + boff[ni] + ((lc ^ bswz[ni]) << 4)));
+    for (int ni = 0; ni < NB; ++ni) {
+      if constexpr (B_KC)
+        bfr[buf][ni] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(sbb + b_off[ni] + ((lc ^ b_sw[ni]) << 4)));
+      else
+        bfr[buf][ni] = km_frag(sbb, BN * 2, b_off[ni], b_sw[ni], kk);
+    }
   };
 
   f32x16 acc[MB][NB];
@@ -515,38 +283,15 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmPara
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
 
-  // Waits until this wave's loads of K step `kt` have landed, given how many
-  // younger steps have been issued after it.
-  auto wait_step = [&](int kt, int KT) {
-    const int younger = KT - 1 - kt < STAGES - 2 ? KT - 1 - kt : STAGES - 2;
-    static_assert(STAGES <= 5, "wait cases");
-    if (younger >= 3) __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * LOADS));
-    else if (younger == 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));
-    else if (younger == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
-    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-  };
-
-  // Ring: steps 0..STAGES-1 are issued up front; the end of step kt refills
-  // stage kt % STAGES with step kt + STAGES once every wave has read it.  When
-  // waiting for step j, the steps issued after it number
-  // min(STAGES-1, KT-1-j) for j = 0 and min(STAGES-2, KT-1-j) afterwards.
-  const int KT = p.K / KSTEP;
-#pragma unroll
-  for (int s = 0; s < STAGES; ++s)
-    if (s < KT) issue(s, s);
+  const int KT = (p.K + KSTEP - 1) / KSTEP;
+  if (KT > 0) issue(0, 0);
+  if (KT > 1) issue(1, 1);
   if (KT > 0) {
-    const int younger = KT - 1 < STAGES - 1 ? KT - 1 : STAGES - 1;
-    if (younger >= 3) __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * LOADS));
-    else if (younger == 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));
-    else if (younger == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
+    if (KT > 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
     else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     __builtin_amdgcn_s_barrier();
     load_frags(0, 0, 0);
   }
-  // Each k-step: the first half of its MFMAs, then the next k-step's fragment
-  // reads (at a stage end: the barrier, the refill of this stage and the next
-  // stage's first fragments), then the second half, so that the LDS latency
-  // is covered by MFMAs already in flight.
   constexpr int NMF = MB * NB;
   auto mfma_range = [&](int cur, int lo, int hi) {
 #pragma unroll
@@ -558,7 +303,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmPara
     }
   };
   for (int kt = 0; kt < KT; ++kt) {
-    const int stage = kt % STAGES;
+    const int stage = kt & 1;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int cur = kk & 1;
@@ -567,13 +312,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmPara
       if (kk + 1 < KK) {
         load_frags(cur ^ 1, stage, kk + 1);
       } else {
-        // after the final step this reads a stale stage, harmlessly, which
-        // keeps the loop body uniform
         __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): this wave's reads are done
-        if (kt + 1 < KT) wait_step(kt + 1, KT);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
         __builtin_amdgcn_s_barrier();
         if (kt + STAGES < KT) issue(kt + STAGES, stage);
-        load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
+        load_frags(cur ^ 1, stage ^ 1, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
       mfma_range(cur, NMF / 2, NMF);
@@ -583,7 +326,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmPara
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   __syncthreads();
 
-  // ---- epilogue (same as gemm_bf16_kernel) ----
+  // ---- epilogue: stage 32-row slices of the wave tile through LDS ----
   float* stage_f = reinterpret_cast<float*>(smem) + wave * 32 * SLD;
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
@@ -610,10 +353,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmPara
           float vv[8];
 #pragma unroll
           for (int u = 0; u < 8; ++u) vv[u] = v[u];
-          Elem<bf16_t>::store8((bf16_t*)p.C + (size_t)e * p.c_bs + (size_t)m * p.ldc + n, vv);
+          const bool second = m >= p.c_split;
+          const int mm = second ? m - p.c_split : m;
+          const size_t off = (size_t)e * p.c_bs + (size_t)mm * p.ldc + n;
+          if constexpr (OUT_F32) Elem<float>::store8((float*)(second ? p.C2 : p.C) + off, vv);
+          else Elem<bf16_t>::store8((bf16_t*)(second ? p.C2 : p.C) + off, vv);
         }
       }
-    } else {
+    } else if constexpr (EPI == EPI_SWIGLU) {
       constexpr int HW = WN / 2;
       constexpr int CPR = HW / 8;
 #pragma unroll
@@ -640,31 +387,45 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_nt_dma_kernel(GemmPara
           }
         }
       }
+    } else {  // EPI_SWIGLU_BWD
+      constexpr int CPR = WN / 8;
+#pragma unroll
+      for (int q = 0; q < (32 * CPR) / 64; ++q) {
+        const int c = lane + q * 64;
+        const int row = c / CPR, cc = c % CPR;
+        const int m = mbase + row;
+        const int n = n0 + wn * WN + cc * 8;
+        if (m < p.M && n < p.N) {
+          const float* v = stage_f + row * SLD + cc * 8;
+          const size_t ho = (size_t)e * p.h_bs + (size_t)m * p.ldh + n;
+          float h1[8], h3[8], d1[8], d3[8];
+          Elem<bf16_t>::load8((const bf16_t*)p.H1 + ho, h1);
+          Elem<bf16_t>::load8((const bf16_t*)p.H3 + ho, h3);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const float da = v[u];
+            const float sg = sigmoid_f(h1[u]);
+            d3[u] = da * h1[u] * sg;
+            d1[u] = da * h3[u] * sg * (1.0f + h1[u] * (1.0f - sg));
+          }
+          const size_t off = (size_t)e * p.c_bs + (size_t)m * p.ldc + n;
+          Elem<bf16_t>::store8((bf16_t*)p.C + off, d1);
+          Elem<bf16_t>::store8((bf16_t*)p.C2 + off, d3);
+        }
+      }
     }
     __builtin_amdgcn_wave_barrier();
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int STAGES, int KSTEP, int EPI>
-hipError_t run_nt_dma(GemmParams p, hipStream_t st) {
-  p.MT = (p.M + BM - 1) / BM;
-  p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
-  const long ntile = (long)p.batches * p.MT * p.NT;
-  if (ntile == 0) return hipSuccess;
-  const long grid = (ntile + 7) / 8 * 8;
-  gemm_nt_dma_kernel<BM, BN, WGM, WGN, STAGES, KSTEP, EPI>
-      <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
-  return hipGetLastError();
-}
-
 template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
-hipError_t run_bf16(GemmParams p, hipStream_t st) {
+hipError_t run_dma(GemmParams p, hipStream_t st) {
   p.MT = (p.M + BM - 1) / BM;
   p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
   const long ntile = (long)p.batches * p.MT * p.NT;
   if (ntile == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
-  gemm_bf16_kernel<BM, BN, WGM, WGN, A_KC, B_KC, EPI, OUT_F32>
+  gemm_dma_kernel<BM, BN, WGM, WGN, A_KC, B_KC, EPI, OUT_F32>
       <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
   return hipGetLastError();
 }
@@ -795,7 +556,7 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
   p.H1 = H1; p.H3 = H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU>(p, 1, 1, st);
-  return run_nt_dma<256, 256, 4, 2, 2, 64, EPI_SWIGLU>(p, st);
+  return run_dma<256, 256, 4, 2, true, true, EPI_SWIGLU, false>(p, st);
 }
 
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
@@ -807,7 +568,7 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
   p.C = O; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
-  return run_nt_dma<256, 256, 4, 2, 2, 64, EPI_STORE>(p, st);
+  return run_dma<256, 256, 4, 2, true, true, EPI_STORE, false>(p, st);
 }
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
@@ -822,7 +583,7 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
   p.H1 = (void*)H1; p.H3 = (void*)H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
-  return run_bf16<256, 256, 4, 2, true, false, EPI_SWIGLU_BWD, false>(p, st);
+  return run_dma<256, 256, 4, 2, true, false, EPI_SWIGLU_BWD, false>(p, st);
 }
 
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
@@ -835,7 +596,7 @@ hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void
   p.C = dXe; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 0, st);
-  return run_bf16<256, 256, 4, 2, true, false, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, true, false, EPI_STORE, false>(p, st);
 }
 
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
@@ -847,7 +608,7 @@ hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, 
   p.M = d; p.N = h; p.K = M; p.kv_a = M; p.kv_b = M; p.batches = E;
   p.C = dW2; p.c_bs = (long)d * h; p.ldc = h;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 0, 0, st);
-  return run_bf16<256, 128, 4, 2, false, false, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, false, false, EPI_STORE, false>(p, st);
 }
 
 hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1, void* dW3,
@@ -859,7 +620,7 @@ hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1
   p.M = 2 * h; p.N = d; p.K = M; p.kv_a = M; p.kv_b = M; p.batches = E;
   p.C = dW1; p.C2 = dW3; p.c_split = h; p.c_bs = (long)h * d; p.ldc = d;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 0, 0, st);
-  return run_bf16<256, 128, 4, 2, false, false, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, false, false, EPI_STORE, false>(p, st);
 }
 
 hipError_t launch_router_dx(int dtype, const void* dZ, const void* Wg, void* dX, int N, int E,
@@ -872,7 +633,7 @@ hipError_t launch_router_dx(int dtype, const void* dZ, const void* Wg, void* dX,
   p.C = dX; p.c_bs = 0; p.ldc = d;
   if (N == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 0, st);
-  return run_bf16<256, 128, 2, 2, true, false, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, true, false, EPI_STORE, false>(p, st);
 }
 
 int router_dwg_splits(int N, int E, int d) {
@@ -902,12 +663,12 @@ hipError_t launch_router_dwg(int dtype, const void* dZ, const void* X, float* dW
   if (last == chunk) {
     p.kv_a = chunk; p.kv_b = chunk;
     if (dtype == DT_F32) err = run_f32<EPI_STORE>(p, 0, 0, st);
-    else err = run_bf16<256, 128, 2, 2, false, false, EPI_STORE, true>(p, st);
+    else err = run_dma<128, 256, 2, 4, false, false, EPI_STORE, true>(p, st);
   } else {
     GemmParams p1 = p;
     p1.batches = splits - 1; p1.kv_a = chunk; p1.kv_b = chunk;
     err = (splits > 1) ? ((dtype == DT_F32) ? run_f32<EPI_STORE>(p1, 0, 0, st)
-                                            : run_bf16<256, 128, 2, 2, false, false, EPI_STORE, true>(p1, st))
+                                            : run_dma<128, 256, 2, 4, false, false, EPI_STORE, true>(p1, st))
                        : hipSuccess;
     if (err != hipSuccess) return err;
     GemmParams p2 = p;
@@ -917,7 +678,7 @@ hipError_t launch_router_dwg(int dtype, const void* dZ, const void* X, float* dW
     p2.C = part + (size_t)(splits - 1) * E * d;
     p2.batches = 1; p2.kv_a = last; p2.kv_b = last;
     err = (dtype == DT_F32) ? run_f32<EPI_STORE>(p2, 0, 0, st)
-                            : run_bf16<256, 128, 2, 2, false, false, EPI_STORE, true>(p2, st);
+                            : run_dma<128, 256, 2, 4, false, false, EPI_STORE, true>(p2, st);
   }
   if (err != hipSuccess) return err;
   const long n = (long)E * d;
