@@ -12,8 +12,11 @@ storage, forward + backward.  Prints ONE JSON line on stdout.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
+import sqlite3
 import sys
 import time
 
@@ -28,6 +31,65 @@ PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 GEMM_STAGES = {"gemm_w13_swiglu", "gemm_w2", "gemm_dA_swiglu_bwd", "gemm_dW2", "gemm_dXe",
                "gemm_dW13", "router_dx", "router_dwg"}
+
+
+# kernel-symbol stage tags of the grouped GEMMs (gemm_dma_kernel's last template argument)
+GEMM_TAGS = {"gemm_w13_swiglu": 1, "gemm_w2": 2, "gemm_dA_swiglu_bwd": 3, "gemm_dXe": 4,
+             "gemm_dW2": 5, "gemm_dW13": 6, "router_dx": 7, "router_dwg": 8}
+KERNEL_SOURCES = ["paper_2604_01622_amd/csrc/gemm.hip", "paper_2604_01622_amd/csrc/ec_common.h"]
+CALIB_BYTES = 1 << 30   # plain elementwise copy used to scale the byte counters
+
+
+def sources_hash():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stage_of_kernel(name):
+    m = re.search(r"gemm_dma_kernel<.*, (\d+)>\(", name)
+    if not m:
+        return None
+    tag = int(m.group(1))
+    return next((k for k, v in GEMM_TAGS.items() if v == tag), None)
+
+
+def pmc_per_dispatch(db, counter):
+    """{kernel name: [value per dispatch]} for one counter of a rocprofv3 --pmc database."""
+    c = sqlite3.connect(db)
+    out = {}
+    for name, did, v in c.execute(
+            "select name, dispatch_id, sum(counter_value) from pmc_events where counter_name = ? "
+            "group by name, dispatch_id order by dispatch_id", (counter,)):
+        out.setdefault(name, []).append(v)
+    return out
+
+
+def traffic_from(fetch_db, write_db, workload):
+    """Turns two --pmc runs of this benchmark (FETCH_SIZE, WRITE_SIZE) into per-launch HBM
+    bytes of every GEMM stage, scaled by what the counters read for the calibration copy."""
+    fetch = pmc_per_dispatch(fetch_db, "FETCH_SIZE")
+    write = pmc_per_dispatch(write_db, "WRITE_SIZE")
+    def calib(d):
+        vals = [v for n, vs in d.items() if "neg" in n.lower() for v in vs]
+        if not vals:
+            raise SystemExit("calibration copy not found in the counter database")
+        return CALIB_BYTES / (sum(vals) / len(vals) * 1024.0)
+    f_fetch, f_write = calib(fetch), calib(write)
+    recs = {}
+    for name, vals in fetch.items():
+        st = stage_of_kernel(name)
+        if st is None or name not in write:
+            continue
+        fb = sum(vals) / len(vals) * 1024.0 * f_fetch
+        wb = sum(write[name]) / len(write[name]) * 1024.0 * f_write
+        recs[st] = {"stage": st, "kernel": name, "fetch_bytes": fb, "write_bytes": wb,
+                    "traffic_bytes": fb + wb, "fetch_scale": f_fetch, "write_scale": f_write,
+                    "dispatches": len(vals), "sources_sha256_16": sources_hash(),
+                    "workload": workload}
+    return recs
 
 
 def log(*a):
@@ -59,8 +121,10 @@ def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits):
     return table[name]
 
 
-def cpu_baseline(inp, caps, inv_tau, backward):
-    """The float64 oracle on a bounded sample (the first routing group) on the host cores."""
+def cpu_baseline(inp, caps, inv_tau, backward, budget_s=10.0):
+    """The float64 oracle on a bounded sample: whole routing groups (sequences), one at a
+    time in order, until the budget is spent; each group is routed on its own, exactly as
+    in the layer (routing never crosses a group)."""
     from oracle import ec_ref as ref
     try:
         from threadpoolctl import threadpool_info
@@ -68,20 +132,26 @@ def cpu_baseline(inp, caps, inv_tau, backward):
     except Exception:  # pragma: no cover
         blas_threads = len(os.sched_getaffinity(0))
     wl = inp.wl
-    L0 = wl.group_lengths[0]
-    X = inp.X[:L0]
-    off = np.array([0, L0])
-    k = [int(caps[0])]
-    t0 = time.perf_counter()
-    fw = ref.forward_ref(X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, inv_tau)
-    if backward:
-        ref.backward_ref(X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY[:L0], off, k, inv_tau,
-                         sel_token=fw["sel_token"])
-    dt = time.perf_counter() - t0
-    return {"value": L0 / dt, "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
-            "sample": f"routing group 0 of {wl.n_groups} ({L0} tokens, k={k[0]}, all "
-                      f"{wl.n_experts} experts), {'fwd+bwd' if backward else 'fwd'}, "
-                      f"numpy float64, {dt:.1f} s",
+    off = wl.group_offsets
+    tokens, dt, groups = 0, 0.0, 0
+    for g in range(wl.n_groups):
+        lo, hi = int(off[g]), int(off[g + 1])
+        X = inp.X[lo:hi]
+        t0 = time.perf_counter()
+        fw = ref.forward_ref(X, inp.Wg, inp.W1, inp.W3, inp.W2, [0, hi - lo], [int(caps[g])],
+                             inv_tau)
+        if backward:
+            ref.backward_ref(X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY[lo:hi], [0, hi - lo],
+                             [int(caps[g])], inv_tau, sel_token=fw["sel_token"])
+        dt += time.perf_counter() - t0
+        tokens += hi - lo
+        groups += 1
+        if dt >= budget_s:
+            break
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
+            "sample": f"routing groups 0..{groups - 1} of {wl.n_groups} ({tokens} tokens, all "
+                      f"{wl.n_experts} experts), {'fwd+bwd' if backward else 'fwd'}, numpy float64, "
+                      f"{dt:.1f} s",
             "seconds": dt}
 
 
@@ -94,7 +164,19 @@ def main():
                     choices=["train", "static", "timestep", "fine", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forward-only", action="store_true")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="run one plain 1 GiB elementwise copy first (scales --pmc byte counters)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
+                    help="write profiles/traffic_<stage>.json from two --pmc runs and exit")
     a = ap.parse_args()
+    if a.traffic_from:
+        recs = traffic_from(a.traffic_from[0], a.traffic_from[1], a.workload)
+        for st, r in recs.items():
+            with open(os.path.join(ROOT, "profiles", f"traffic_{st}.json"), "w") as f:
+                json.dump(r, f, indent=1)
+            print(f"{st}: fetch {r['fetch_bytes'] / 1e9:.3f} GB write {r['write_bytes'] / 1e9:.3f} GB "
+                  f"per launch")
+        return
     if a.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {a.gpus} is not supported (the layer's "
               "multi-GPU sharding is a design, not part of this build)", file=sys.stderr)
@@ -134,6 +216,13 @@ def main():
         layer.forward()
         if backward:
             layer.backward(dY)
+
+    if a.calibration_copy:
+        src = torch.ones(CALIB_BYTES // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)   # reads and writes CALIB_BYTES
+        torch.cuda.synchronize()
+        del src, dst
 
     log(f"[bench] warmup {a.warmup}")
     for _ in range(a.warmup):
@@ -178,15 +267,22 @@ def main():
     dom = max(stage_ms, key=stage_ms.get)
     fl, by = stage_work(dom, N, d, E, h, K, esz, EP, backward, splits)
     t_dom = stage_ms[dom] * 1e-3
+    traffic = None
+    tf = os.path.join(ROOT, "profiles", f"traffic_{dom}.json")
+    if os.path.exists(tf):
+        with open(tf) as f:
+            rec = json.load(f)
+        if rec.get("sources_sha256_16") == sources_hash() and rec.get("workload") == a.workload:
+            traffic = round(rec["traffic_bytes"])
     if dom in GEMM_STAGES:
         peak = PEAK_BF16_TFLOPS if esz == 2 else PEAK_F32_TFLOPS
         roof = {"kernel": dom, "bound": "mfma", "achieved": round(fl / t_dom / 1e12, 1),
                 "peak": peak, "unit": "TFLOP/s", "frac": round(fl / t_dom / 1e12 / peak, 4),
-                "traffic": None, "work_per_launch": fl, "avg_launch_ms": round(stage_ms[dom], 4)}
+                "traffic": traffic, "work_per_launch": fl, "avg_launch_ms": round(stage_ms[dom], 4)}
     else:
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(by / t_dom / 1e9, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(by / t_dom / 1e9 / PEAK_HBM_GBS, 4),
-                "traffic": None, "work_per_launch": by, "avg_launch_ms": round(stage_ms[dom], 4)}
+                "traffic": traffic, "work_per_launch": by, "avg_launch_ms": round(stage_ms[dom], 4)}
     gemm_fl = sum(stage_work(n, N, d, E, h, K, esz, EP, backward, splits)[0]
                   for n in stage_ms if n.startswith("gemm_"))
     gemm_ms = sum(stage_ms[n] for n in stage_ms if n.startswith("gemm_"))

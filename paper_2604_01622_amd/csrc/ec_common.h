@@ -31,6 +31,16 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 template <typename T> struct Elem;
 
 template <> struct Elem<float> {
+  struct Raw { float4 a, b; };
+  static __device__ __forceinline__ Raw load_raw(const float* p) {
+    return Raw{*reinterpret_cast<const float4*>(p), *reinterpret_cast<const float4*>(p + 4)};
+  }
+  static __device__ __forceinline__ void fma_raw(float acc[8], float g, const Raw& r) {
+    acc[0] = fmaf(g, r.a.x, acc[0]); acc[1] = fmaf(g, r.a.y, acc[1]);
+    acc[2] = fmaf(g, r.a.z, acc[2]); acc[3] = fmaf(g, r.a.w, acc[3]);
+    acc[4] = fmaf(g, r.b.x, acc[4]); acc[5] = fmaf(g, r.b.y, acc[5]);
+    acc[6] = fmaf(g, r.b.z, acc[6]); acc[7] = fmaf(g, r.b.w, acc[7]);
+  }
   static __device__ __forceinline__ void load8(const float* p, float v[8]) {
     const float4 a = *reinterpret_cast<const float4*>(p);
     const float4 b = *reinterpret_cast<const float4*>(p + 4);
@@ -46,6 +56,16 @@ template <> struct Elem<float> {
 };
 
 template <> struct Elem<bf16_t> {
+  typedef uint4 Raw;
+  static __device__ __forceinline__ Raw load_raw(const bf16_t* p) {
+    return *reinterpret_cast<const uint4*>(p);
+  }
+  static __device__ __forceinline__ void fma_raw(float acc[8], float g, const Raw& r) {
+    acc[0] = fmaf(g, bf16_to_f32(r.x & 0xffffu), acc[0]); acc[1] = fmaf(g, bf16_to_f32(r.x >> 16), acc[1]);
+    acc[2] = fmaf(g, bf16_to_f32(r.y & 0xffffu), acc[2]); acc[3] = fmaf(g, bf16_to_f32(r.y >> 16), acc[3]);
+    acc[4] = fmaf(g, bf16_to_f32(r.z & 0xffffu), acc[4]); acc[5] = fmaf(g, bf16_to_f32(r.z >> 16), acc[5]);
+    acc[6] = fmaf(g, bf16_to_f32(r.w & 0xffffu), acc[6]); acc[7] = fmaf(g, bf16_to_f32(r.w >> 16), acc[7]);
+  }
   static __device__ __forceinline__ void load8(const bf16_t* p, float v[8]) {
     const uint4 a = *reinterpret_cast<const uint4*>(p);
     v[0] = bf16_to_f32(a.x & 0xffffu); v[1] = bf16_to_f32(a.x >> 16);

@@ -26,6 +26,10 @@ namespace {
 
 enum { EPI_STORE = 0, EPI_SWIGLU = 1, EPI_SWIGLU_BWD = 2 };
 
+// Stage tags: every product gets its own kernel symbol, so that traces and
+// counters attribute each launch to its stage.
+enum { G_W13 = 1, G_W2, G_DA, G_DXE, G_DW2, G_DW13, G_ROUTER_DX, G_ROUTER_DWG };
+
 struct GemmParams {
   // A operand, element (m, k) of batch e:
   //   K-contiguous:  A[e*a_bs + m*lda + k];   M-contiguous: A[e*a_bs + k*lda + m]
@@ -91,38 +95,40 @@ __device__ __forceinline__ v4i16 ds_read_tr16(const char* p) {
 #endif
 }
 
-template <int R, bool KC, int NT>
+template <int R, bool KC, int NT, int KSTEP>
 struct DmaOperand {
-  static constexpr int BYTES = KC ? R * 128 : 64 * R * 2;   // per stage
-  static constexpr int LOADS = R * 8 / NT;                  // 16-byte chunks per thread
-  static constexpr int CPR = R / 8;                         // chunks per K-major row
-  static_assert(R * 8 % NT == 0, "whole chunks per thread");
+  static constexpr int BYTES = R * KSTEP * 2;               // per stage
+  static constexpr int LOADS = R * KSTEP / 8 / NT;          // 16-byte chunks per thread
+  static constexpr int CPR = KC ? KSTEP / 8 : R / 8;        // chunks per LDS row
+  static_assert(R * KSTEP / 8 % NT == 0, "whole chunks per thread");
   static_assert(KC || (R % 128 == 0), "K-major tiles are multiples of 128 wide");
 };
 
-__device__ __forceinline__ int kc_swz(int row) { return (row ^ (row >> 3)) & 7; }
+// Chunk swizzles, chosen by measuring the fragment-read pattern on gfx950:
+// K-contiguous rows of 64 or 128 bytes, and K-major rows (by k).
+template <int KSTEP>
+__device__ __forceinline__ int kc_swz(int row) {
+  if constexpr (KSTEP == 64) return (row ^ (row >> 3)) & 7;
+  else return ((row >> 1) ^ (row >> 2)) & 3;
+}
 __device__ __forceinline__ int km_swz(int k) { return (k & 3) << 2; }
 
-template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
-__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams p) {
+template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
+          bool OUT_F32>
+__device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* smem) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int MB = WM / 32, NB = WN / 32;
-  constexpr int KSTEP = 64, STAGES = 2, KK = KSTEP / 16;
-  using OA = DmaOperand<BM, A_KC, NT>;
-  using OB = DmaOperand<BN, B_KC, NT>;
+  constexpr int KK = KSTEP / 16;
+  static_assert(KSTEP == 32 || KSTEP == 64, "K step");
+  static_assert(STAGES >= 2 && STAGES <= 5, "ring depth");
+  using OA = DmaOperand<BM, A_KC, NT, KSTEP>;
+  using OB = DmaOperand<BN, B_KC, NT, KSTEP>;
   constexpr int STAGE_BYTES = OA::BYTES + OB::BYTES;
   constexpr int LOADS = OA::LOADS + OB::LOADS;
   constexpr int SLD = WN + 4;
-  constexpr int STAGE_EPI = NT / 64 * 32 * SLD * 4;
-  constexpr int SMEM = STAGES * STAGE_BYTES > STAGE_EPI ? STAGES * STAGE_BYTES : STAGE_EPI;
   static_assert(EPI != EPI_SWIGLU || (NB % 2 == 0), "SwiGLU needs W1 and W3 blocks per wave");
   static_assert(EPI != EPI_SWIGLU || B_KC, "SwiGLU forward has K-contiguous weights");
-  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-
-  const int ntile = p.batches * p.MT * p.NT;
-  const int t = xcd_tile_id(blockIdx.x, gridDim.x);
-  if (t >= ntile) return;
   const int per_b = p.MT * p.NT;
   const int e = t / per_b;
   const int rem = t - e * per_b;
@@ -146,7 +152,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
   for (int q = 0; q < OA::LOADS; ++q) {
     const int id = (wave * OA::LOADS + q) * 64 + lane;
     if constexpr (A_KC) {
-      const int row = id >> 3, lc = (id & 7) ^ kc_swz(row);
+      const int row = id / OA::CPR, lc = (id % OA::CPR) ^ kc_swz<KSTEP>(row);
       int r = m0 + row;
       r = r < p.M ? r : p.M - 1;
       a_src[q] = Ab + (size_t)r * p.lda + lc * 8;
@@ -160,7 +166,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
   for (int q = 0; q < OB::LOADS; ++q) {
     const int id = (wave * OB::LOADS + q) * 64 + lane;
     if constexpr (B_KC) {
-      const int row = id >> 3, lc = (id & 7) ^ kc_swz(row);
+      const int row = id / OB::CPR, lc = (id % OB::CPR) ^ kc_swz<KSTEP>(row);
       const bf16_t* rp;
       if constexpr (EPI == EPI_SWIGLU) {
         int r = n0 + row % (BN / 2);
@@ -223,8 +229,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
   for (int mi = 0; mi < MB; ++mi) {
     if constexpr (A_KC) {
       const int row = wm * WM + mi * 32 + (lane & 31);
-      a_off[mi] = row * 128;
-      a_sw[mi] = kc_swz(row);
+      a_off[mi] = row * KSTEP * 2;
+      a_sw[mi] = kc_swz<KSTEP>(row);
     } else {
       const int col = wm * WM + mi * 32 + 16 * (g16 & 1) + 4 * (j16 & 3);
       a_off[mi] = col >> 3;           // logical chunk
@@ -235,8 +241,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
   for (int ni = 0; ni < NB; ++ni) {
     if constexpr (B_KC) {
       const int row = b_lds_col(ni) + (lane & 31);
-      b_off[ni] = row * 128;
-      b_sw[ni] = kc_swz(row);
+      b_off[ni] = row * KSTEP * 2;
+      b_sw[ni] = kc_swz<KSTEP>(row);
     } else {
       const int col = b_lds_col(ni) + 16 * (g16 & 1) + 4 * (j16 & 3);
       b_off[ni] = col >> 3;
@@ -283,12 +289,24 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
 
-  const int KT = (p.K + KSTEP - 1) / KSTEP;
-  if (KT > 0) issue(0, 0);
-  if (KT > 1) issue(1, 1);
-  if (KT > 0) {
-    if (KT > 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
+  // Ring: steps 0..STAGES-1 are issued up front; the end of step kt refills
+  // stage kt % STAGES with step kt + STAGES once every wave has read it.  When
+  // waiting for step j, the steps issued after it number min(STAGES-1, KT-1-j)
+  // for j = 0 and min(STAGES-2, KT-1-j) afterwards (vmcnt counts this wave's
+  // outstanding loads, which complete in order).
+  auto wait_younger = [&](int younger) {
+    if (younger >= 3) __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * LOADS));
+    else if (younger == 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));
+    else if (younger == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
     else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  };
+  static_assert(3 * LOADS <= 63, "vmcnt range");
+  const int KT = (p.K + KSTEP - 1) / KSTEP;
+#pragma unroll
+  for (int s2 = 0; s2 < STAGES; ++s2)
+    if (s2 < KT) issue(s2, s2);
+  if (KT > 0) {
+    wait_younger(KT - 1 < STAGES - 1 ? KT - 1 : STAGES - 1);
     __builtin_amdgcn_s_barrier();
     load_frags(0, 0, 0);
   }
@@ -303,7 +321,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
     }
   };
   for (int kt = 0; kt < KT; ++kt) {
-    const int stage = kt & 1;
+    const int stage = kt % STAGES;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int cur = kk & 1;
@@ -312,11 +330,13 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
       if (kk + 1 < KK) {
         load_frags(cur ^ 1, stage, kk + 1);
       } else {
+        // after the final step this reads a stale stage, harmlessly, which
+        // keeps the loop body uniform
         __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): this wave's reads are done
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        if (kt + 1 < KT) wait_younger(KT - 2 - kt < STAGES - 2 ? KT - 2 - kt : STAGES - 2);
         __builtin_amdgcn_s_barrier();
         if (kt + STAGES < KT) issue(kt + STAGES, stage);
-        load_frags(cur ^ 1, stage ^ 1, 0);
+        load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
       mfma_range(cur, NMF / 2, NMF);
@@ -418,14 +438,36 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, bool A_KC, bool B_KC, int EPI, bool OUT_F32>
+// smem bytes of gemm_dma_tile's configuration
+template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC>
+constexpr int dma_smem_bytes() {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int STAGE_BYTES = (BM + BN) * KSTEP * 2;
+  constexpr int STAGE_EPI = NT / 64 * 32 * (BN / WGN + 4) * 4;
+  return STAGES * STAGE_BYTES > STAGE_EPI ? STAGES * STAGE_BYTES : STAGE_EPI;
+}
+
+// One output tile per workgroup; consecutive tile ids (same expert) are kept
+// on one XCD so that its L2 serves their shared A rows and B columns.
+template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
+          bool OUT_F32, int TAG>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(1024)))
+  char smem[dma_smem_bytes<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC>()];
+  const int t = xcd_tile_id(blockIdx.x, gridDim.x);
+  if (t >= p.batches * p.MT * p.NT) return;
+  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32>(p, t, smem);
+}
+
+template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
+          bool OUT_F32, int TAG>
 hipError_t run_dma(GemmParams p, hipStream_t st) {
   p.MT = (p.M + BM - 1) / BM;
   p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
   const long ntile = (long)p.batches * p.MT * p.NT;
   if (ntile == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
-  gemm_dma_kernel<BM, BN, WGM, WGN, A_KC, B_KC, EPI, OUT_F32>
+  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG>
       <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
   return hipGetLastError();
 }
@@ -556,7 +598,7 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
   p.H1 = H1; p.H3 = H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU>(p, 1, 1, st);
-  return run_dma<256, 256, 4, 2, true, true, EPI_SWIGLU, false>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
 }
 
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
@@ -568,7 +610,7 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
   p.C = O; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
-  return run_dma<256, 256, 4, 2, true, true, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
 }
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
@@ -583,7 +625,7 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
   p.H1 = (void*)H1; p.H3 = (void*)H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
-  return run_dma<256, 256, 4, 2, true, false, EPI_SWIGLU_BWD, false>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_DA>(p, st);
 }
 
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
@@ -596,7 +638,7 @@ hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void
   p.C = dXe; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 0, st);
-  return run_dma<256, 256, 4, 2, true, false, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE, false, G_DXE>(p, st);
 }
 
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
@@ -608,7 +650,7 @@ hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, 
   p.M = d; p.N = h; p.K = M; p.kv_a = M; p.kv_b = M; p.batches = E;
   p.C = dW2; p.c_bs = (long)d * h; p.ldc = h;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 0, 0, st);
-  return run_dma<256, 256, 4, 2, false, false, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, false, false, EPI_STORE, false, G_DW2>(p, st);
 }
 
 hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1, void* dW3,
@@ -620,7 +662,7 @@ hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1
   p.M = 2 * h; p.N = d; p.K = M; p.kv_a = M; p.kv_b = M; p.batches = E;
   p.C = dW1; p.C2 = dW3; p.c_split = h; p.c_bs = (long)h * d; p.ldc = d;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 0, 0, st);
-  return run_dma<256, 256, 4, 2, false, false, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, false, false, EPI_STORE, false, G_DW13>(p, st);
 }
 
 hipError_t launch_router_dx(int dtype, const void* dZ, const void* Wg, void* dX, int N, int E,
@@ -633,7 +675,7 @@ hipError_t launch_router_dx(int dtype, const void* dZ, const void* Wg, void* dX,
   p.C = dX; p.c_bs = 0; p.ldc = d;
   if (N == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 0, st);
-  return run_dma<256, 256, 4, 2, true, false, EPI_STORE, false>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE, false, G_ROUTER_DX>(p, st);
 }
 
 int router_dwg_splits(int N, int E, int d) {
@@ -663,12 +705,12 @@ hipError_t launch_router_dwg(int dtype, const void* dZ, const void* X, float* dW
   if (last == chunk) {
     p.kv_a = chunk; p.kv_b = chunk;
     if (dtype == DT_F32) err = run_f32<EPI_STORE>(p, 0, 0, st);
-    else err = run_dma<128, 256, 2, 4, false, false, EPI_STORE, true>(p, st);
+    else err = run_dma<128, 256, 2, 4, 64, 2, false, false, EPI_STORE, true, G_ROUTER_DWG>(p, st);
   } else {
     GemmParams p1 = p;
     p1.batches = splits - 1; p1.kv_a = chunk; p1.kv_b = chunk;
     err = (splits > 1) ? ((dtype == DT_F32) ? run_f32<EPI_STORE>(p1, 0, 0, st)
-                                            : run_dma<128, 256, 2, 4, false, false, EPI_STORE, true>(p1, st))
+                                            : run_dma<128, 256, 2, 4, 64, 2, false, false, EPI_STORE, true, G_ROUTER_DWG>(p1, st))
                        : hipSuccess;
     if (err != hipSuccess) return err;
     GemmParams p2 = p;
@@ -678,7 +720,7 @@ hipError_t launch_router_dwg(int dtype, const void* dZ, const void* X, float* dW
     p2.C = part + (size_t)(splits - 1) * E * d;
     p2.batches = 1; p2.kv_a = last; p2.kv_b = last;
     err = (dtype == DT_F32) ? run_f32<EPI_STORE>(p2, 0, 0, st)
-                            : run_dma<128, 256, 2, 4, false, false, EPI_STORE, true>(p2, st);
+                            : run_dma<128, 256, 2, 4, 64, 2, false, false, EPI_STORE, true, G_ROUTER_DWG>(p2, st);
   }
   if (err != hipSuccess) return err;
   const long n = (long)E * d;

@@ -43,10 +43,10 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint4* __restrict__ X
 // ---------------------------------------------------------------- combine
 constexpr int CB_TOK = 16;   // tokens per workgroup (4 per wave)
 constexpr int CB_Q = 4;      // 8-element chunks per lane per column block
-constexpr int CB_MAXE = 256;
 
-// Builds, for one token, the ascending list of (expert, row, gate) it was
-// selected by; returns the list length.  list is wave-private LDS.
+// Builds, for one token, the ascending list of (expert, row) it was selected
+// by, with the gate values; returns the list length.  Lists are wave-private.
+template <int MAXE>
 __device__ __forceinline__ int token_expert_list(const int32_t* sslot, const float* sgate,
                                                  int t, int E, int K, int2* list, float* lgate) {
   const int lane = threadIdx.x & 63;
@@ -59,7 +59,7 @@ __device__ __forceinline__ int token_expert_list(const int32_t* sslot, const flo
     const int before = __popcll(m & ((1ull << lane) - 1ull));
     if (r >= 0) {
       list[n + before] = make_int2(j, r);
-      lgate[n + before] = sgate ? sgate[t * CB_MAXE + j] : 1.0f;
+      lgate[n + before] = sgate ? sgate[t * MAXE + j] : 1.0f;
     }
     n += __popcll(m);
   }
@@ -67,18 +67,19 @@ __device__ __forceinline__ int token_expert_list(const int32_t* sslot, const flo
   return n;
 }
 
-// Y[i] = (Xr[i] if Xr) + sum_j g_ij Src[j, slot_ij]; with S == nullptr the
-// gates are 1 (backward combine of dXe).
-template <typename T>
+// Y[i] = (Xr[i] if Xr) + sum_j g_ij Src[j, slot_ij] in ascending j; with
+// S == nullptr the gates are 1 (backward combine of dXe).  Two expert rows are
+// loaded per step so that each lane keeps 8 16-byte loads in flight.
+template <typename T, int MAXE>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
                                                       const float* __restrict__ S,
                                                       const int32_t* __restrict__ slotT,
                                                       const T* Xr, T* Y, int N, int E, int K,
                                                       int d) {
-  __shared__ int32_t sslot[CB_MAXE * CB_TOK];
-  __shared__ float sgate[CB_TOK * CB_MAXE];
-  __shared__ int2 slist[4][CB_MAXE];
-  __shared__ float sglist[4][CB_MAXE];
+  __shared__ int32_t sslot[MAXE * CB_TOK];
+  __shared__ float sgate[CB_TOK * MAXE];
+  __shared__ int2 slist[4][MAXE];
+  __shared__ float sglist[4][MAXE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i0 = blockIdx.x * CB_TOK;
   for (int c = tid; c < E * CB_TOK; c += 256) {
@@ -88,7 +89,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
   if (S) {
     for (int c = tid; c < CB_TOK * E; c += 256) {
       const int t = c / E, j = c % E;
-      sgate[t * CB_MAXE + j] = (i0 + t < N) ? S[(size_t)(i0 + t) * E + j] : 0.f;
+      sgate[t * MAXE + j] = (i0 + t < N) ? S[(size_t)(i0 + t) * E + j] : 0.f;
     }
   }
   __syncthreads();
@@ -96,8 +97,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
   for (int t = wave; t < CB_TOK; t += 4) {
     const int i = i0 + t;
     if (i >= N) break;
-    const int n = token_expert_list(sslot, S ? sgate : nullptr, t, E, K, slist[wave],
-                                      sglist[wave]);
+    const int n = token_expert_list<MAXE>(sslot, S ? sgate : nullptr, t, E, K, slist[wave],
+                                          sglist[wave]);
     for (int c0 = 0; c0 < nch; c0 += 64 * CB_Q) {
       float acc[CB_Q][8];
 #pragma unroll
@@ -110,20 +111,38 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
           for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
         }
       }
-      for (int p = 0; p < n; ++p) {
-        const int2 jr = slist[wave][p];
-        const float g = sglist[wave][p];
-        const T* src = Src + ((size_t)jr.x * K + jr.y) * d;
-        float v[CB_Q][8];
+      int p = 0;
+      for (; p + 2 <= n; p += 2) {
+        const int2 jr0 = slist[wave][p], jr1 = slist[wave][p + 1];
+        const float g0 = sglist[wave][p], g1 = sglist[wave][p + 1];
+        const T* src0 = Src + ((size_t)jr0.x * K + jr0.y) * d;
+        const T* src1 = Src + ((size_t)jr1.x * K + jr1.y) * d;
+        typename Elem<T>::Raw v0[CB_Q], v1[CB_Q];
 #pragma unroll
         for (int q = 0; q < CB_Q; ++q) {
           const int c = c0 + q * 64 + lane;
-          if (c < nch) Elem<T>::load8(src + c * 8, v[q]);
+          if (c < nch) {
+            v0[q] = Elem<T>::load_raw(src0 + c * 8);
+            v1[q] = Elem<T>::load_raw(src1 + c * 8);
+          }
         }
 #pragma unroll
         for (int q = 0; q < CB_Q; ++q) {
+          const int c = c0 + q * 64 + lane;
+          if (c < nch) {
+            Elem<T>::fma_raw(acc[q], g0, v0[q]);   // ascending expert order
+            Elem<T>::fma_raw(acc[q], g1, v1[q]);
+          }
+        }
+      }
+      if (p < n) {
+        const int2 jr = slist[wave][p];
+        const float g = sglist[wave][p];
+        const T* src = Src + ((size_t)jr.x * K + jr.y) * d;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[q][e] = fmaf(g, v[q][e], acc[q][e]);
+        for (int q = 0; q < CB_Q; ++q) {
+          const int c = c0 + q * 64 + lane;
+          if (c < nch) Elem<T>::fma_raw(acc[q], g, Elem<T>::load_raw(src + c * 8));
         }
       }
 #pragma unroll
@@ -134,6 +153,19 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
     }
     __builtin_amdgcn_wave_barrier();
   }
+}
+
+template <typename T>
+hipError_t run_combine(const T* Src, const float* S, const int32_t* slotT, const T* Xr, T* Y,
+                       int N, int E, int K, int d, hipStream_t st) {
+  const int grid = (N + CB_TOK - 1) / CB_TOK;
+  if (E <= 64)
+    combine_kernel<T, 64><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d);
+  else if (E <= 128)
+    combine_kernel<T, 128><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d);
+  else
+    combine_kernel<T, 256><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- backward gather
@@ -179,31 +211,57 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(const T* __restrict__ d
 // ---------------------------------------------------------------- router dZ
 // dZ[i, :] = S_i * (dS_i - <S_i, dS_i>) / tau with dS_ij = dSp[j, slot_ij] on
 // the selection and 0 elsewhere.  Writes fp32 dZ [N, E] and, if dZb is given,
-// a bf16 copy [N, EP] whose columns E..EP-1 are zero.
+// a bf16 copy [N, EP] whose columns E..EP-1 are zero.  A workgroup stages a
+// tile of `tok` (<= RZ_TOK) tokens through LDS so that every global access is
+// coalesced; the tile keeps the dynamic LDS under 64 KiB for any E <= 256.
+constexpr int RZ_TOK = 32;
+
 __global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict__ S,
                                                         const float* __restrict__ dSp,
                                                         const int32_t* __restrict__ slotT,
                                                         float* __restrict__ dZ,
                                                         bf16_t* __restrict__ dZb, int N, int E,
-                                                        int EP, int K, float inv_tau) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= N) return;
-  const float* s = S + (size_t)i * E;
-  float dot = 0.f;
-  for (int j = 0; j < E; ++j) {
-    const int r = slotT[(size_t)j * N + i];
-    const float ds = (r >= 0 && r < K) ? dSp[(size_t)j * K + r] : 0.f;
-    dot = fmaf(s[j], ds, dot);
+                                                        int EP, int K, float inv_tau, int tok) {
+  extern __shared__ float rz_lds[];
+  const int LD = E + 1;
+  float* sS = rz_lds;              // [tok][E+1]
+  float* sD = rz_lds + tok * LD;   // [tok][E+1]
+  __shared__ float sdot[RZ_TOK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i0 = blockIdx.x * tok;
+  const int nt = N - i0 < tok ? N - i0 : tok;
+  for (int c = tid; c < nt * E; c += 256) {            // S tile: contiguous rows
+    const int t = c / E, j = c % E;
+    sS[t * LD + j] = S[(size_t)i0 * E + c];
   }
-  for (int j = 0; j < EP; ++j) {
-    float z = 0.f;
-    if (j < E) {
-      const int r = slotT[(size_t)j * N + i];
-      const float ds = (r >= 0 && r < K) ? dSp[(size_t)j * K + r] : 0.f;
-      z = s[j] * (ds - dot) * inv_tau;
-      dZ[(size_t)i * E + j] = z;
+  for (int c = tid; c < E * tok; c += 256) {           // slot tile: tok tokens per expert
+    const int j = c / tok, t = c % tok;
+    float ds = 0.f;
+    if (t < nt) {
+      const int r = slotT[(size_t)j * N + i0 + t];
+      if (r >= 0 && r < K) ds = dSp[(size_t)j * K + r];
     }
-    if (dZb) dZb[(size_t)i * EP + j] = (bf16_t)f32_to_bf16(z);
+    sD[t * LD + j] = ds;
+  }
+  __syncthreads();
+  for (int t = wave; t < nt; t += 4) {                 // <S_t, dS_t>, one wave per token
+    float v = 0.f;
+    for (int j = lane; j < E; j += 64) v = fmaf(sS[t * LD + j], sD[t * LD + j], v);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    if (lane == 0) sdot[t] = v;
+  }
+  __syncthreads();
+  for (int c = tid; c < nt * E; c += 256) {
+    const int t = c / E, j = c % E;
+    dZ[(size_t)i0 * E + c] = sS[t * LD + j] * (sD[t * LD + j] - sdot[t]) * inv_tau;
+  }
+  if (dZb) {
+    for (int c = tid; c < nt * EP; c += 256) {
+      const int t = c / EP, j = c % EP;
+      const float z = (j < E) ? sS[t * LD + j] * (sD[t * LD + j] - sdot[t]) * inv_tau : 0.f;
+      dZb[(size_t)i0 * EP + c] = (bf16_t)f32_to_bf16(z);
+    }
   }
 }
 
@@ -229,27 +287,19 @@ hipError_t launch_gather(int dtype, const void* X, const int32_t* sel_token, voi
 hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_t* slotT, void* Y,
                           int N, int E, int K, int d, hipStream_t st) {
   if (N == 0) return hipSuccess;
-  const int grid = (N + CB_TOK - 1) / CB_TOK;
   if (dtype == DT_F32)
-    combine_kernel<float><<<grid, 256, 0, st>>>((const float*)O, S, slotT, nullptr, (float*)Y, N,
-                                                E, K, d);
-  else
-    combine_kernel<bf16_t><<<grid, 256, 0, st>>>((const bf16_t*)O, S, slotT, nullptr, (bf16_t*)Y,
-                                                 N, E, K, d);
-  return hipGetLastError();
+    return run_combine<float>((const float*)O, S, slotT, nullptr, (float*)Y, N, E, K, d, st);
+  return run_combine<bf16_t>((const bf16_t*)O, S, slotT, nullptr, (bf16_t*)Y, N, E, K, d, st);
 }
 
 hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, const void* Xr,
                               void* dX, int N, int E, int K, int d, hipStream_t st) {
   if (N == 0) return hipSuccess;
-  const int grid = (N + CB_TOK - 1) / CB_TOK;
   if (dtype == DT_F32)
-    combine_kernel<float><<<grid, 256, 0, st>>>((const float*)dXe, nullptr, slotT,
-                                                (const float*)Xr, (float*)dX, N, E, K, d);
-  else
-    combine_kernel<bf16_t><<<grid, 256, 0, st>>>((const bf16_t*)dXe, nullptr, slotT,
-                                                 (const bf16_t*)Xr, (bf16_t*)dX, N, E, K, d);
-  return hipGetLastError();
+    return run_combine<float>((const float*)dXe, nullptr, slotT, (const float*)Xr, (float*)dX, N,
+                              E, K, d, st);
+  return run_combine<bf16_t>((const bf16_t*)dXe, nullptr, slotT, (const bf16_t*)Xr, (bf16_t*)dX, N,
+                             E, K, d, st);
 }
 
 hipError_t launch_bwd_gather(int dtype, const void* dY, const void* O, const float* S,
@@ -271,7 +321,10 @@ hipError_t launch_router_dz(const float* S, const float* dSp, const int32_t* slo
                             bf16_t* dZb, int N, int E, int EP, int K, float inv_tau,
                             hipStream_t st) {
   if (N == 0) return hipSuccess;
-  router_dz_kernel<<<(N + 255) / 256, 256, 0, st>>>(S, dSp, slotT, dZ, dZb, N, E, EP, K, inv_tau);
+  const int tok = E > 128 ? RZ_TOK / 2 : RZ_TOK;
+  const size_t lds = (size_t)2 * tok * (E + 1) * sizeof(float);
+  router_dz_kernel<<<(N + tok - 1) / tok, 256, lds, st>>>(S, dSp, slotT, dZ, dZb, N, E, EP, K,
+                                                           inv_tau, tok);
   return hipGetLastError();
 }
 
