@@ -10,6 +10,7 @@ from __future__ import annotations
 
 import argparse
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -65,6 +66,34 @@ def build(debug: bool = False, verbose: bool = False, jobs: int = 8) -> str:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, OUT)
     return OUT
+
+
+_RES_KEYS = {"VGPRs": "vgpr", "AGPRs": "agpr", "ScratchSize [bytes/lane]": "scratch",
+             "Occupancy [waves/SIMD]": "occupancy", "LDS Size [bytes/block]": "lds"}
+
+
+def resource_usage(src: str) -> dict:
+    """Per-kernel register, scratch and LDS use of one source, as the compiler
+    reports it for gfx950 (device-only compile to a temporary object)."""
+    import tempfile
+    with tempfile.TemporaryDirectory() as td:
+        cmd = [hipcc(), *flags(False), "--cuda-device-only", "-x", "hip", "-c",
+               os.path.join(CSRC, src), "-o", os.path.join(td, "res.o"),
+               "-Rpass-analysis=kernel-resource-usage"]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
+    out, cur = {}, None
+    for ln in r.stderr.splitlines():
+        m = re.search(r"remark: (?:\s*)(.+?): (\S+) \[-Rpass-analysis", ln)
+        if not m:
+            continue
+        key, val = m.group(1).strip(), m.group(2)
+        if key == "Function Name":
+            cur = out.setdefault(val, {})
+        elif cur is not None and key in _RES_KEYS:
+            cur[_RES_KEYS[key]] = int(val)
+    return out
 
 
 def main():
