@@ -5,7 +5,8 @@
 //
 // bf16: one pipelined kernel (gemm_dma_kernel) for every product of the
 // forward and backward.  v_mfma_f32_32x32x16_bf16 with fp32 accumulation; a
-// 256 x 256 output tile per workgroup of 8 waves (2 per SIMD, 64 x 128 each);
+// 256 x 256 output tile per workgroup of 8 waves (2 per SIMD, 64 x 128 or
+// 128 x 64 each);
 // K advances 64 at a time through a 2-stage LDS ring filled straight from
 // global memory by global_load_lds_dwordx4 (no VGPR staging).  K-contiguous
 // operands sit in LDS as 128-byte rows with XOR-swizzled 16-byte chunks
@@ -132,7 +133,13 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
   const int per_b = p.MT * p.NT;
   const int e = t / per_b;
   const int rem = t - e * per_b;
-  const int mt = rem % p.MT, nt = rem / p.MT;
+  // Tiles go in groups of GROUP_M row blocks, row block fastest inside a
+  // group: the workgroups resident on one XCD then share few A row blocks and
+  // B column blocks at a time (fewer L2 misses than a full column of row blocks).
+  constexpr int GROUP_M = 3;
+  const int grp = rem / (GROUP_M * p.NT), in_grp = rem - grp * GROUP_M * p.NT;
+  const int gm = (p.MT - grp * GROUP_M) < GROUP_M ? (p.MT - grp * GROUP_M) : GROUP_M;
+  const int mt = grp * GROUP_M + in_grp % gm, nt = in_grp / gm;
   const int m0 = mt * BM;
   const int n0 = (EPI == EPI_SWIGLU) ? nt * (BN / 2) : nt * BN;
 
@@ -348,8 +355,24 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
 
   // ---- epilogue: stage 32-row slices of the wave tile through LDS ----
   float* stage_f = reinterpret_cast<float*>(smem) + wave * 32 * SLD;
+  // SwiGLU backward: this slice's H1/H3 chunks are loaded before the slice is
+  // staged, so their latency overlaps the staging (rows or columns past the
+  // matrix read element 0 and are not stored).
+  constexpr int BWD_CPR = WN / 8, BWD_Q = (EPI == EPI_SWIGLU_BWD) ? (32 * BWD_CPR) / 64 : 1;
+  u32x4 h1raw[BWD_Q], h3raw[BWD_Q];
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
+    if constexpr (EPI == EPI_SWIGLU_BWD) {
+      const int mb = m0 + wm * WM + mi * 32;
+#pragma unroll
+      for (int q = 0; q < BWD_Q; ++q) {
+        const int c = lane + q * 64;
+        const int m = mb + c / BWD_CPR, n = n0 + wn * WN + (c % BWD_CPR) * 8;
+        const size_t ho = (m < p.M && n < p.N) ? (size_t)e * p.h_bs + (size_t)m * p.ldh + n : 0;
+        h1raw[q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H1 + ho);
+        h3raw[q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H3 + ho);
+      }
+    }
 #pragma unroll
     for (int ni = 0; ni < NB; ++ni)
 #pragma unroll
@@ -408,25 +431,24 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
         }
       }
     } else {  // EPI_SWIGLU_BWD
-      constexpr int CPR = WN / 8;
 #pragma unroll
-      for (int q = 0; q < (32 * CPR) / 64; ++q) {
+      for (int q = 0; q < BWD_Q; ++q) {
         const int c = lane + q * 64;
-        const int row = c / CPR, cc = c % CPR;
+        const int row = c / BWD_CPR, cc = c % BWD_CPR;
         const int m = mbase + row;
         const int n = n0 + wn * WN + cc * 8;
         if (m < p.M && n < p.N) {
           const float* v = stage_f + row * SLD + cc * 8;
-          const size_t ho = (size_t)e * p.h_bs + (size_t)m * p.ldh + n;
-          float h1[8], h3[8], d1[8], d3[8];
-          Elem<bf16_t>::load8((const bf16_t*)p.H1 + ho, h1);
-          Elem<bf16_t>::load8((const bf16_t*)p.H3 + ho, h3);
+          float d1[8], d3[8];
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
+            const uint32_t w1 = h1raw[q][u >> 1], w3 = h3raw[q][u >> 1];
+            const float h1 = bf16_to_f32((u & 1) ? (w1 >> 16) : (w1 & 0xffffu));
+            const float h3 = bf16_to_f32((u & 1) ? (w3 >> 16) : (w3 & 0xffffu));
             const float da = v[u];
-            const float sg = sigmoid_f(h1[u]);
-            d3[u] = da * h1[u] * sg;
-            d1[u] = da * h3[u] * sg * (1.0f + h1[u] * (1.0f - sg));
+            const float sg = sigmoid_f(h1);
+            d3[u] = da * h1 * sg;
+            d1[u] = da * h3 * sg * (1.0f + h1 * (1.0f - sg));
           }
           const size_t off = (size_t)e * p.c_bs + (size_t)m * p.ldc + n;
           Elem<bf16_t>::store8((bf16_t*)p.C + off, d1);
@@ -598,7 +620,7 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
   p.H1 = H1; p.H3 = H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU>(p, 1, 1, st);
-  return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
+  return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
 }
 
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
