@@ -20,8 +20,9 @@ its Section 2.2 and its Section 4):
 Pins (tests/test_oracle.py): brute-force selection on tiny inputs, exactly k_g
 tokens per (group, expert), softmax closed forms, the dense soft mixture when
 every token is selected, the textbook SwiGLU FFN when E = 1, central finite
-differences of the backward, and Table 5 of the paper for the capacity
-schedulers.
+differences of the backward, Table 5 of the paper for the capacity
+schedulers, and the drop statistic's closed cases (every token kept when
+k_g = L_g, every token dropped when k_g = 0, L_g - k_g dropped when E = 1).
 """
 from __future__ import annotations
 
@@ -157,6 +158,21 @@ def slot_ref(sel_token, n_tokens: int) -> np.ndarray:
     for j in range(E):
         slot[sel_token[j], j] = np.arange(K)
     return slot
+
+
+def coverage_ref(sel_token, group_offsets):
+    """Token drop statistic (Appendix D): experts_per_token[i] = number of experts
+    whose chosen set contains token i; dropped[g] = tokens of group g that no
+    expert chose (their layer output is zero)."""
+    off = np.asarray(group_offsets, dtype=np.int64)
+    N = int(off[-1])
+    counts = np.zeros(N, dtype=np.int64)
+    for row in np.asarray(sel_token):
+        for i in row:
+            counts[int(i)] += 1
+    dropped = np.array([int(np.sum(counts[off[g]:off[g + 1]] == 0)) for g in range(len(off) - 1)],
+                       dtype=np.int64)
+    return counts, dropped
 
 
 def bruteforce_select(col, k: int) -> tuple:

@@ -257,6 +257,39 @@ def test_unselected_tokens_get_zero():
     assert np.array_equal(out["gate"], np.take_along_axis(out["S"].T, out["sel_token"], 1))
 
 
+# --------------------------------------------------------------------- drop statistic
+
+def test_coverage_closed_cases():
+    rng = np.random.default_rng(8)
+    lens = [7, 1, 12, 4]
+    off = np.concatenate([[0], np.cumsum(lens)])
+    S = ref.softmax_ref(rng.standard_normal((sum(lens), 5)))
+    cnt, drop = ref.coverage_ref(ref.select_ref(S, off, lens), off)       # k = L: all kept by all
+    assert np.all(cnt == 5) and np.all(drop == 0)
+    cnt, drop = ref.coverage_ref(ref.select_ref(S, off, [0] * 4), off)    # k = 0: all dropped
+    assert np.all(cnt == 0) and list(drop) == lens
+    k = [3, 0, 5, 4]
+    cnt, drop = ref.coverage_ref(ref.select_ref(S[:, :1], off, k), off)  # one expert: L - k dropped
+    assert list(drop) == [L - kk for L, kk in zip(lens, k)]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_coverage_equals_bruteforce_membership(seed):
+    rng = np.random.default_rng(300 + seed)
+    lens = list(rng.integers(1, 8, size=rng.integers(1, 4)))
+    E = int(rng.integers(1, 5))
+    off = np.concatenate([[0], np.cumsum(lens)])
+    S = rng.integers(0, 3, size=(int(off[-1]), E)).astype(np.float64) / 3   # many ties
+    k = np.array([rng.integers(0, L + 1) for L in lens])
+    sets = [set(int(off[g]) + v for v in ref.bruteforce_select(S[off[g]:off[g + 1], j], int(k[g])))
+            for j in range(E) for g in range(len(lens))]
+    want = [sum(i in s for s in sets) for i in range(int(off[-1]))]
+    cnt, drop = ref.coverage_ref(ref.select_ref(S, off, k), off)
+    assert list(cnt) == want
+    assert list(drop) == [sum(want[i] == 0 for i in range(off[g], off[g + 1])) for g in range(len(lens))]
+    assert cnt.sum() == E * k.sum()
+
+
 # --------------------------------------------------------------------- backward
 
 def test_backward_matches_finite_differences():
