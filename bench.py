@@ -298,6 +298,16 @@ def main():
            "grouped_gemm": {"tflops": round(gemm_fl / (gemm_ms * 1e-3) / 1e12, 1),
                             "mfma_frac": round(gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
 
+    # token drop statistic (Appendix D) of this batch, from the routing the step made
+    if backward:
+        slot = binding.saved_views(layer.saved, layer.P)["slot"]
+    else:
+        slot = ec.route(X, Wg, wl.group_offsets, caps, inv_tau, d_ff=h)[3]
+    _, dropped = ec.token_coverage(slot, wl.group_offsets, caps, d_model=d, d_ff=h)
+    n_drop = int(dropped.sum().item())
+    out["token_drop"] = {"dropped_tokens": n_drop, "fraction": round(n_drop / N, 5),
+                         "per_group": [int(v) for v in dropped.cpu().tolist()]}
+
     if backward and not a.no_forward_only:
         # forward alone, inference mode (no saved activations), same inputs
         inf = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, training=False)

@@ -140,6 +140,18 @@ int ec_route(const ec_problem *p, const void *X, const void *Wg, float *S,
              int32_t *sel_token, float *sel_gate, int32_t *slot,
              void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Token drop statistic (Appendix D: the fraction of tokens that no routed
+ * expert chose, whose layer output is therefore zero).  Reads a slot map as
+ * written by ec_route or kept in the saved buffer:
+ *   slot [E, N] int32 ([j, i] = row of token i in expert j's buffer or -1);
+ *   experts_per_token [N] int32 out: number of experts that chose token i;
+ *   dropped [G] int32 out: number of tokens of group g that no expert chose.
+ * Exact integer counts; no workspace.  slot and experts_per_token may be NULL
+ * only when N = 0.                                                            */
+int ec_token_coverage(const ec_problem *p, const int32_t *slot,
+                      int32_t *experts_per_token, int32_t *dropped,
+                      hipStream_t stream);
+
 /* Layer forward: routing, gather, SwiGLU experts as a grouped GEMM, and the
  * gate-weighted combine (Section 2.2, Appendix E).
  *   W1, W3 [E, h, d] dtype;  W2 [E, d, h] dtype;  Y [N, d] dtype out.

@@ -14,8 +14,9 @@ from .binding import (  # noqa: F401
     lib,
     route,
     saved_views,
+    token_coverage,
     Layer,
 )
 
 __all__ = ["ECError", "Problem", "Layer", "route", "forward", "backward", "capacity",
-           "saved_views", "lib"]
+           "saved_views", "token_coverage", "lib"]

@@ -21,8 +21,8 @@ EC_F32, EC_BF16 = 0, 1
 SCHEDULERS = {"linear": 0, "linear_rev": 1, "cosine": 2, "cosine_rev": 3, "gaussian": 4,
               "gaussian_rev": 5}
 EXPORTS = ("ec_status_string", "ec_last_error", "ec_total_capacity", "ec_workspace_size",
-           "ec_saved_layout_of", "ec_capacity", "ec_route", "ec_moe_forward", "ec_moe_backward",
-           "ec_set_stage_events")
+           "ec_saved_layout_of", "ec_capacity", "ec_route", "ec_token_coverage", "ec_moe_forward",
+           "ec_moe_backward", "ec_set_stage_events")
 
 
 class ECError(RuntimeError):
@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
                                   ctypes.c_double, ctypes.c_int, i32p]
         L.ec_route.restype = ctypes.c_int
         L.ec_route.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.ec_token_coverage.restype = ctypes.c_int
+        L.ec_token_coverage.argtypes = [pp, vp, vp, vp, vp]
         L.ec_moe_forward.restype = ctypes.c_int
         L.ec_moe_forward.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, sz, vp, sz, vp]
         L.ec_moe_backward.restype = ctypes.c_int
@@ -190,6 +192,20 @@ def route(X: torch.Tensor, Wg: torch.Tensor, group_offsets, capacity, inv_temper
                           _ptr(gate) if K else None, _ptr(slot), _ptr(ws), ws.numel(),
                           _stream()))
     return S, sel, gate, slot
+
+
+def token_coverage(slot: torch.Tensor, group_offsets, capacity, d_model: int = 64,
+                   d_ff: int = 64):
+    """Token drop statistic from a slot map [E,N] int32.  Returns experts_per_token [N]
+    int32 and dropped [G] int32 (tokens of each group that no expert chose)."""
+    E, N = slot.shape
+    off = np.asarray(group_offsets, dtype=np.int64)
+    P = Problem(N, d_model, E, d_ff, off, capacity, 1.0, torch.bfloat16)
+    cnt = torch.empty((N,), dtype=torch.int32, device=slot.device)
+    dropped = torch.empty((len(off) - 1,), dtype=torch.int32, device=slot.device)
+    _check(lib().ec_token_coverage(P.ref, _ptr(slot) if N else None, _ptr(cnt) if N else None,
+                                   _ptr(dropped), _stream()))
+    return cnt, dropped
 
 
 def forward(X, Wg, W1, W3, W2, group_offsets, capacity, inv_temperature=1.0, save=False):

@@ -361,6 +361,29 @@ int ec_route(const ec_problem* p, const void* X, const void* Wg, float* S, int32
   return enqueue_route(p, P, X, Wg, S, ST, sel_token, sel_gate, sl, stream);
 }
 
+int ec_token_coverage(const ec_problem* p, const int32_t* slot, int32_t* experts_per_token,
+                      int32_t* dropped, hipStream_t stream) {
+  Plan P;
+  EC_TRY(validate(p, &P));
+  EC_TRY(check_ptr(slot, "slot", P.N == 0));
+  EC_TRY(check_ptr(experts_per_token, "experts_per_token", P.N == 0));
+  EC_TRY(check_ptr(dropped, "dropped"));
+  EC_HIP(ec::launch_coverage_count(slot, (int)P.N, P.E, experts_per_token, stream));
+  ec::GroupTable tab;
+  for (int g0 = 0; g0 < P.G; g0 += ec::TOPK_MAX_GROUPS) {
+    tab.n = 0;
+    for (int g = g0; g < P.G && g < g0 + ec::TOPK_MAX_GROUPS; ++g) {
+      tab.off[tab.n] = p->group_offsets[g];
+      tab.len[tab.n] = p->group_offsets[g + 1] - p->group_offsets[g];
+      tab.k[tab.n] = p->capacity[g];
+      tab.seg[tab.n] = 0;
+      ++tab.n;
+    }
+    EC_HIP(ec::launch_coverage_drop(experts_per_token, tab, dropped + g0, stream));
+  }
+  return EC_OK;
+}
+
 int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const void* W1,
                    const void* W3, const void* W2, void* Y, void* saved, size_t saved_bytes_in,
                    void* ws, size_t ws_bytes, hipStream_t stream) {

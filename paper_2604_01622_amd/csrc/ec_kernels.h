@@ -84,6 +84,13 @@ hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, 
 hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1, void* dW3,
                             int E, int M, int d, int h, hipStream_t st);
 
+// Token drop statistic: cnt[i] = #{j : slotT[j, i] >= 0} for i < N, then
+// dropped[g] = #{i in group g : cnt[i] == 0} for the tab.n groups of the table.
+hipError_t launch_coverage_count(const int32_t* slotT, int N, int E, int32_t* cnt,
+                                 hipStream_t st);
+hipError_t launch_coverage_drop(const int32_t* cnt, const GroupTable& tab, int32_t* dropped,
+                                hipStream_t st);
+
 // Fill n int32/fp32/bytes with zero (a kernel, not a memset node).
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);
 

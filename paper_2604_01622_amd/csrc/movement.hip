@@ -265,6 +265,35 @@ __global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict_
   }
 }
 
+// Token drop statistic (Appendix D: tokens that no routed expert chose).
+// cnt[i] = number of experts j with slotT[j, i] >= 0; one thread per token,
+// coalesced over i for every expert row of the slot map.
+__global__ __launch_bounds__(256) void coverage_count_kernel(const int32_t* __restrict__ slotT,
+                                                              int N, int E,
+                                                              int32_t* __restrict__ cnt) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= N) return;
+  int c = 0;
+  for (int j = 0; j < E; ++j) c += slotT[(size_t)j * N + i] >= 0;
+  cnt[i] = c;
+}
+
+// dropped[g] = tokens of group g with cnt == 0; one workgroup per group of the table.
+__global__ __launch_bounds__(256) void coverage_drop_kernel(const int32_t* __restrict__ cnt,
+                                                             GroupTable tab,
+                                                             int32_t* __restrict__ dropped) {
+  __shared__ int part[4];
+  const int g = blockIdx.x;
+  const int off = tab.off[g], len = tab.len[g];
+  int z = 0;
+  for (int i = threadIdx.x; i < len; i += 256) z += cnt[off + i] == 0;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) z += __shfl_xor(z, m);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = z;
+  __syncthreads();
+  if (threadIdx.x == 0) dropped[g] = part[0] + part[1] + part[2] + part[3];
+}
+
 __global__ void zero_kernel(uint4* p, size_t n16, unsigned char* tail, size_t ntail) {
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
@@ -325,6 +354,20 @@ hipError_t launch_router_dz(const float* S, const float* dSp, const int32_t* slo
   const size_t lds = (size_t)2 * tok * (E + 1) * sizeof(float);
   router_dz_kernel<<<(N + tok - 1) / tok, 256, lds, st>>>(S, dSp, slotT, dZ, dZb, N, E, EP, K,
                                                            inv_tau, tok);
+  return hipGetLastError();
+}
+
+hipError_t launch_coverage_count(const int32_t* slotT, int N, int E, int32_t* cnt,
+                                 hipStream_t st) {
+  if (N == 0) return hipSuccess;
+  coverage_count_kernel<<<(N + 255) / 256, 256, 0, st>>>(slotT, N, E, cnt);
+  return hipGetLastError();
+}
+
+hipError_t launch_coverage_drop(const int32_t* cnt, const GroupTable& tab, int32_t* dropped,
+                                hipStream_t st) {
+  if (tab.n == 0) return hipSuccess;
+  coverage_drop_kernel<<<tab.n, 256, 0, st>>>(cnt, tab, dropped);
   return hipGetLastError();
 }
 

@@ -93,6 +93,16 @@ def test_bad_dtype_and_pointers():
     assert L.ec_workspace_size(P.ref, 9) == 0
 
 
+def test_token_coverage_validation():
+    L = ec.lib()
+    P = _problem()
+    assert L.ec_token_coverage(P.ref, FAKE, FAKE, None, None) == EC_ERR_ARG        # dropped
+    assert L.ec_token_coverage(P.ref, None, FAKE, FAKE, None) == EC_ERR_ARG        # slot, N > 0
+    assert L.ec_token_coverage(P.ref, FAKE, MISALIGNED, FAKE, None) == EC_ERR_ALIGN
+    assert L.ec_token_coverage(_problem(capacity=[101, 20]).ref, FAKE, FAKE, FAKE,
+                               None) == EC_ERR_CAPACITY
+
+
 def test_workspace_and_saved_layout():
     P = _problem()
     assert P.K == 30

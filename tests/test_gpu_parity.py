@@ -75,6 +75,11 @@ def check_route(inp, caps, inv_tau, S_rows=None):
     assert np.array_equal(slot_h, slot_exp)
     if sel_h.size:
         assert np.array_equal(gate_h, np.take_along_axis(S_h.T, sel_h.astype(np.int64), 1))
+    # token drop statistic from the slot map: exact counts
+    cnt, dropped = ec.token_coverage(slot, off, caps)
+    cnt_ref, dropped_ref = ref.coverage_ref(sel_ref, off)
+    assert np.array_equal(cnt.cpu().numpy(), cnt_ref)
+    assert np.array_equal(dropped.cpu().numpy(), dropped_ref)
     return S_h, sel_h
 
 
