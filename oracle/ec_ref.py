@@ -217,9 +217,10 @@ def swiglu_ffn_ref(x, W1j, W3j, W2j):
 
 
 def forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 1.0,
-                sel_token=None) -> dict:
+                sel_token=None, shared=None) -> dict:
     """Layer output y_i = sum over experts j that selected i of g_ij FFN_j(x_i),
-    with g_ij = S_ij; y_i = 0 when no expert selected token i.
+    with g_ij = S_ij; y_i = 0 when no expert selected token i.  With shared
+    experts (Ws1, Ws3, Ws2), their FFN of x_i is added to every y_i.
 
     If sel_token is given it replaces the selection (used to evaluate the layer on
     the selection another implementation made from its own score matrix)."""
@@ -234,12 +235,16 @@ def forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 1.0
         gate[j] = S[rows, j]
         o = swiglu_ffn_ref(Xf[rows], W1f[j], W3f[j], W2f[j])
         Y[rows] += gate[j][:, None] * o            # rows are distinct within one expert
+    if shared is not None:
+        Y += shared_ffn_ref(Xf, shared)
     return {"S": S, "sel_token": sel, "gate": gate, "Y": Y}
 
 
-def dense_loop_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 1.0):
+def dense_loop_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 1.0,
+                   shared_experts=()):
     """The combine as an explicit loop over (expert, selected token), one vector at a
-    time.  Small inputs only."""
+    time, plus every shared expert (a list of (W1s, W3s, W2s), one per shared
+    expert) on every token.  Small inputs only."""
     Xf, W1f, W3f, W2f = widen(X), widen(W1), widen(W3), widen(W2)
     S = router_ref(X, Wg, inv_tau)
     sel = select_ref(S, group_offsets, capacity)
@@ -249,7 +254,54 @@ def dense_loop_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 
             x = Xf[i]
             a = silu(W1f[j] @ x) * (W3f[j] @ x)
             Y[i] = Y[i] + S[i, j] * (W2f[j] @ a)
+    for (w1, w3, w2) in shared_experts:
+        w1, w3, w2 = widen(w1), widen(w3), widen(w2)
+        for i in range(Xf.shape[0]):
+            x = Xf[i]
+            Y[i] = Y[i] + w2 @ (silu(w1 @ x) * (w3 @ x))
     return Y
+
+
+# ---------------------------------------------------------------------------
+# Shared experts (Appendix D: they process every token whatever the routing;
+# Appendix E: 2 per MoE layer).  n_s shared SwiGLU experts of width h_s are one
+# SwiGLU of width n_s h_s whose hidden units are theirs side by side
+# (Ws1, Ws3 [n_s h_s, d], Ws2 [d, n_s h_s]); the output is added to the routed
+# sum without a gate.
+# ---------------------------------------------------------------------------
+
+def shared_ffn_ref(X, shared):
+    """FFN_shared(x) for every row x of X."""
+    Ws1, Ws3, Ws2 = shared
+    return swiglu_ffn_ref(X, Ws1, Ws3, Ws2)
+
+
+def shared_backward_ref(X, shared, dY):
+    """(dX, dWs1, dWs3, dWs2) of sum(FFN_shared(X) * dY)."""
+    Ws1, Ws3, Ws2 = (widen(w) for w in shared)
+    x, dy = widen(X), widen(dY)
+    h1, h3 = x @ Ws1.T, x @ Ws3.T
+    sg = 1.0 / (1.0 + np.exp(-h1))
+    a = h1 * sg * h3
+    da = dy @ Ws2
+    dh3 = da * (h1 * sg)
+    dh1 = da * h3 * (sg * (1.0 + h1 * (1.0 - sg)))
+    return dh1 @ Ws1 + dh3 @ Ws3, dh1.T @ x, dh3.T @ x, dy.T @ a
+
+
+def shared_grads_units_ref(X, shared, dY, units):
+    """Rows `units` of dWs1 and dWs3 and columns `units` of dWs2 (hidden units of
+    the shared FFN), each needing only its own unit over all tokens."""
+    Ws1, Ws3, Ws2 = shared
+    u = np.asarray(units, dtype=np.int64)
+    x, dy = widen(X), widen(dY)
+    h1, h3 = x @ widen(np.asarray(Ws1)[u]).T, x @ widen(np.asarray(Ws3)[u]).T
+    sg = 1.0 / (1.0 + np.exp(-h1))
+    a = h1 * sg * h3
+    da = dy @ widen(np.asarray(Ws2)[:, u])
+    dh3 = da * (h1 * sg)
+    dh1 = da * h3 * (sg * (1.0 + h1 * (1.0 - sg)))
+    return dh1.T @ x, dh3.T @ x, dy.T @ a
 
 
 # ---------------------------------------------------------------------------
@@ -257,8 +309,9 @@ def dense_loop_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 
 # ---------------------------------------------------------------------------
 
 def backward_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau: float = 1.0,
-                 sel_token=None) -> dict:
-    """Gradients of sum(Y * dY) w.r.t. X, Wg, W1, W3, W2.
+                 sel_token=None, shared=None) -> dict:
+    """Gradients of sum(Y * dY) w.r.t. X, Wg, W1, W3, W2 (and the shared experts'
+    Ws1, Ws3, Ws2 when given: their FFN adds its own dX term).
 
     Chain, per selected pair (i, j) with x = x_i:
       O = W2_j A, A = SiLU(H1) * H3, H1 = W1_j x, H3 = W3_j x, y_i += S_ij O
@@ -301,13 +354,18 @@ def backward_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau: float 
     dZ = S * (dS - np.sum(S * dS, axis=1, keepdims=True)) * float(inv_tau)
     dWg = dZ.T @ Xf
     dX += dZ @ Wgf
-    return {"dX": dX, "dWg": dWg, "dW1": dW1, "dW3": dW3, "dW2": dW2, "dS": dS,
-            "S": S, "sel_token": sel}
+    out = {"dX": dX, "dWg": dWg, "dW1": dW1, "dW3": dW3, "dW2": dW2, "dS": dS,
+           "S": S, "sel_token": sel}
+    if shared is not None:
+        dXs, out["dWs1"], out["dWs3"], out["dWs2"] = shared_backward_ref(Xf, shared, dYf)
+        out["dX"] = dX + dXs
+    return out
 
 
-def loss_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau, sel_token) -> float:
+def loss_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau, sel_token,
+             shared=None) -> float:
     """sum(Y * dY) with a fixed selection: the scalar whose gradient backward_ref returns."""
-    Y = forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau, sel_token)["Y"]
+    Y = forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau, sel_token, shared)["Y"]
     return float(np.sum(Y * widen(dY)))
 
 
@@ -317,7 +375,8 @@ def loss_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau, sel_token)
 # checked against forward_ref / backward_ref on small inputs.
 # ---------------------------------------------------------------------------
 
-def forward_rows_ref(X, Wg, W1, W3, W2, sel_token, rows, inv_tau: float = 1.0) -> np.ndarray:
+def forward_rows_ref(X, Wg, W1, W3, W2, sel_token, rows, inv_tau: float = 1.0,
+                     shared=None) -> np.ndarray:
     """y_i for the listed tokens only, with the selection given."""
     rows = np.asarray(rows, dtype=np.int64)
     slot = slot_ref(np.asarray(sel_token), np.asarray(X).shape[0])[rows]
@@ -328,6 +387,8 @@ def forward_rows_ref(X, Wg, W1, W3, W2, sel_token, rows, inv_tau: float = 1.0) -
         q = np.nonzero(slot[:, j] >= 0)[0]          # listed tokens that expert j selected
         if len(q):
             Y[q] += S[q, j][:, None] * swiglu_ffn_ref(Xr[q], W1[j], W3[j], W2[j])
+    if shared is not None:
+        Y += shared_ffn_ref(Xr, shared)
     return Y
 
 
@@ -340,8 +401,10 @@ def _pair_terms(x, W1j, W3j, W2j):
     return h1, h3, sg, a, a @ widen(W2j).T
 
 
-def backward_rows_ref(X, Wg, W1, W3, W2, dY, sel_token, rows, inv_tau: float = 1.0) -> np.ndarray:
-    """dX_i for the listed tokens only (expert and router terms), selection given."""
+def backward_rows_ref(X, Wg, W1, W3, W2, dY, sel_token, rows, inv_tau: float = 1.0,
+                      shared=None) -> np.ndarray:
+    """dX_i for the listed tokens only (expert, router and shared-expert terms),
+    selection given."""
     rows = np.asarray(rows, dtype=np.int64)
     slot = slot_ref(np.asarray(sel_token), np.asarray(X).shape[0])[rows]
     Xr, dYr, Wgf = widen(np.asarray(X)[rows]), widen(np.asarray(dY)[rows]), widen(Wg)
@@ -359,6 +422,8 @@ def backward_rows_ref(X, Wg, W1, W3, W2, dY, sel_token, rows, inv_tau: float = 1
         dh1 = da * h3 * (sg * (1.0 + h1 * (1.0 - sg)))
         dX[q] += dh1 @ widen(W1[j]) + dh3 @ widen(W3[j])
     dZ = S * (dS - np.sum(S * dS, axis=1, keepdims=True)) * float(inv_tau)
+    if shared is not None:
+        dX += shared_backward_ref(Xr, shared, dYr)[0]
     return dX + dZ @ Wgf
 
 

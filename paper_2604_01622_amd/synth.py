@@ -80,6 +80,7 @@ class Workload:
     inv_temperatures: tuple = (1.0,)
     backward: bool = False
     dy_seed: Optional[int] = None
+    d_shared: int = 0             # hidden width of the shared experts side by side (0: none)
 
     @property
     def n_tokens(self) -> int:
@@ -109,6 +110,7 @@ class Inputs:
     W2: np.ndarray
     t: Optional[np.ndarray]       # float64 [G] mask ratios, or None
     dY: Optional[np.ndarray] = None
+    shared: Optional[tuple] = None   # (Ws1 [hs,d], Ws3 [hs,d], Ws2 [d,hs]) or None
 
 
 def draw(wl: Workload, with_dy: Optional[bool] = None, threads: int = 8) -> Inputs:
@@ -131,7 +133,13 @@ def draw(wl: Workload, with_dy: Optional[bool] = None, threads: int = 8) -> Inpu
     if with_dy if with_dy is not None else wl.backward:
         seed = wl.dy_seed if wl.dy_seed is not None else wl.seed + 1000
         dY = conv(_normal(np.random.SeedSequence(seed).spawn(1)[0], (N, d), 1.0, threads))
-    return Inputs(wl, X, Wg, W1, W3, W2, t, dY)
+    shared = None
+    if wl.d_shared:
+        hs = wl.d_shared
+        sk = np.random.SeedSequence([wl.seed, 2]).spawn(3)   # apart from the draws above
+        shared = tuple(conv(_normal(k, shp, wl.w_std, threads))
+                       for k, shp in zip(sk, ((hs, d), (hs, d), (d, hs))))
+    return Inputs(wl, X, Wg, W1, W3, W2, t, dY, shared)
 
 
 # The five workloads.  Sizes follow the paper's 8B-A1B block (Appendix E) and the
@@ -147,14 +155,20 @@ FINE_BF16 = Workload("fine_bf16_4x4096_d2048_E128_h768_c8", (4096,) * 4, 2048, 1
 TRAIN_BF16 = dataclasses.replace(TIMESTEP_BF16, name="train_bf16_8x2048_d2048_E64_h1024_c12-8t",
                                  backward=True, dy_seed=4)
 
-WORKLOADS = {w.name: w for w in (TINY_F32, STATIC_BF16, TIMESTEP_BF16, FINE_BF16, TRAIN_BF16)}
+# the training workload with the 8B-A1B block's 2 shared experts (each of the
+# routed experts' width) added to every token
+TRAIN_SHARED_BF16 = dataclasses.replace(
+    TRAIN_BF16, name="train_shared_bf16_8x2048_d2048_E64_h1024_s2x1024_c12-8t", d_shared=2048)
+
+WORKLOADS = {w.name: w for w in (TINY_F32, STATIC_BF16, TIMESTEP_BF16, FINE_BF16, TRAIN_BF16,
+                                 TRAIN_SHARED_BF16)}
 
 
 def small(name: str, group_lengths: Sequence[int], d: int, E: int, h: int, dtype: str = "bf16",
           seed: int = 7, capacity_factor: Optional[float] = None, c_min=None, c_max=None,
-          inv_temperature: float = 1.0, backward: bool = False) -> Workload:
+          inv_temperature: float = 1.0, backward: bool = False, d_shared: int = 0) -> Workload:
     """A reduced workload for parity tests (any shapes; weights std 1/sqrt(d))."""
     return Workload(name, tuple(int(x) for x in group_lengths), d, E, h, dtype, seed,
                     x_std=1.0, w_std=float(1.0 / np.sqrt(d)), capacity_factor=capacity_factor,
                     c_min=c_min, c_max=c_max, inv_temperatures=(inv_temperature,),
-                    backward=backward, dy_seed=seed + 100)
+                    backward=backward, dy_seed=seed + 100, d_shared=d_shared)

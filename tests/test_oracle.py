@@ -343,6 +343,103 @@ def _torch_swiglu_t(x, W1, W3, W2):
     return (torch.nn.functional.silu(x @ W1.T) * (x @ W3.T)) @ W2.T
 
 
+# --------------------------------------------------------------------- shared experts
+
+def _two_shared(d, hs, seed):
+    """Two shared experts drawn separately, and their side-by-side form."""
+    rng = np.random.default_rng(seed)
+    e = [tuple(rng.standard_normal(shp) / np.sqrt(shp[1]) for shp in ((hs, d), (hs, d), (d, hs)))
+         for _ in range(2)]
+    cat = (np.vstack([e[0][0], e[1][0]]), np.vstack([e[0][1], e[1][1]]),
+           np.hstack([e[0][2], e[1][2]]))
+    return e, cat
+
+
+def test_shared_only_is_sum_of_textbook_swiglus():
+    inp = _tiny_inputs([9, 14], 16, 4, 8, seed=30)
+    experts, cat = _two_shared(16, 6, seed=31)
+    Y = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.wl.group_offsets, [0, 0],
+                        shared=cat)["Y"]
+    x = torch.from_numpy(ref.widen(inp.X))
+    want = sum(_torch_swiglu_t(x, *(torch.from_numpy(w) for w in e)) for e in experts)
+    assert np.max(np.abs(Y - want.numpy())) < 1e-12
+
+
+def test_forward_with_shared_equals_dense_loop():
+    inp = _tiny_inputs([11, 6, 13], 8, 5, 12, seed=32, dtype="bf16")
+    experts, cat = _two_shared(8, 5, seed=33)
+    off, k = inp.wl.group_offsets, [3, 2, 5]
+    Y = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, shared=cat)["Y"]
+    Yl = ref.dense_loop_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, shared_experts=experts)
+    assert np.max(np.abs(Y - Yl)) < 1e-12
+
+
+def test_shared_backward_matches_finite_differences():
+    inp = _tiny_inputs([7, 5], 8, 3, 6, seed=34)
+    _, cat = _two_shared(8, 4, seed=35)
+    off, k, inv_tau = inp.wl.group_offsets, [2, 3], 1.3
+    args = [ref.widen(a) for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2)]
+    sh = [ref.widen(a) for a in cat]
+    dY = ref.widen(inp.dY)
+    g = ref.backward_ref(*args, dY, off, k, inv_tau, shared=tuple(sh))
+    sel = g["sel_token"]
+    rng = np.random.default_rng(1)
+    eps = 1e-6
+    for arr, name in [(args[0], "dX"), (sh[0], "dWs1"), (sh[1], "dWs3"), (sh[2], "dWs2")]:
+        flat = arr.reshape(-1)
+        for q in rng.choice(flat.size, size=min(20, flat.size), replace=False):
+            old = flat[q]
+            flat[q] = old + eps
+            lp = ref.loss_ref(*args, dY, off, k, inv_tau, sel, tuple(sh))
+            flat[q] = old - eps
+            lm = ref.loss_ref(*args, dY, off, k, inv_tau, sel, tuple(sh))
+            flat[q] = old
+            fd = (lp - lm) / (2 * eps)
+            an = g[name].reshape(-1)[q]
+            assert abs(fd - an) <= 1e-7 * max(1.0, abs(an)), (name, q, fd, an)
+
+
+def test_shared_backward_matches_torch_autograd():
+    inp = _tiny_inputs([8, 9], 16, 4, 8, seed=36, dtype="bf16")
+    _, cat = _two_shared(16, 8, seed=37)
+    off, k, inv_tau = inp.wl.group_offsets, [3, 4], 0.8
+    g = ref.backward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, off, k, inv_tau,
+                         shared=cat)
+    sel = g["sel_token"]
+    T = [torch.from_numpy(ref.widen(a)).requires_grad_(True)
+         for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2) + tuple(cat)]
+    X, Wg, W1, W3, W2, Ws1, Ws3, Ws2 = T
+    S = torch.softmax((X @ Wg.T) * inv_tau, dim=1)
+    Y = _torch_swiglu_t(X, Ws1, Ws3, Ws2)
+    for j in range(4):
+        rows = torch.from_numpy(sel[j])
+        Y = Y.index_add(0, rows, S[rows, j:j + 1] * _torch_swiglu_t(X[rows], W1[j], W3[j], W2[j]))
+    (Y * torch.from_numpy(ref.widen(inp.dY))).sum().backward()
+    for t, name in zip(T, ["dX", "dWg", "dW1", "dW3", "dW2", "dWs1", "dWs3", "dWs2"]):
+        assert np.max(np.abs(t.grad.numpy() - g[name])) < 1e-12, name
+
+
+def test_shared_restricted_forms_equal_full_definitions():
+    inp = _tiny_inputs([13, 10], 16, 3, 8, seed=38, dtype="bf16")
+    _, cat = _two_shared(16, 12, seed=39)
+    off, k, inv_tau = inp.wl.group_offsets, [4, 2], 1.1
+    full = ref.backward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, off, k, inv_tau,
+                            shared=cat)
+    sel = full["sel_token"]
+    Y = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, inv_tau, shared=cat)["Y"]
+    rows = [0, 3, 12, 13, 22]
+    assert np.max(np.abs(ref.forward_rows_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, sel, rows,
+                                              inv_tau, shared=cat) - Y[rows])) < 1e-12
+    assert np.max(np.abs(ref.backward_rows_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY,
+                                               sel, rows, inv_tau, shared=cat)
+                         - full["dX"][rows])) < 1e-12
+    units = [0, 7, 23]
+    g1, g3, g2 = ref.shared_grads_units_ref(inp.X, cat, inp.dY, units)
+    assert np.max(np.abs(g1 - full["dWs1"][units])) < 1e-12
+    assert np.max(np.abs(g3 - full["dWs3"][units])) < 1e-12
+    assert np.max(np.abs(g2 - full["dWs2"][:, units])) < 1e-12
+
+
 # --------------------------------------------------------------------- mutation tests
 
 def test_pins_catch_planted_mistakes(monkeypatch):
