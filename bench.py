@@ -7,7 +7,8 @@ Default workload: 8 sequences x 2048 tokens, d = 2048, 64 experts of hidden
 1024, per-sequence capacity c(t) = 12 - 8t (mask ratio t ~ U(0,1)), bf16
 storage, forward + backward.  Prints ONE JSON line on stdout.
 
-    python bench.py [--steps K] [--warmup W] [--workload train|static|timestep|fine|tiny]
+    python bench.py [--steps K] [--warmup W]
+                    [--workload train|train_shared|static|timestep|fine|tiny]
 """
 from __future__ import annotations
 
@@ -30,12 +31,15 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 GEMM_STAGES = {"gemm_w13_swiglu", "gemm_w2", "gemm_dA_swiglu_bwd", "gemm_dW2", "gemm_dXe",
-               "gemm_dW13", "router_dx", "router_dwg"}
+               "gemm_dW13", "router_dx", "router_dwg", "shared_w13_swiglu", "shared_w2",
+               "shared_dA_swiglu_bwd", "shared_dW2", "shared_dX", "shared_dW13"}
 
 
 # kernel-symbol stage tags of the grouped GEMMs (gemm_dma_kernel's last template argument)
 GEMM_TAGS = {"gemm_w13_swiglu": 1, "gemm_w2": 2, "gemm_dA_swiglu_bwd": 3, "gemm_dXe": 4,
-             "gemm_dW2": 5, "gemm_dW13": 6, "router_dx": 7, "router_dwg": 8}
+             "gemm_dW2": 5, "gemm_dW13": 6, "router_dx": 7, "router_dwg": 8,
+             "shared_w13_swiglu": 9, "shared_w2": 10, "shared_dA_swiglu_bwd": 11, "shared_dX": 12,
+             "shared_dW2": 13, "shared_dW13": 14}
 KERNEL_SOURCES = ["paper_2604_01622_amd/csrc/gemm.hip", "paper_2604_01622_amd/csrc/ec_common.h"]
 CALIB_BYTES = 1 << 30   # plain elementwise copy used to scale the byte counters
 
@@ -96,8 +100,9 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits):
-    """(algorithmic flops, algorithmic HBM bytes) of one launch of a stage."""
+def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits, hs=0):
+    """(algorithmic flops, algorithmic HBM bytes) of one launch of a stage (hs: hidden width
+    of the shared experts)."""
     P = E * K
     s = esz
     table = {
@@ -117,6 +122,12 @@ def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits):
         "router_dx": (2 * N * EP * d, N * EP * 2 + E * d * s + N * d * s),
         "bwd_combine": (0, E * N * 4 + P * d * s + 2 * N * d * s),
         "router_dwg": (2 * N * EP * d, N * EP * 2 + N * d * s + 2 * splits * E * d * 4),
+        "shared_w13_swiglu": (4 * N * d * hs, N * d * s + 2 * hs * d * s + 3 * N * hs * s),
+        "shared_w2": (2 * N * d * hs, N * hs * s + hs * d * s + 2 * N * d * s),
+        "shared_dA_swiglu_bwd": (2 * N * d * hs, N * d * s + hs * d * s + 4 * N * hs * s),
+        "shared_dW2": (2 * N * d * hs, N * d * s + N * hs * s + hs * d * s),
+        "shared_dX": (4 * N * d * hs, 2 * N * hs * s + 2 * hs * d * s + 2 * N * d * s),
+        "shared_dW13": (4 * N * d * hs, 2 * N * hs * s + N * d * s + 2 * hs * d * s),
     }
     return table[name]
 
@@ -139,10 +150,11 @@ def cpu_baseline(inp, caps, inv_tau, backward, budget_s=10.0):
         X = inp.X[lo:hi]
         t0 = time.perf_counter()
         fw = ref.forward_ref(X, inp.Wg, inp.W1, inp.W3, inp.W2, [0, hi - lo], [int(caps[g])],
-                             inv_tau)
+                             inv_tau, shared=inp.shared)
         if backward:
             ref.backward_ref(X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY[lo:hi], [0, hi - lo],
-                             [int(caps[g])], inv_tau, sel_token=fw["sel_token"])
+                             [int(caps[g])], inv_tau, sel_token=fw["sel_token"],
+                             shared=inp.shared)
         dt += time.perf_counter() - t0
         tokens += hi - lo
         groups += 1
@@ -161,7 +173,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="train",
-                    choices=["train", "static", "timestep", "fine", "tiny"])
+                    choices=["train", "train_shared", "static", "timestep", "fine", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forward-only", action="store_true")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -186,9 +198,10 @@ def main():
     import paper_2604_01622_amd as ec
     from paper_2604_01622_amd import binding, synth
 
-    wl = {"train": synth.TRAIN_BF16, "static": synth.STATIC_BF16, "timestep": synth.TIMESTEP_BF16,
+    wl = {"train": synth.TRAIN_BF16, "train_shared": synth.TRAIN_SHARED_BF16,
+          "static": synth.STATIC_BF16, "timestep": synth.TIMESTEP_BF16,
           "fine": synth.FINE_BF16, "tiny": synth.TINY_F32}[a.workload]
-    backward = a.workload == "train"
+    backward = a.workload in ("train", "train_shared")
     inv_tau = wl.inv_temperatures[0]
     torch.cuda.set_device(0)
     log(f"[bench] drawing {wl.name}")
@@ -206,7 +219,10 @@ def main():
 
     X, Wg, W1, W3, W2 = (dev(x) for x in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2))
     dY = dev(inp.dY) if backward else None
-    layer = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, training=backward)
+    shared = None if inp.shared is None else tuple(dev(w) for w in inp.shared)
+    hs = wl.d_shared
+    layer = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, training=backward,
+                     shared=shared)
     N, d, E, h, K = wl.n_tokens, wl.d_model, wl.n_experts, wl.d_ff, layer.P.K
     esz = 2 if wl.dtype == "bf16" else 4
     EP = (E + 63) // 64 * 64
@@ -253,9 +269,11 @@ def main():
     if backward:
         for n, col in zip(binding.BACKWARD_STAGES, zip(*[e.durations_ms() for e in bwd_ev])):
             stage_ms[n] = float(np.mean(col))
+    if not hs:   # the shared-expert stages are empty
+        stage_ms = {n: t for n, t in stage_ms.items() if not n.startswith("shared_")}
     stages = {}
     for n, t in stage_ms.items():
-        fl, by = stage_work(n, N, d, E, h, K, esz, EP, backward, splits)
+        fl, by = stage_work(n, N, d, E, h, K, esz, EP, backward, splits, hs)
         st = {"ms": round(t, 4)}
         if n in GEMM_STAGES:
             st["tflops"] = round(fl / (t * 1e-3) / 1e12, 1)
@@ -265,7 +283,7 @@ def main():
             st["hbm_frac"] = round(by / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
         stages[n] = st
     dom = max(stage_ms, key=stage_ms.get)
-    fl, by = stage_work(dom, N, d, E, h, K, esz, EP, backward, splits)
+    fl, by = stage_work(dom, N, d, E, h, K, esz, EP, backward, splits, hs)
     t_dom = stage_ms[dom] * 1e-3
     traffic = None
     tf = os.path.join(ROOT, "profiles", f"traffic_{dom}.json")
@@ -283,9 +301,9 @@ def main():
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(by / t_dom / 1e9, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(by / t_dom / 1e9 / PEAK_HBM_GBS, 4),
                 "traffic": traffic, "work_per_launch": by, "avg_launch_ms": round(stage_ms[dom], 4)}
-    gemm_fl = sum(stage_work(n, N, d, E, h, K, esz, EP, backward, splits)[0]
-                  for n in stage_ms if n.startswith("gemm_"))
-    gemm_ms = sum(stage_ms[n] for n in stage_ms if n.startswith("gemm_"))
+    gemm_fl = sum(stage_work(n, N, d, E, h, K, esz, EP, backward, splits, hs)[0]
+                  for n in stage_ms if n.startswith("gemm_") or n.startswith("shared_"))
+    gemm_ms = sum(stage_ms[n] for n in stage_ms if n.startswith("gemm_") or n.startswith("shared_"))
 
     out = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
            "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 4),
@@ -293,7 +311,8 @@ def main():
            "dtype": wl.dtype, "data": "synthetic (seeded normal inputs and random-init weights)",
            "config": {"workload": wl.name, "pass": "fwd+bwd" if backward else "fwd",
                       "tokens": N, "groups": wl.n_groups, "d_model": d, "experts": E,
-                      "d_ff": h, "k_per_group": [int(x) for x in caps], "K_tot": K},
+                      "d_ff": h, "shared_hidden": hs, "k_per_group": [int(x) for x in caps],
+                      "K_tot": K},
            "stages": stages, "roofline": roof,
            "grouped_gemm": {"tflops": round(gemm_fl / (gemm_ms * 1e-3) / 1e12, 1),
                             "mfma_frac": round(gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
@@ -310,7 +329,8 @@ def main():
 
     if backward and not a.no_forward_only:
         # forward alone, inference mode (no saved activations), same inputs
-        inf = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, training=False)
+        inf = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, training=False,
+                       shared=shared)
         for _ in range(a.warmup):
             inf.forward()
         torch.cuda.synchronize()

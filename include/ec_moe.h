@@ -70,7 +70,7 @@ typedef enum {
 
 /* Problem description.  Limits: 1 <= E <= 256; d and h multiples of 64 with
  * 64 <= d, h <= 16384; 1 <= G; N = group_offsets[G] < 2^31; every expert
- * buffer E * K_tot * max(d, h) < 2^31 elements.                               */
+ * buffer E * K_tot * max(d, h) < 2^31 elements; N * 2 * max(d, hs) < 2^31.    */
 typedef struct {
   int64_t n_tokens;              /* N = sum of the group lengths                       */
   int32_t d_model;               /* d                                                  */
@@ -83,6 +83,13 @@ typedef struct {
                                     0 <= k_g <= off[g+1] - off[g]                       */
   float inv_temperature;         /* 1/tau > 0; S = softmax(logits * inv_temperature)   */
   ec_dtype dtype;                /* storage dtype                                      */
+  int32_t d_shared;              /* hidden width hs of the shared experts, 0 for none:
+                                    n_s shared SwiGLU experts of width h_s are one
+                                    SwiGLU of width hs = n_s h_s (hidden units side by
+                                    side), applied to every token and added to y
+                                    without a gate (Appendix D: shared experts process
+                                    all tokens; Appendix E: 2 per layer).  0 or a
+                                    multiple of 64 in [64, 16384].                      */
 } ec_problem;
 
 /* Byte offsets of the forward activations inside the `saved` buffer that
@@ -99,6 +106,9 @@ typedef struct {
   size_t H3;         /* dtype [E, K, h] W3 projection                           */
   size_t A;          /* dtype [E, K, h] SiLU(H1) * H3                           */
   size_t O;          /* dtype [E, K, d] expert outputs (not gate-scaled)        */
+  size_t Hs1;        /* dtype [N, hs]   shared experts' W1 projection           */
+  size_t Hs3;        /* dtype [N, hs]   shared experts' W3 projection           */
+  size_t As;         /* dtype [N, hs]   shared experts' SiLU(Hs1) * Hs3         */
   size_t total;      /* bytes of the whole buffer                               */
 } ec_saved_layout;
 
@@ -153,12 +163,16 @@ int ec_token_coverage(const ec_problem *p, const int32_t *slot,
                       hipStream_t stream);
 
 /* Layer forward: routing, gather, SwiGLU experts as a grouped GEMM, and the
- * gate-weighted combine (Section 2.2, Appendix E).
- *   W1, W3 [E, h, d] dtype;  W2 [E, d, h] dtype;  Y [N, d] dtype out.
+ * gate-weighted combine (Section 2.2, Appendix E), plus the shared experts'
+ * FFN of every token when p->d_shared > 0.
+ *   W1, W3 [E, h, d] dtype;  W2 [E, d, h] dtype;
+ *   Ws1, Ws3 [hs, d] dtype;  Ws2 [d, hs] dtype (NULL when d_shared = 0);
+ *   Y [N, d] dtype out.
  * saved: NULL for inference, else ec_saved_layout.total bytes that receive the
  * activations the backward needs.  ws: ec_workspace_size(p, 1) bytes.         */
 int ec_moe_forward(const ec_problem *p, const void *X, const void *Wg,
-                   const void *W1, const void *W3, const void *W2, void *Y,
+                   const void *W1, const void *W3, const void *W2,
+                   const void *Ws1, const void *Ws3, const void *Ws2, void *Y,
                    void *saved, size_t saved_bytes,
                    void *ws, size_t ws_bytes, hipStream_t stream);
 
@@ -167,12 +181,15 @@ int ec_moe_forward(const ec_problem *p, const void *X, const void *Wg,
  * values S_ij of the selected pairs and the softmax).
  *   dY [N, d] dtype;  saved: filled by ec_moe_forward with the same inputs;
  *   dX [N, d] dtype out;  dWg [E, d] fp32 out;  dW1, dW3 [E, h, d] and
- *   dW2 [E, d, h] dtype out (overwritten, not accumulated).
+ *   dW2 [E, d, h] dtype out;  dWs1, dWs3 [hs, d] and dWs2 [d, hs] dtype out
+ *   (NULL when d_shared = 0).  Outputs are overwritten, not accumulated.
  * ws: ec_workspace_size(p, 2) bytes.                                           */
 int ec_moe_backward(const ec_problem *p, const void *X, const void *Wg,
                     const void *W1, const void *W3, const void *W2,
+                    const void *Ws1, const void *Ws3, const void *Ws2,
                     const void *dY, const void *saved, size_t saved_bytes,
                     void *dX, float *dWg, void *dW1, void *dW3, void *dW2,
+                    void *dWs1, void *dWs3, void *dWs2,
                     void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Stage timing for profiling.  After this call, every entry point called on
@@ -181,10 +198,12 @@ int ec_moe_backward(const ec_problem *p, const void *X, const void *Wg,
  * hipEventElapsedTime(events[s], events[s+1]) is the duration of stage s.
  * The caller creates and owns the events; pass NULL / 0 to stop recording.
  * Stages of ec_moe_forward: 0 router+softmax, 1 top-k, 2 gather,
- *   3 W1/W3 grouped GEMM + SwiGLU, 4 W2 grouped GEMM, 5 combine.
+ *   3 W1/W3 grouped GEMM + SwiGLU, 4 W2 grouped GEMM, 5 shared W1/W3 + SwiGLU,
+ *   6 shared W2, 7 combine (5 and 6 are empty without shared experts).
  * Stages of ec_moe_backward: 0 dY gather + gate gradient, 1 dA grouped GEMM +
  *   SwiGLU backward, 2 dW2, 3 dXe, 4 dW1/dW3, 5 router dZ, 6 router dX,
- *   7 combine of dXe, 8 dWg.
+ *   7 shared dA + SwiGLU backward, 8 shared dW2, 9 shared dX, 10 shared
+ *   dW1/dW3 (7-10 empty without shared experts), 11 combine of dXe, 12 dWg.
  * Stages of ec_route: 0 router+softmax, 1 top-k.                              */
 int ec_set_stage_events(hipEvent_t *events /* HOST array */, int n_events);
 

@@ -36,12 +36,12 @@ class _Problem(ctypes.Structure):
                 ("n_experts", ctypes.c_int32), ("d_ff", ctypes.c_int32),
                 ("n_groups", ctypes.c_int32), ("group_offsets", ctypes.POINTER(ctypes.c_int32)),
                 ("capacity", ctypes.POINTER(ctypes.c_int32)), ("inv_temperature", ctypes.c_float),
-                ("dtype", ctypes.c_int)]
+                ("dtype", ctypes.c_int), ("d_shared", ctypes.c_int32)]
 
 
 class _SavedLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in ("S", "sel_token", "slot", "Xe", "H1", "H3", "A",
-                                               "O", "total")]
+                                               "O", "Hs1", "Hs3", "As", "total")]
 
 
 _lib = None
@@ -76,10 +76,9 @@ def lib() -> ctypes.CDLL:
         L.ec_token_coverage.restype = ctypes.c_int
         L.ec_token_coverage.argtypes = [pp, vp, vp, vp, vp]
         L.ec_moe_forward.restype = ctypes.c_int
-        L.ec_moe_forward.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, sz, vp, sz, vp]
+        L.ec_moe_forward.argtypes = [pp] + [vp] * 9 + [vp, sz, vp, sz, vp]
         L.ec_moe_backward.restype = ctypes.c_int
-        L.ec_moe_backward.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp, vp, vp, vp, vp,
-                                      sz, vp]
+        L.ec_moe_backward.argtypes = [pp] + [vp] * 9 + [vp, sz] + [vp] * 8 + [vp, sz, vp]
         L.ec_set_stage_events.restype = ctypes.c_int
         L.ec_set_stage_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
         _lib = L
@@ -114,7 +113,7 @@ class Problem:
 
     def __init__(self, n_tokens: int, d_model: int, n_experts: int, d_ff: int,
                  group_offsets: Sequence[int], capacity: Sequence[int], inv_temperature: float,
-                 dtype: torch.dtype):
+                 dtype: torch.dtype, d_shared: int = 0):
         self.off = np.ascontiguousarray(np.asarray(group_offsets, dtype=np.int32))
         self.cap = np.ascontiguousarray(np.asarray(capacity, dtype=np.int32))
         self.dtype = dtype
@@ -122,7 +121,7 @@ class Problem:
                           int(len(self.cap)),
                           self.off.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                           self.cap.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-                          float(inv_temperature), _dtype_code(dtype))
+                          float(inv_temperature), _dtype_code(dtype), int(d_shared))
 
     @property
     def ref(self):
@@ -150,9 +149,9 @@ class Problem:
 
     @staticmethod
     def of(X: torch.Tensor, Wg: torch.Tensor, d_ff: int, group_offsets, capacity,
-           inv_temperature: float = 1.0) -> "Problem":
+           inv_temperature: float = 1.0, shared=None) -> "Problem":
         return Problem(X.shape[0], X.shape[1], Wg.shape[0], d_ff, group_offsets, capacity,
-                       inv_temperature, X.dtype)
+                       inv_temperature, X.dtype, 0 if shared is None else shared[0].shape[0])
 
 
 def _empty(nbytes: int, device) -> torch.Tensor:
@@ -208,31 +207,44 @@ def token_coverage(slot: torch.Tensor, group_offsets, capacity, d_model: int = 6
     return cnt, dropped
 
 
-def forward(X, Wg, W1, W3, W2, group_offsets, capacity, inv_temperature=1.0, save=False):
-    """Layer forward.  Returns Y [N,d] (and the saved-activation buffer if save)."""
-    P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature)
+def _shared_ptrs(shared):
+    return [None, None, None] if shared is None else [_ptr(w) for w in shared]
+
+
+def forward(X, Wg, W1, W3, W2, group_offsets, capacity, inv_temperature=1.0, save=False,
+            shared=None):
+    """Layer forward.  shared: (Ws1 [hs,d], Ws3 [hs,d], Ws2 [d,hs]) of the shared experts or
+    None.  Returns Y [N,d] (and the saved-activation buffer if save)."""
+    P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature, shared)
     dev = X.device
     Y = torch.empty_like(X)
     saved = _empty(P.saved_layout()["total"], dev) if save else None
     ws = _empty(P.workspace_size(1), dev)
-    _check(lib().ec_moe_forward(P.ref, _ptr(X), _ptr(Wg), _ptr(W1), _ptr(W3), _ptr(W2), _ptr(Y),
-                                _ptr(saved), 0 if saved is None else saved.numel(), _ptr(ws),
-                                ws.numel(), _stream()))
+    _check(lib().ec_moe_forward(P.ref, _ptr(X), _ptr(Wg), _ptr(W1), _ptr(W3), _ptr(W2),
+                                *_shared_ptrs(shared), _ptr(Y), _ptr(saved),
+                                0 if saved is None else saved.numel(), _ptr(ws), ws.numel(),
+                                _stream()))
     return (Y, saved) if save else Y
 
 
-def backward(X, Wg, W1, W3, W2, dY, saved, group_offsets, capacity, inv_temperature=1.0):
-    """Layer backward.  Returns dX, dWg (fp32), dW1, dW3, dW2."""
-    P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature)
+def backward(X, Wg, W1, W3, W2, dY, saved, group_offsets, capacity, inv_temperature=1.0,
+             shared=None):
+    """Layer backward.  Returns dX, dWg (fp32), dW1, dW3, dW2 (and dWs1, dWs3, dWs2 with
+    shared experts)."""
+    P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature, shared)
     dev = X.device
     dX = torch.empty_like(X)
     dWg = torch.empty(Wg.shape, dtype=torch.float32, device=dev)
     dW1, dW3, dW2 = torch.empty_like(W1), torch.empty_like(W3), torch.empty_like(W2)
+    dsh = None if shared is None else [torch.empty_like(w) for w in shared]
     ws = _empty(P.workspace_size(2), dev)
-    _check(lib().ec_moe_backward(P.ref, _ptr(X), _ptr(Wg), _ptr(W1), _ptr(W3), _ptr(W2), _ptr(dY),
-                                 _ptr(saved), saved.numel(), _ptr(dX), _ptr(dWg), _ptr(dW1),
-                                 _ptr(dW3), _ptr(dW2), _ptr(ws), ws.numel(), _stream()))
-    return dX, dWg, dW1, dW3, dW2
+    _check(lib().ec_moe_backward(P.ref, _ptr(X), _ptr(Wg), _ptr(W1), _ptr(W3), _ptr(W2),
+                                 *_shared_ptrs(shared), _ptr(dY), _ptr(saved), saved.numel(),
+                                 _ptr(dX), _ptr(dWg), _ptr(dW1), _ptr(dW3), _ptr(dW2),
+                                 *_shared_ptrs(dsh), _ptr(ws), ws.numel(), _stream()))
+    if shared is None:
+        return dX, dWg, dW1, dW3, dW2
+    return (dX, dWg, dW1, dW3, dW2) + tuple(dsh)
 
 
 def saved_views(saved: torch.Tensor, P: Problem) -> dict:
@@ -251,7 +263,10 @@ def saved_views(saved: torch.Tensor, P: Problem) -> dict:
             "slot": view(lay["slot"], (E, N), torch.int32, 4),
             "Xe": view(lay["Xe"], (E, K, d), dt, es), "H1": view(lay["H1"], (E, K, h), dt, es),
             "H3": view(lay["H3"], (E, K, h), dt, es), "A": view(lay["A"], (E, K, h), dt, es),
-            "O": view(lay["O"], (E, K, d), dt, es)}
+            "O": view(lay["O"], (E, K, d), dt, es),
+            "Hs1": view(lay["Hs1"], (N, P.c.d_shared), dt, es),
+            "Hs3": view(lay["Hs3"], (N, P.c.d_shared), dt, es),
+            "As": view(lay["As"], (N, P.c.d_shared), dt, es)}
 
 
 class Layer:
@@ -259,9 +274,10 @@ class Layer:
     that repeated calls only enqueue kernels (used by the benchmark)."""
 
     def __init__(self, X, Wg, W1, W3, W2, group_offsets, capacity, inv_temperature=1.0,
-                 training=False):
+                 training=False, shared=None):
         self.X, self.Wg, self.W1, self.W3, self.W2 = X, Wg, W1, W3, W2
-        self.P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature)
+        self.shared = shared
+        self.P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature, shared)
         dev = X.device
         self.Y = torch.empty_like(X)
         self.saved = _empty(self.P.saved_layout()["total"], dev) if training else None
@@ -272,27 +288,33 @@ class Layer:
             self.dWg = torch.empty(Wg.shape, dtype=torch.float32, device=dev)
             self.dW1, self.dW3 = torch.empty_like(W1), torch.empty_like(W3)
             self.dW2 = torch.empty_like(W2)
+            self.dshared = None if shared is None else [torch.empty_like(w) for w in shared]
         self._fwd_args = None
 
     def forward(self):
         _check(lib().ec_moe_forward(self.P.ref, _ptr(self.X), _ptr(self.Wg), _ptr(self.W1),
-                                    _ptr(self.W3), _ptr(self.W2), _ptr(self.Y), _ptr(self.saved),
+                                    _ptr(self.W3), _ptr(self.W2), *_shared_ptrs(self.shared),
+                                    _ptr(self.Y), _ptr(self.saved),
                                     0 if self.saved is None else self.saved.numel(),
                                     _ptr(self.ws_f), self.ws_f.numel(), _stream()))
         return self.Y
 
     def backward(self, dY):
         _check(lib().ec_moe_backward(self.P.ref, _ptr(self.X), _ptr(self.Wg), _ptr(self.W1),
-                                     _ptr(self.W3), _ptr(self.W2), _ptr(dY), _ptr(self.saved),
+                                     _ptr(self.W3), _ptr(self.W2), *_shared_ptrs(self.shared),
+                                     _ptr(dY), _ptr(self.saved),
                                      self.saved.numel(), _ptr(self.dX), _ptr(self.dWg),
                                      _ptr(self.dW1), _ptr(self.dW3), _ptr(self.dW2),
+                                     *_shared_ptrs(self.dshared),
                                      _ptr(self.ws_b), self.ws_b.numel(), _stream()))
         return self.dX, self.dWg, self.dW1, self.dW3, self.dW2
 
 
-FORWARD_STAGES = ("router", "topk", "gather", "gemm_w13_swiglu", "gemm_w2", "combine")
+FORWARD_STAGES = ("router", "topk", "gather", "gemm_w13_swiglu", "gemm_w2", "shared_w13_swiglu",
+                  "shared_w2", "combine")
 BACKWARD_STAGES = ("bwd_gather", "gemm_dA_swiglu_bwd", "gemm_dW2", "gemm_dXe", "gemm_dW13",
-                   "router_dz", "router_dx", "bwd_combine", "router_dwg")
+                   "router_dz", "router_dx", "shared_dA_swiglu_bwd", "shared_dW2", "shared_dX",
+                   "shared_dW13", "bwd_combine", "router_dwg")
 
 
 class StageEvents:

@@ -36,6 +36,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Plan {
   int N = 0, d = 0, E = 0, h = 0, G = 0, EP = 0;
+  int hs = 0;          // hidden width of the shared experts (0: none)
   long K = 0;          // K_tot
   int dtype = 0;
   size_t esz = 0;      // storage bytes per element
@@ -56,6 +57,9 @@ int validate(const ec_problem* p, Plan* out) {
                 p->d_model);
   if (p->d_ff < 64 || p->d_ff > 16384 || p->d_ff % 64)
     return fail(EC_ERR_SHAPE, "d_ff must be a multiple of 64 in [64, 16384] (got %d)", p->d_ff);
+  if (p->d_shared != 0 && (p->d_shared < 64 || p->d_shared > 16384 || p->d_shared % 64))
+    return fail(EC_ERR_SHAPE, "d_shared must be 0 or a multiple of 64 in [64, 16384] (got %d)",
+                p->d_shared);
   if (!std::isfinite(p->inv_temperature) || !(p->inv_temperature > 0.f))
     return fail(EC_ERR_ARG, "inv_temperature must be finite and > 0");
   if (p->n_tokens < 0 || p->n_tokens >= (int64_t)1 << 31)
@@ -76,13 +80,16 @@ int validate(const ec_problem* p, Plan* out) {
                 (long long)p->n_tokens);
   const int64_t maxw = p->d_model > p->d_ff ? p->d_model : p->d_ff;
   if ((int64_t)p->n_experts * K * 2 * maxw >= ((int64_t)1 << 31) ||
-      (int64_t)p->n_experts * p->n_tokens >= ((int64_t)1 << 31))
+      (int64_t)p->n_experts * p->n_tokens >= ((int64_t)1 << 31) ||
+      p->n_tokens * 2 * (int64_t)(p->d_shared > p->d_model ? p->d_shared : p->d_model) >=
+          ((int64_t)1 << 31))
     return fail(EC_ERR_SHAPE, "problem too large for 32-bit element indices");
   Plan& P = *out;
   P.N = (int)p->n_tokens;
   P.d = p->d_model;
   P.E = p->n_experts;
   P.h = p->d_ff;
+  P.hs = p->d_shared;
   P.G = p->n_groups;
   P.K = K;
   P.EP = (P.E + 63) / 64 * 64;
@@ -112,6 +119,9 @@ struct Saved {
   void* H3;
   void* A;
   void* O;
+  void* Hs1;      // shared experts, [N, hs] each (null when there are none)
+  void* Hs3;
+  void* As;
 };
 
 Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
@@ -124,6 +134,10 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
   s.H3 = with_h ? c.take((size_t)P.E * P.K * P.h * P.esz) : nullptr;
   s.A = c.take((size_t)P.E * P.K * P.h * P.esz);
   s.O = c.take((size_t)P.E * P.K * P.d * P.esz);
+  const size_t sh = (size_t)P.N * P.hs * P.esz;
+  s.Hs1 = (with_h && sh) ? c.take(sh) : nullptr;
+  s.Hs3 = (with_h && sh) ? c.take(sh) : nullptr;
+  s.As = sh ? c.take(sh) : nullptr;
   return s;
 }
 
@@ -135,6 +149,9 @@ struct BwdWs {
   uint16_t* dZb;  // [N, EP] (bf16 only)
   float* part;    // [splits, E, d]
   int splits;
+  void* dHs;      // [N, 2 hs] shared experts' dH1 | dH3
+  float* spart;   // split-K partials of the shared weight gradients
+  int s_splits2, s_splits13;
 };
 
 BwdWs carve_bwd(Carve& c, const Plan& P) {
@@ -146,6 +163,16 @@ BwdWs carve_bwd(Carve& c, const Plan& P) {
   w.dZb = P.dtype == EC_BF16 ? (uint16_t*)c.take((size_t)P.N * P.EP * 2) : nullptr;
   w.splits = ec::router_dwg_splits(P.N, P.E, P.d);
   w.part = (float*)c.take((size_t)w.splits * P.E * P.d * 4);
+  w.dHs = nullptr;
+  w.spart = nullptr;
+  w.s_splits2 = w.s_splits13 = 0;
+  if (P.hs) {
+    w.dHs = c.take((size_t)P.N * 2 * P.hs * P.esz);
+    w.s_splits2 = ec::wgrad_splits(P.d, P.hs, P.N);
+    w.s_splits13 = ec::wgrad_splits(2 * P.hs, P.d, P.N);
+    const size_t a = (size_t)w.s_splits2 * P.d * P.hs, b = (size_t)w.s_splits13 * 2 * P.hs * P.d;
+    if (P.dtype == EC_BF16) w.spart = (float*)c.take((a > b ? a : b) * 4);
+  }
   return w;
 }
 
@@ -275,26 +302,22 @@ int ec_saved_layout_of(const ec_problem* p, ec_saved_layout* out) {
   Plan P;
   EC_TRY(validate(p, &P));
   if (!out) return fail(EC_ERR_ARG, "out is NULL");
-  // carve an imaginary buffer at address 0 and read the offsets back
-  Carve m(nullptr);
-  size_t offs[8];
-  int n = 0;
-  const size_t sizes[8] = {(size_t)P.N * P.E * 4, (size_t)P.E * P.K * 4, (size_t)P.E * P.N * 4,
-                           (size_t)P.E * P.K * P.d * P.esz, (size_t)P.E * P.K * P.h * P.esz,
-                           (size_t)P.E * P.K * P.h * P.esz, (size_t)P.E * P.K * P.h * P.esz,
-                           (size_t)P.E * P.K * P.d * P.esz};
-  for (size_t b : sizes) {
-    offs[n++] = m.used;
-    m.take(b);
-  }
-  out->S = offs[0];
-  out->sel_token = offs[1];
-  out->slot = offs[2];
-  out->Xe = offs[3];
-  out->H1 = offs[4];
-  out->H3 = offs[5];
-  out->A = offs[6];
-  out->O = offs[7];
+  // carve an imaginary buffer at a nominal address and read the offsets back
+  char* const base = (char*)(uintptr_t)4096;
+  Carve m(base);
+  const Saved s = carve_saved(m, P, true);
+  auto off = [&](const void* q) -> size_t { return q ? (size_t)((const char*)q - base) : m.used; };
+  out->S = off(s.S);
+  out->sel_token = off(s.sel);
+  out->slot = off(s.slot);
+  out->Xe = off(s.Xe);
+  out->H1 = off(s.H1);
+  out->H3 = off(s.H3);
+  out->A = off(s.A);
+  out->O = off(s.O);
+  out->Hs1 = off(s.Hs1);
+  out->Hs3 = off(s.Hs3);
+  out->As = off(s.As);
   out->total = m.used;
   return EC_OK;
 }
@@ -385,8 +408,9 @@ int ec_token_coverage(const ec_problem* p, const int32_t* slot, int32_t* experts
 }
 
 int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const void* W1,
-                   const void* W3, const void* W2, void* Y, void* saved, size_t saved_bytes_in,
-                   void* ws, size_t ws_bytes, hipStream_t stream) {
+                   const void* W3, const void* W2, const void* Ws1, const void* Ws3,
+                   const void* Ws2, void* Y, void* saved, size_t saved_bytes_in, void* ws,
+                   size_t ws_bytes, hipStream_t stream) {
   Plan P;
   EC_TRY(validate(p, &P));
   EC_TRY(check_ptr(X, "X"));
@@ -394,6 +418,9 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
   EC_TRY(check_ptr(W1, "W1"));
   EC_TRY(check_ptr(W3, "W3"));
   EC_TRY(check_ptr(W2, "W2"));
+  EC_TRY(check_ptr(Ws1, "Ws1", P.hs == 0));
+  EC_TRY(check_ptr(Ws3, "Ws3", P.hs == 0));
+  EC_TRY(check_ptr(Ws2, "Ws2", P.hs == 0));
   EC_TRY(check_ptr(Y, "Y"));
   EC_TRY(check_ptr(saved, "saved", true));
   if (saved && saved_bytes_in < saved_bytes(P))
@@ -422,15 +449,28 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
   EC_HIP(mark(4, stream));
   EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream));
   EC_HIP(mark(5, stream));
-  EC_HIP(ec::launch_combine(P.dtype, s.O, s.S, s.slot, Y, P.N, P.E, M, P.d, stream));
-  EC_HIP(mark(6, stream));
+  if (P.hs) {
+    // shared experts on every token; their output goes to Y and the combine adds
+    // the routed sum to it
+    EC_HIP(ec::launch_gemm_w13(P.dtype, X, Ws1, Ws3, s.As, s.Hs1, s.Hs3, 1, P.N, P.d, P.hs,
+                               stream, true));
+    EC_HIP(mark(6, stream));
+    EC_HIP(ec::launch_gemm_w2(P.dtype, s.As, Ws2, Y, 1, P.N, P.d, P.hs, stream, true));
+  } else {
+    EC_HIP(mark(6, stream));
+  }
+  EC_HIP(mark(7, stream));
+  EC_HIP(ec::launch_combine(P.dtype, s.O, s.S, s.slot, P.hs ? Y : nullptr, Y, P.N, P.E, M, P.d,
+                            stream));
+  EC_HIP(mark(8, stream));
   return EC_OK;
 }
 
 int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const void* W1,
-                    const void* W3, const void* W2, const void* dY, const void* saved,
-                    size_t saved_bytes_in, void* dX, float* dWg, void* dW1, void* dW3, void* dW2,
-                    void* ws, size_t ws_bytes, hipStream_t stream) {
+                    const void* W3, const void* W2, const void* Ws1, const void* Ws3,
+                    const void* Ws2, const void* dY, const void* saved, size_t saved_bytes_in,
+                    void* dX, float* dWg, void* dW1, void* dW3, void* dW2, void* dWs1,
+                    void* dWs3, void* dWs2, void* ws, size_t ws_bytes, hipStream_t stream) {
   Plan P;
   EC_TRY(validate(p, &P));
   EC_TRY(check_ptr(X, "X"));
@@ -438,6 +478,9 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   EC_TRY(check_ptr(W1, "W1"));
   EC_TRY(check_ptr(W3, "W3"));
   EC_TRY(check_ptr(W2, "W2"));
+  EC_TRY(check_ptr(Ws1, "Ws1", P.hs == 0));
+  EC_TRY(check_ptr(Ws3, "Ws3", P.hs == 0));
+  EC_TRY(check_ptr(Ws2, "Ws2", P.hs == 0));
   EC_TRY(check_ptr(dY, "dY"));
   EC_TRY(check_ptr(saved, "saved"));
   EC_TRY(check_ptr(dX, "dX"));
@@ -445,6 +488,9 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   EC_TRY(check_ptr(dW1, "dW1"));
   EC_TRY(check_ptr(dW3, "dW3"));
   EC_TRY(check_ptr(dW2, "dW2"));
+  EC_TRY(check_ptr(dWs1, "dWs1", P.hs == 0));
+  EC_TRY(check_ptr(dWs3, "dWs3", P.hs == 0));
+  EC_TRY(check_ptr(dWs2, "dWs2", P.hs == 0));
   if (saved_bytes_in < saved_bytes(P))
     return fail(EC_ERR_WORKSPACE, "saved buffer %zu bytes < %zu required", saved_bytes_in,
                 saved_bytes(P));
@@ -458,7 +504,7 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   Carve c(ws);
   const BwdWs w = carve_bwd(c, P);
   const int M = (int)P.K;
-  const int E = P.E, d = P.d, h = P.h, N = P.N;
+  const int E = P.E, d = P.d, h = P.h, N = P.N, hs = P.hs;
   void* dXe = w.dO;  // dO is dead once dW2 is formed
   EC_HIP(mark(0, stream));
   EC_HIP(ec::launch_bwd_gather(P.dtype, dY, s.O, s.S, s.sel, w.dO, w.dSp, N, E, M, d, stream));
@@ -477,10 +523,31 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   const void* dZop = P.dtype == EC_BF16 ? (const void*)w.dZb : (const void*)w.dZ;
   EC_HIP(ec::launch_router_dx(P.dtype, dZop, Wg, dX, N, E, P.EP, d, stream));
   EC_HIP(mark(7, stream));
+  if (hs && N > 0) {
+    // shared experts: their output gradient is dY itself (no gate)
+    EC_HIP(ec::launch_gemm_dA(P.dtype, dY, Ws2, s.Hs1, s.Hs3, w.dHs, 1, N, d, hs, stream, true));
+    EC_HIP(mark(8, stream));
+    EC_HIP(ec::launch_shared_dW2(P.dtype, dY, s.As, dWs2, N, d, hs, w.spart, w.s_splits2, stream));
+    EC_HIP(mark(9, stream));
+    EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dHs, Ws1, Ws3, dX, 1, N, d, hs, stream, true));
+    EC_HIP(mark(10, stream));
+    EC_HIP(ec::launch_shared_dW13(P.dtype, w.dHs, X, dWs1, dWs3, N, d, hs, w.spart,
+                                  w.s_splits13, stream));
+  } else {
+    if (hs) {   // no tokens: zero shared weight gradients
+      EC_HIP(ec::launch_zero(dWs1, (size_t)hs * d * P.esz, stream));
+      EC_HIP(ec::launch_zero(dWs3, (size_t)hs * d * P.esz, stream));
+      EC_HIP(ec::launch_zero(dWs2, (size_t)hs * d * P.esz, stream));
+    }
+    EC_HIP(mark(8, stream));
+    EC_HIP(mark(9, stream));
+    EC_HIP(mark(10, stream));
+  }
+  EC_HIP(mark(11, stream));
   EC_HIP(ec::launch_bwd_combine(P.dtype, dXe, s.slot, dX, dX, N, E, M, d, stream));
-  EC_HIP(mark(8, stream));
+  EC_HIP(mark(12, stream));
   EC_HIP(ec::launch_router_dwg(P.dtype, dZop, X, dWg, w.part, w.splits, N, E, P.EP, d, stream));
-  EC_HIP(mark(9, stream));
+  EC_HIP(mark(13, stream));
   return EC_OK;
 }
 

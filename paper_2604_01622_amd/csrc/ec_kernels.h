@@ -32,9 +32,10 @@ hipError_t launch_topk(const float* ST, int N, int E, int K, const GroupTable& t
 hipError_t launch_gather(int dtype, const void* X, const int32_t* sel_token, void* Xe,
                          long rows, int d, int N, hipStream_t st);
 
-// Y[i, :] = sum_j S[i,j] O[j, slotT[j,i], :] over experts j with slotT[j,i] >= 0.
+// Y[i, :] = Xr[i, :] (if Xr) + sum_j S[i,j] O[j, slotT[j,i], :] over experts j with
+// slotT[j,i] >= 0 (Xr may alias Y).
 hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_t* slotT,
-                          void* Y, int N, int E, int K, int d, hipStream_t st);
+                          const void* Xr, void* Y, int N, int E, int K, int d, hipStream_t st);
 
 // Backward gather: dO[j,r,:] = S[i,j] dY[i,:] and dS[i,j] = <dY[i,:], O[j,r,:]>,
 // i = sel_token[j,r]; dS [N,E] fp32 is zero for unselected pairs.
@@ -66,17 +67,21 @@ int router_dwg_splits(int N, int E, int d);
 // ---- grouped GEMMs over E experts (M = K rows per expert) ----
 
 // H = Xe W1^T, Xe W3^T -> A = SiLU(H1) * H3 (and H1, H3 if non-null).
+// `shared`: the same product for the shared experts (own kernel symbol).
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
-                           void* H1, void* H3, int E, int M, int d, int h, hipStream_t st);
+                           void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
+                           bool shared = false);
 // O = A W2^T.
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
-                          int h, hipStream_t st);
+                          int h, hipStream_t st, bool shared = false);
 // dA = dO W2 and the SwiGLU backward: dH[:, 0:h] = dH1, dH[:, h:2h] = dH3 ([E,M,2h]).
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
-                          const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st);
+                          const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
+                          bool shared = false);
 // dXe = dH1 W1 + dH3 W3  ([E,M,d]).
+// shared: dXe += dH1 W1 + dH3 W3 (the shared experts' term added to dX).
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
-                           int E, int M, int d, int h, hipStream_t st);
+                           int E, int M, int d, int h, hipStream_t st, bool shared = false);
 // dW2 = dO^T A  ([E,d,h]).
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
                            int d, int h, hipStream_t st);
@@ -90,6 +95,16 @@ hipError_t launch_coverage_count(const int32_t* slotT, int N, int E, int32_t* cn
                                  hipStream_t st);
 hipError_t launch_coverage_drop(const int32_t* cnt, const GroupTable& tab, int32_t* dropped,
                                 hipStream_t st);
+
+// Shared experts' weight gradients (one batch of N rows, K-major operands):
+// dW2 = dY^T A ([d,h]) and [dW1; dW3] = dH^T X ([h,d] each), split over the
+// rows into `splits` fp32 partials (part: splits * max(d*h, 2*h*d) floats)
+// added in a fixed order.
+int wgrad_splits(int M, int N, int K);
+hipError_t launch_shared_dW2(int dtype, const void* dY, const void* A, void* dW2, int N, int d,
+                             int h, float* part, int splits, hipStream_t st);
+hipError_t launch_shared_dW13(int dtype, const void* dH, const void* X, void* dW1, void* dW3,
+                              int N, int d, int h, float* part, int splits, hipStream_t st);
 
 // Fill n int32/fp32/bytes with zero (a kernel, not a memset node).
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);

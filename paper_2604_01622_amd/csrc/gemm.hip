@@ -25,11 +25,12 @@ namespace ec {
 
 namespace {
 
-enum { EPI_STORE = 0, EPI_SWIGLU = 1, EPI_SWIGLU_BWD = 2 };
+enum { EPI_STORE = 0, EPI_SWIGLU = 1, EPI_SWIGLU_BWD = 2, EPI_STORE_ADD = 3 };
 
 // Stage tags: every product gets its own kernel symbol, so that traces and
 // counters attribute each launch to its stage.
-enum { G_W13 = 1, G_W2, G_DA, G_DXE, G_DW2, G_DW13, G_ROUTER_DX, G_ROUTER_DWG };
+enum { G_W13 = 1, G_W2, G_DA, G_DXE, G_DW2, G_DW13, G_ROUTER_DX, G_ROUTER_DWG,
+       G_SH_W13, G_SH_W2, G_SH_DA, G_SH_DXE, G_SH_DW2, G_SH_DW13 };
 
 struct GemmParams {
   // A operand, element (m, k) of batch e:
@@ -383,7 +384,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
     const int mbase = m0 + wm * WM + mi * 32;
-    if constexpr (EPI == EPI_STORE) {
+    if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_ADD) {
       constexpr int CPR = WN / 8;
 #pragma unroll
       for (int q = 0; q < (32 * CPR) / 64; ++q) {
@@ -399,8 +400,25 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
           const bool second = m >= p.c_split;
           const int mm = second ? m - p.c_split : m;
           const size_t off = (size_t)e * p.c_bs + (size_t)mm * p.ldc + n;
-          if constexpr (OUT_F32) Elem<float>::store8((float*)(second ? p.C2 : p.C) + off, vv);
-          else Elem<bf16_t>::store8((bf16_t*)(second ? p.C2 : p.C) + off, vv);
+          if constexpr (OUT_F32) {
+            float* dst = (float*)(second ? p.C2 : p.C) + off;
+            if constexpr (EPI == EPI_STORE_ADD) {
+              float old[8];
+              Elem<float>::load8(dst, old);
+#pragma unroll
+              for (int u = 0; u < 8; ++u) vv[u] += old[u];
+            }
+            Elem<float>::store8(dst, vv);
+          } else {
+            bf16_t* dst = (bf16_t*)(second ? p.C2 : p.C) + off;
+            if constexpr (EPI == EPI_STORE_ADD) {
+              float old[8];
+              Elem<bf16_t>::load8(dst, old);
+#pragma unroll
+              for (int u = 0; u < 8; ++u) vv[u] += old[u];
+            }
+            Elem<bf16_t>::store8(dst, vv);
+          }
         }
       }
     } else if constexpr (EPI == EPI_SWIGLU) {
@@ -555,10 +573,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p, int a_kc, i
     for (int jj = 0; jj < 4; ++jj) {
       const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + jj;
       if (m >= p.M || n >= p.N) continue;
-      if (EPI == EPI_STORE) {
+      if (EPI == EPI_STORE || EPI == EPI_STORE_ADD) {
         const bool second = m >= p.c_split;
         const int mm = second ? m - p.c_split : m;
-        ((float*)(second ? p.C2 : p.C))[(size_t)e * p.c_bs + (size_t)mm * p.ldc + n] = acc[i][jj];
+        float* dst = (float*)(second ? p.C2 : p.C) + (size_t)e * p.c_bs + (size_t)mm * p.ldc + n;
+        *dst = (EPI == EPI_STORE_ADD) ? *dst + acc[i][jj] : acc[i][jj];
       } else if (EPI == EPI_SWIGLU) {
         const float h1 = acc[i][jj], h3 = acc3[i][jj];
         ((float*)p.C)[(size_t)e * p.c_bs + (size_t)m * p.ldc + n] = silu_f(h1) * h3;
@@ -606,12 +625,27 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ part, float* __re
   (void)rows_in;
 }
 
+// deterministic split-K reduction into the storage dtype, with the output's
+// row split: row r < c_split goes to C, the others to C2 at r - c_split.
+template <typename T>
+__global__ void splitk_store_kernel(const float* __restrict__ part, int splits, int M, int N,
+                                    int c_split, T* __restrict__ C, T* __restrict__ C2, int ldc) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long)M * N) return;
+  const int r = (int)(i / N), c = (int)(i % N);
+  float s = 0.f;
+  for (int q = 0; q < splits; ++q) s += part[(size_t)q * M * N + i];
+  if (r < c_split) Elem<T>::store1(C + (size_t)r * ldc + c, s);
+  else Elem<T>::store1(C2 + (size_t)(r - c_split) * ldc + c, s);
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
 
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
-                           void* H1, void* H3, int E, int M, int d, int h, hipStream_t st) {
+                           void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
+                           bool shared) {
   GemmParams p = base_params();
   p.A = Xe; p.a_bs = (long)M * d; p.lda = d;
   p.B = W1; p.B2 = W3; p.b_bs = (long)h * d; p.ldb = d;
@@ -620,11 +654,12 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
   p.H1 = H1; p.H3 = H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU>(p, 1, 1, st);
+  if (shared) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13>(p, st);
   return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
 }
 
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
-                          int h, hipStream_t st) {
+                          int h, hipStream_t st, bool shared) {
   GemmParams p = base_params();
   p.A = A; p.a_bs = (long)M * h; p.lda = h;
   p.B = W2; p.b_bs = (long)d * h; p.ldb = h;
@@ -632,11 +667,13 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
   p.C = O; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
+  if (shared) return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
 }
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
-                          const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st) {
+                          const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
+                          bool shared) {
   // dA[m, n] = sum_k dO[m, k] W2[k, n]  (k over d, n over h); epilogue -> dH1, dH3
   GemmParams p = base_params();
   p.A = dO; p.a_bs = (long)M * d; p.lda = d;
@@ -647,11 +684,13 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
   p.H1 = (void*)H1; p.H3 = (void*)H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
+  if (shared)
+    return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_DA>(p, st);
 }
 
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
-                           int E, int M, int d, int h, hipStream_t st) {
+                           int E, int M, int d, int h, hipStream_t st, bool shared) {
   // dXe[m, n] = sum_k dH[m, k] W13[k, n], k < h from W1, k >= h from W3
   GemmParams p = base_params();
   p.A = dH; p.a_bs = (long)M * 2 * h; p.lda = 2 * h;
@@ -659,6 +698,11 @@ hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void
   p.M = M; p.N = d; p.K = 2 * h; p.kv_a = 2 * h; p.kv_b = 2 * h; p.batches = E;
   p.C = dXe; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
+  // the shared experts' input gradient is added to dX
+  if (shared) {
+    if (dtype == DT_F32) return run_f32<EPI_STORE_ADD>(p, 1, 0, st);
+    return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
+  }
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 0, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE, false, G_DXE>(p, st);
 }
@@ -748,6 +792,76 @@ hipError_t launch_router_dwg(int dtype, const void* dZ, const void* X, float* dW
   const long n = (long)E * d;
   splitk_reduce_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(part, dWg, splits, n, E, E, d);
   return hipGetLastError();
+}
+
+int wgrad_splits(int M, int N, int K) {
+  const int tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  int s = (512 + tiles - 1) / tiles;
+  const int maxs = (K + 255) / 256;
+  if (s > maxs) s = maxs;
+  return s < 1 ? 1 : s;
+}
+
+namespace {
+
+// C[m, n] = sum_k A[k, m] B[k, n] over K rows (both operands K-major), split
+// over the rows into `splits` fp32 partials (part [splits, M, N]) added in a
+// fixed order into C (rows < c_split) and C2 (the others).  One batch only.
+template <int TAG>
+hipError_t run_wgrad_splitk(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
+                            void* C, void* C2, int c_split, int ldc, float* part, int splits,
+                            hipStream_t st) {
+  if (K == 0 || splits < 1) {
+    // no rows: the gradient is zero
+    hipError_t e = launch_zero(C, (size_t)(c_split < M ? c_split : M) * ldc * 2, st);
+    if (e != hipSuccess || c_split >= M) return e;
+    return launch_zero(C2, (size_t)(M - c_split) * ldc * 2, st);
+  }
+  const int chunk = ((K + splits - 1) / splits + 63) / 64 * 64;
+  const int full = K / chunk;                 // splits with chunk rows
+  const int last = K - full * chunk;          // rows of the final short split (may be 0)
+  const int nsplit = full + (last > 0 ? 1 : 0);
+  GemmParams p = base_params();
+  p.A = A; p.a_bs = (long)chunk * lda; p.lda = lda;
+  p.B = B; p.b_bs = (long)chunk * ldb; p.ldb = ldb;
+  p.M = M; p.N = N; p.K = chunk; p.kv_a = chunk; p.kv_b = chunk;
+  p.C = part; p.c_bs = (long)M * N; p.ldc = N;
+  hipError_t err = hipSuccess;
+  if (full > 0) {
+    p.batches = full;
+    err = run_dma<256, 256, 4, 2, 64, 2, false, false, EPI_STORE, true, TAG>(p, st);
+    if (err != hipSuccess) return err;
+  }
+  if (last > 0) {
+    GemmParams q = p;
+    q.A = (const bf16_t*)A + (size_t)full * chunk * lda;
+    q.B = (const bf16_t*)B + (size_t)full * chunk * ldb;
+    q.C = part + (size_t)full * M * N;
+    q.K = last; q.kv_a = last; q.kv_b = last; q.batches = 1;
+    err = run_dma<256, 256, 4, 2, 64, 2, false, false, EPI_STORE, true, TAG>(q, st);
+    if (err != hipSuccess) return err;
+  }
+  const long n = (long)M * N;
+  splitk_store_kernel<bf16_t><<<(unsigned)((n + 255) / 256), 256, 0, st>>>(
+      part, nsplit, M, N, c_split, (bf16_t*)C, (bf16_t*)C2, ldc);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_shared_dW2(int dtype, const void* dY, const void* A, void* dW2, int N, int d,
+                             int h, float* part, int splits, hipStream_t st) {
+  // dW2[m, n] = sum_i dY[i, m] A[i, n]  (m over d, n over h, i over all N tokens)
+  if (dtype == DT_F32) return launch_gemm_dW2(dtype, dY, A, dW2, 1, N, d, h, st);
+  return run_wgrad_splitk<G_SH_DW2>(dY, d, A, h, d, h, N, dW2, dW2, 1 << 30, h, part, splits, st);
+}
+
+hipError_t launch_shared_dW13(int dtype, const void* dH, const void* X, void* dW1, void* dW3,
+                              int N, int d, int h, float* part, int splits, hipStream_t st) {
+  // [dW1; dW3][m, n] = sum_i dH[i, m] X[i, n]  (m over 2h, n over d)
+  if (dtype == DT_F32) return launch_gemm_dW13(dtype, dH, X, dW1, dW3, 1, N, d, h, st);
+  return run_wgrad_splitk<G_SH_DW13>(dH, 2 * h, X, d, 2 * h, d, N, dW1, dW3, h, d, part, splits,
+                                     st);
 }
 
 }  // namespace ec

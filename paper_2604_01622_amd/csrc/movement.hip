@@ -313,12 +313,14 @@ hipError_t launch_gather(int dtype, const void* X, const int32_t* sel_token, voi
   return hipGetLastError();
 }
 
-hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_t* slotT, void* Y,
-                          int N, int E, int K, int d, hipStream_t st) {
+hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_t* slotT,
+                          const void* Xr, void* Y, int N, int E, int K, int d, hipStream_t st) {
   if (N == 0) return hipSuccess;
   if (dtype == DT_F32)
-    return run_combine<float>((const float*)O, S, slotT, nullptr, (float*)Y, N, E, K, d, st);
-  return run_combine<bf16_t>((const bf16_t*)O, S, slotT, nullptr, (bf16_t*)Y, N, E, K, d, st);
+    return run_combine<float>((const float*)O, S, slotT, (const float*)Xr, (float*)Y, N, E, K, d,
+                              st);
+  return run_combine<bf16_t>((const bf16_t*)O, S, slotT, (const bf16_t*)Xr, (bf16_t*)Y, N, E, K,
+                             d, st);
 }
 
 hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, const void* Xr,

@@ -62,6 +62,9 @@ def _route(P, X=FAKE, ws_bytes=1 << 30):
     (dict(n_experts=0), EC_ERR_SHAPE),
     (dict(n_experts=257), EC_ERR_SHAPE),
     (dict(inv_temperature=0.0), EC_ERR_ARG),
+    (dict(d_shared=32), EC_ERR_SHAPE),
+    (dict(d_shared=96), EC_ERR_SHAPE),
+    (dict(d_shared=-64), EC_ERR_SHAPE),
     (dict(inv_temperature=float("nan")), EC_ERR_ARG),
 ])
 def test_invalid_problems_rejected(kw, status):
@@ -82,13 +85,20 @@ def test_bad_dtype_and_pointers():
     assert _route(P, ws_bytes=16) == EC_ERR_WORKSPACE
     L = ec.lib()
     # forward: saved buffer too small, workspace too small
-    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 1 << 40, None)
+    NS = (None, None, None)          # no shared experts
+    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, *NS, FAKE, FAKE, 64, FAKE, 1 << 40,
+                          None)
     assert st == EC_ERR_WORKSPACE
-    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, FAKE, 64, None)
+    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, *NS, FAKE, None, 0, FAKE, 64, None)
     assert st == EC_ERR_WORKSPACE
+    # shared experts declared but their weights missing
+    Ps = _problem(d_shared=128)
+    st = L.ec_moe_forward(Ps.ref, FAKE, FAKE, FAKE, FAKE, FAKE, *NS, FAKE, None, 0, FAKE, 1 << 40,
+                          None)
+    assert st == EC_ERR_ARG
     # backward needs the saved buffer
-    st = L.ec_moe_backward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, FAKE, FAKE, FAKE,
-                           FAKE, FAKE, FAKE, 1 << 40, None)
+    st = L.ec_moe_backward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, *NS, FAKE, None, 0, FAKE, FAKE,
+                           FAKE, FAKE, FAKE, *NS, FAKE, 1 << 40, None)
     assert st == EC_ERR_ARG
     assert L.ec_workspace_size(P.ref, 9) == 0
 
@@ -117,6 +127,13 @@ def test_workspace_and_saved_layout():
     assert lay["total"] - lay["O"] >= E * K * d * 2
     for mode in (0, 1, 2):
         assert P.workspace_size(mode) > 0
+    assert lay["Hs1"] == lay["Hs3"] == lay["As"] == lay["total"]    # no shared experts
+    Ps = _problem(d_shared=192)
+    ls = Ps.saved_layout()
+    assert [ls[k] for k in order[:8]] == offs[:8]
+    assert ls["Hs3"] - ls["Hs1"] >= N * 192 * 2 and ls["As"] - ls["Hs3"] >= N * 192 * 2
+    assert ls["total"] - ls["As"] >= N * 192 * 2
+    assert Ps.workspace_size(1) > P.workspace_size(1) and Ps.workspace_size(2) > P.workspace_size(2)
 
 
 @pytest.mark.parametrize("sched", list(binding.SCHEDULERS))

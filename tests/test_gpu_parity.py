@@ -83,17 +83,24 @@ def check_route(inp, caps, inv_tau, S_rows=None):
     return S_h, sel_h
 
 
+GRADS = ("dX", "dWg", "dW1", "dW3", "dW2")
+SHARED_GRADS = ("dWs1", "dWs3", "dWs2")
+
+
 def run_layer(inp, caps, inv_tau, backward=False):
     wl = inp.wl
     X, Wg, W1, W3, W2 = (dev(a) for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2))
-    Y, saved = ec.forward(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, save=True)
+    shared = None if inp.shared is None else tuple(dev(w) for w in inp.shared)
+    Y, saved = ec.forward(X, Wg, W1, W3, W2, wl.group_offsets, caps, inv_tau, save=True,
+                          shared=shared)
     out = {"Y": host(Y), "saved": saved}
     if backward:
-        g = ec.backward(X, Wg, W1, W3, W2, dev(inp.dY), saved, wl.group_offsets, caps, inv_tau)
-        for n, t in zip(("dX", "dWg", "dW1", "dW3", "dW2"), g):
+        g = ec.backward(X, Wg, W1, W3, W2, dev(inp.dY), saved, wl.group_offsets, caps, inv_tau,
+                        shared=shared)
+        for n, t in zip(GRADS + (SHARED_GRADS if shared else ()), g):
             out[n] = host(t)
     torch.cuda.synchronize()
-    P = ec.Problem.of(X, Wg, wl.d_ff, wl.group_offsets, caps, inv_tau)
+    P = ec.Problem.of(X, Wg, wl.d_ff, wl.group_offsets, caps, inv_tau, shared)
     out["views"] = {k: v for k, v in ec.saved_views(saved, P).items()}
     return out
 
@@ -111,14 +118,16 @@ def full_case(wl, inv_tau=None, backward=None, inp=None):
     assert np.array_equal(out["views"]["S"].cpu().numpy(), S_h)
     tol = out_tol(wl.dtype)
     args = (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2)
+    sh = inp.shared
     if not backward:
-        Y_ref = ref.forward_ref(*args, wl.group_offsets, caps, inv_tau, sel_token=sel)["Y"]
+        Y_ref = ref.forward_ref(*args, wl.group_offsets, caps, inv_tau, sel_token=sel,
+                                shared=sh)["Y"]
         assert rel_l2(out["Y"], Y_ref) <= tol, rel_l2(out["Y"], Y_ref)
         return out
-    g = ref.backward_ref(*args, inp.dY, wl.group_offsets, caps, inv_tau, sel_token=sel)
-    Y_ref = ref.forward_ref(*args, wl.group_offsets, caps, inv_tau, sel_token=sel)["Y"]
+    g = ref.backward_ref(*args, inp.dY, wl.group_offsets, caps, inv_tau, sel_token=sel, shared=sh)
+    Y_ref = ref.forward_ref(*args, wl.group_offsets, caps, inv_tau, sel_token=sel, shared=sh)["Y"]
     errs = {"Y": rel_l2(out["Y"], Y_ref)}
-    for n in ("dX", "dWg", "dW1", "dW3", "dW2"):
+    for n in GRADS + (SHARED_GRADS if sh is not None else ()):
         errs[n] = rel_l2(out[n], g[n])
     print("[errs]", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
     assert all(v <= tol for v in errs.values()), errs
@@ -281,5 +290,52 @@ def test_full_train_bf16():
         errs[f"dW3[{j}]"] = rel_l2(out["dW3"][j], g3)
         errs[f"dW2[{j}]"] = rel_l2(out["dW2"][j], g2)
     errs["dWg"] = rel_l2(out["dWg"], ref.router_grad_ref(*args, 1.0))
+    print("[errs]", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    assert all(v <= 2e-2 for v in errs.values()), errs
+
+
+# ------------------------------------------------------------------ shared experts
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_shared_experts_forward_backward(dtype):
+    # 777 tokens: the shared weight gradients' split over the tokens ends in a short split
+    wl = synth.small("shared", [500, 277], 128, 8, 192, dtype=dtype, seed=40, c_min=1.0,
+                     c_max=3.0, backward=True, d_shared=256)
+    full_case(wl)
+
+
+def test_shared_experts_without_routed_capacity():
+    # no routed expert takes any token: the layer is the shared SwiGLU alone
+    wl = synth.small("shared0", [200, 56], 64, 4, 64, seed=41, capacity_factor=0.0,
+                     backward=True, d_shared=128)
+    out = full_case(wl)
+    assert np.all(out["dW1"] == 0) and np.all(out["dW2"] == 0)
+
+
+def test_full_train_shared_bf16():
+    wl = synth.TRAIN_SHARED_BF16
+    print(f"[case] {wl.name} backward", flush=True)
+    inp = synth.draw(wl, with_dy=True)
+    caps = caps_for(wl, inp)
+    rng = np.random.default_rng(5)
+    rows = np.sort(rng.choice(wl.n_tokens, size=256, replace=False))
+    S_h, sel = check_route(inp, caps, 1.0, S_rows=rows)
+    out = run_layer(inp, caps, 1.0, backward=True)
+    sh = inp.shared
+    args = (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2)
+    yrows = np.sort(rng.choice(wl.n_tokens, size=16, replace=False))
+    errs = {"Y": rel_l2(out["Y"][yrows],
+                        ref.forward_rows_ref(*args, sel, yrows, 1.0, shared=sh))}
+    xrows = np.sort(rng.choice(wl.n_tokens, size=8, replace=False))
+    errs["dX"] = rel_l2(out["dX"][xrows],
+                        ref.backward_rows_ref(*args, inp.dY, sel, xrows, 1.0, shared=sh))
+    g1, g3, g2 = ref.expert_grads_ref(*args, inp.dY, sel, 3, 1.0)
+    errs["dW1[3]"], errs["dW3[3]"], errs["dW2[3]"] = (
+        rel_l2(out["dW1"][3], g1), rel_l2(out["dW3"][3], g3), rel_l2(out["dW2"][3], g2))
+    units = np.sort(rng.choice(wl.d_shared, size=4, replace=False))
+    s1, s3, s2 = ref.shared_grads_units_ref(inp.X, sh, inp.dY, units)
+    errs["dWs1"] = rel_l2(out["dWs1"][units], s1)
+    errs["dWs3"] = rel_l2(out["dWs3"][units], s3)
+    errs["dWs2"] = rel_l2(out["dWs2"][:, units], s2)
     print("[errs]", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
     assert all(v <= 2e-2 for v in errs.values()), errs
