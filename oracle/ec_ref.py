@@ -263,6 +263,67 @@ def dense_loop_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 
 
 
 # ---------------------------------------------------------------------------
+# Token choice (Section 2.2, the comparison policy): each token takes the
+# top_k experts of its row of S (equal scores: lower expert index first) with
+# gates normalised over those k experts; expert j keeps at most capacity[g] of
+# the tokens of group g that chose it, the lowest token indices first, and the
+# other pairs are dropped (their gate weight is lost, not renormalised).
+# ---------------------------------------------------------------------------
+
+def tc_capacity_ref(group_lengths, n_experts: int, top_k: int, cf: float):
+    """Tokens each expert may keep from group g: ceil(CF k L_g / E), at most L_g;
+    CF <= 0 means no cap (dropless)."""
+    L = np.asarray(group_lengths, dtype=np.int64)
+    if cf <= 0:
+        return L.copy()
+    return np.minimum(L, np.ceil(cf * top_k * L / n_experts - 1e-9).astype(np.int64))
+
+
+def tc_select_ref(S, group_offsets, top_k: int, capacity):
+    """Returns choice [N, top_k] (expert ids, descending score), gate [N, top_k]
+    (normalised over the row's choice), kept [N, top_k] (bool) and rows, a list
+    over experts of the kept tokens of each expert in ascending order."""
+    S = np.asarray(S, dtype=np.float64)
+    N, E = S.shape
+    off = np.asarray(group_offsets, dtype=np.int64)
+    choice = np.empty((N, top_k), dtype=np.int64)
+    for i in range(N):
+        order = np.lexsort((np.arange(E), -S[i]))     # score descending, index ascending
+        choice[i] = order[:top_k]
+    picked = np.take_along_axis(S, choice, 1)
+    gate = picked / picked.sum(axis=1, keepdims=True)
+    kept = np.zeros((N, top_k), dtype=bool)
+    rows = [[] for _ in range(E)]
+    for g in range(len(off) - 1):
+        used = np.zeros(E, dtype=np.int64)
+        for i in range(int(off[g]), int(off[g + 1])):
+            for r in range(top_k):
+                j = int(choice[i, r])
+                if used[j] < capacity[g]:
+                    used[j] += 1
+                    kept[i, r] = True
+                    rows[j].append(i)
+    return choice, gate, kept, [np.asarray(r, dtype=np.int64) for r in rows]
+
+
+def tc_forward_ref(X, Wg, W1, W3, W2, group_offsets, top_k: int, capacity,
+                   inv_tau: float = 1.0) -> dict:
+    """y_i = sum over the kept pairs (i, j) of g_ij FFN_j(x_i)."""
+    Xf = widen(X)
+    S = router_ref(X, Wg, inv_tau)
+    choice, gate, kept, rows = tc_select_ref(S, group_offsets, top_k, capacity)
+    N, E = S.shape
+    G = np.zeros((N, E))
+    for r in range(top_k):
+        G[np.arange(N), choice[:, r]] += np.where(kept[:, r], gate[:, r], 0.0)
+    Y = np.zeros_like(Xf)
+    for j in range(E):
+        if len(rows[j]):
+            Y[rows[j]] += G[rows[j], j][:, None] * swiglu_ffn_ref(Xf[rows[j]], W1[j], W3[j], W2[j])
+    return {"S": S, "choice": choice, "gate": gate, "kept": kept, "rows": rows, "G": G, "Y": Y}
+
+
+# ---------------------------------------------------------------------------
 # Shared experts (Appendix D: they process every token whatever the routing;
 # Appendix E: 2 per MoE layer).  n_s shared SwiGLU experts of width h_s are one
 # SwiGLU of width n_s h_s whose hidden units are theirs side by side

@@ -440,6 +440,69 @@ def test_shared_restricted_forms_equal_full_definitions():
     assert np.max(np.abs(g2 - full["dWs2"][:, units])) < 1e-12
 
 
+# --------------------------------------------------------------------- token choice
+
+@pytest.mark.parametrize("seed", range(6))
+def test_tc_choice_equals_rank_definition(seed):
+    # j is among token i's experts iff fewer than k experts rank above it
+    # (higher score, or equal score and lower index)
+    rng = np.random.default_rng(400 + seed)
+    N, E = 9, int(rng.integers(1, 7))
+    k = int(rng.integers(1, E + 1))
+    S = rng.integers(0, 3, size=(N, E)).astype(np.float64) / 3 + 0.1      # many ties
+    choice, gate, kept, rows = ref.tc_select_ref(S, [0, N], k, [N])
+    for i in range(N):
+        want = {j for j in range(E)
+                if sum(S[i, q] > S[i, j] or (S[i, q] == S[i, j] and q < j) for q in range(E)) < k}
+        assert set(choice[i].tolist()) == want
+        assert abs(gate[i].sum() - 1.0) < 1e-12
+    assert kept.all()                                     # capacity N: nothing dropped
+
+
+def test_tc_capacity_keeps_lowest_indices():
+    rng = np.random.default_rng(7)
+    lens = [11, 7]
+    off = np.concatenate([[0], np.cumsum(lens)])
+    S = ref.softmax_ref(rng.standard_normal((18, 4)))
+    cap = [2, 3]
+    choice, gate, kept, rows = ref.tc_select_ref(S, off, 2, cap)
+    for j in range(4):
+        for g in range(2):
+            lo, hi = off[g], off[g + 1]
+            demand = [i for i in range(lo, hi) if j in choice[i]]
+            got = [i for i in rows[j] if lo <= i < hi]
+            assert got == demand[:cap[g]]                 # first come, first kept
+    assert kept.sum() == sum(len(r) for r in rows)
+
+
+def test_tc_all_experts_no_cap_is_dense_soft_mixture():
+    # k = E, no cap: gates are the softmax itself, the same layer as EC with k = L
+    inp = _tiny_inputs([10, 6], 8, 4, 8, seed=42)
+    off = inp.wl.group_offsets
+    tc = ref.tc_forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, 4, [10, 6])
+    ec_ = ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, [10, 6])
+    assert np.max(np.abs(tc["Y"] - ec_["Y"])) < 1e-12
+
+
+def test_tc_top1_is_argmax_expert():
+    inp = _tiny_inputs([12], 8, 5, 8, seed=43)
+    tc = ref.tc_forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, [0, 12], 1, [12])
+    x = torch.from_numpy(ref.widen(inp.X))
+    S = ref.router_ref(inp.X, inp.Wg)
+    for i in range(12):
+        j = int(np.argmax(S[i]))
+        want = _torch_swiglu_t(x[i:i + 1], *(torch.from_numpy(ref.widen(w[j]))
+                                            for w in (inp.W1, inp.W3, inp.W2)))
+        assert np.max(np.abs(tc["Y"][i] - want.numpy()[0])) < 1e-12
+
+
+def test_tc_capacity_rule():
+    assert list(ref.tc_capacity_ref([2048, 100], 64, 8, 1.0)) == [256, 13]   # ceil(8 L / 64)
+    assert list(ref.tc_capacity_ref([2048], 64, 8, 1.25)) == [320]
+    assert list(ref.tc_capacity_ref([30], 4, 2, 0.0)) == [30]                # dropless
+    assert list(ref.tc_capacity_ref([10], 2, 2, 2.0)) == [10]                # at most L
+
+
 # --------------------------------------------------------------------- mutation tests
 
 def test_pins_catch_planted_mistakes(monkeypatch):
