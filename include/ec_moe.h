@@ -192,6 +192,43 @@ int ec_moe_backward(const ec_problem *p, const void *X, const void *Wg,
                     void *dWs1, void *dWs3, void *dWs2,
                     void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- Token choice (Section 2.2), the policy expert choice is compared with,
+ * on the same kernels.  Every token takes the top_k experts of its row of S
+ * (equal scores: the lower expert index) with gates normalised over those k
+ * experts, g_ij = S_ij / sum of the k chosen S_ij'; expert j keeps at most
+ * p->capacity[g] of the tokens of group g that chose it, the lowest token
+ * indices first; the other pairs are dropped (their gate weight is lost, not
+ * renormalised).  Per-expert loads are data dependent: the kept pairs are
+ * packed expert after expert, expert j's rows being
+ * [expert_rows[j], expert_rows[j+1]), tokens ascending within each group.    */
+
+/* TC capacity: cap_g = min(L_g, ceil(cf * top_k * L_g / E)); cf <= 0: no cap
+ * (dropless, cap_g = L_g).  HOST arrays of length G.  Returns ec_status.      */
+int ec_tc_capacity(int32_t n_groups, const int32_t *group_lengths, int32_t n_experts,
+                   int32_t top_k, double cf, int32_t *cap_out);
+
+/* Workspace bytes of ec_tc_route (mode 0) or ec_tc_forward (mode 1); 0 on an
+ * invalid problem.                                                            */
+size_t ec_tc_workspace_size(const ec_problem *p, int32_t top_k, int mode);
+
+/* Token-choice routing: S [N, E] fp32 out; G [N, E] fp32 out, the gate of every
+ * kept pair (0 for unchosen or dropped pairs); slot [E, N] int32 out, the
+ * packed row of pair (j, i) or -1; expert_rows [E+1] int32 out;
+ * sel_token [min(top_k N, E sum_g cap_g)] int32 out, the token of each packed
+ * row (the first expert_rows[E] entries are written).  1 <= top_k <= E.      */
+int ec_tc_route(const ec_problem *p, int32_t top_k, const void *X, const void *Wg,
+                float *S, float *G, int32_t *slot, int32_t *expert_rows,
+                int32_t *sel_token, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Token-choice layer forward (inference): y_i = sum over kept pairs of
+ * g_ij FFN_j(x_i), plus the shared experts when p->d_shared > 0.  Weights as
+ * for ec_moe_forward; expert_rows [E+1] int32 out, may be NULL.  The stage
+ * events of ec_set_stage_events are those of ec_moe_forward.                */
+int ec_tc_forward(const ec_problem *p, int32_t top_k, const void *X, const void *Wg,
+                  const void *W1, const void *W3, const void *W2,
+                  const void *Ws1, const void *Ws3, const void *Ws2, void *Y,
+                  int32_t *expert_rows, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Stage timing for profiling.  After this call, every entry point called on
  * the same thread records events[0] on its stream before its first kernel and
  * events[s+1] after stage s, for s < n_events - 1, so that

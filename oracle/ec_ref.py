@@ -307,11 +307,20 @@ def tc_select_ref(S, group_offsets, top_k: int, capacity):
 
 
 def tc_forward_ref(X, Wg, W1, W3, W2, group_offsets, top_k: int, capacity,
-                   inv_tau: float = 1.0) -> dict:
-    """y_i = sum over the kept pairs (i, j) of g_ij FFN_j(x_i)."""
+                   inv_tau: float = 1.0, selection=None) -> dict:
+    """y_i = sum over the kept pairs (i, j) of g_ij FFN_j(x_i).  selection =
+    (choice, kept) replaces the selection (another implementation's, made on its
+    own scores); the gates are then the normalised scores of that choice."""
     Xf = widen(X)
     S = router_ref(X, Wg, inv_tau)
-    choice, gate, kept, rows = tc_select_ref(S, group_offsets, top_k, capacity)
+    if selection is None:
+        choice, gate, kept, rows = tc_select_ref(S, group_offsets, top_k, capacity)
+    else:
+        choice, kept = (np.asarray(a) for a in selection)
+        picked = np.take_along_axis(S, choice, 1)
+        gate = picked / picked.sum(axis=1, keepdims=True)
+        rows = [np.asarray(sorted(int(i) for i, r in zip(*np.nonzero(kept)) if choice[i, r] == j),
+                           dtype=np.int64) for j in range(S.shape[1])]
     N, E = S.shape
     G = np.zeros((N, E))
     for r in range(top_k):
@@ -321,6 +330,23 @@ def tc_forward_ref(X, Wg, W1, W3, W2, group_offsets, top_k: int, capacity,
         if len(rows[j]):
             Y[rows[j]] += G[rows[j], j][:, None] * swiglu_ffn_ref(Xf[rows[j]], W1[j], W3[j], W2[j])
     return {"S": S, "choice": choice, "gate": gate, "kept": kept, "rows": rows, "G": G, "Y": Y}
+
+
+def tc_forward_rows_ref(X, Wg, W1, W3, W2, choice, kept, rows, inv_tau: float = 1.0):
+    """y_i of the token-choice layer for the listed tokens only, selection given."""
+    rows = np.asarray(rows, dtype=np.int64)
+    Xr = widen(np.asarray(X)[rows])
+    S = softmax_ref(Xr @ widen(Wg).T, inv_tau)
+    ch, kp = np.asarray(choice)[rows], np.asarray(kept)[rows]
+    picked = np.take_along_axis(S, ch, 1)
+    gate = picked / picked.sum(axis=1, keepdims=True)
+    Y = np.zeros_like(Xr)
+    for q in range(len(rows)):
+        for r in range(ch.shape[1]):
+            if kp[q, r]:
+                j = int(ch[q, r])
+                Y[q] += gate[q, r] * swiglu_ffn_ref(Xr[q:q + 1], W1[j], W3[j], W2[j])[0]
+    return Y
 
 
 # ---------------------------------------------------------------------------

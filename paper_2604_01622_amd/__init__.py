@@ -15,8 +15,11 @@ from .binding import (  # noqa: F401
     route,
     saved_views,
     token_coverage,
+    tc_capacity,
+    tc_route,
+    tc_forward,
     Layer,
 )
 
 __all__ = ["ECError", "Problem", "Layer", "route", "forward", "backward", "capacity",
-           "saved_views", "token_coverage", "lib"]
+           "saved_views", "token_coverage", "tc_capacity", "tc_route", "tc_forward", "lib"]

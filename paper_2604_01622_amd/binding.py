@@ -22,7 +22,8 @@ SCHEDULERS = {"linear": 0, "linear_rev": 1, "cosine": 2, "cosine_rev": 3, "gauss
               "gaussian_rev": 5}
 EXPORTS = ("ec_status_string", "ec_last_error", "ec_total_capacity", "ec_workspace_size",
            "ec_saved_layout_of", "ec_capacity", "ec_route", "ec_token_coverage", "ec_moe_forward",
-           "ec_moe_backward", "ec_set_stage_events")
+           "ec_moe_backward", "ec_tc_capacity", "ec_tc_workspace_size", "ec_tc_route",
+           "ec_tc_forward", "ec_set_stage_events")
 
 
 class ECError(RuntimeError):
@@ -79,6 +80,15 @@ def lib() -> ctypes.CDLL:
         L.ec_moe_forward.argtypes = [pp] + [vp] * 9 + [vp, sz, vp, sz, vp]
         L.ec_moe_backward.restype = ctypes.c_int
         L.ec_moe_backward.argtypes = [pp] + [vp] * 9 + [vp, sz] + [vp] * 8 + [vp, sz, vp]
+        L.ec_tc_capacity.restype = ctypes.c_int
+        L.ec_tc_capacity.argtypes = [ctypes.c_int32, i32p, ctypes.c_int32, ctypes.c_int32,
+                                     ctypes.c_double, i32p]
+        L.ec_tc_workspace_size.restype = sz
+        L.ec_tc_workspace_size.argtypes = [pp, ctypes.c_int32, ctypes.c_int]
+        L.ec_tc_route.restype = ctypes.c_int
+        L.ec_tc_route.argtypes = [pp, ctypes.c_int32] + [vp] * 8 + [sz, vp]
+        L.ec_tc_forward.restype = ctypes.c_int
+        L.ec_tc_forward.argtypes = [pp, ctypes.c_int32] + [vp] * 11 + [sz, vp]
         L.ec_set_stage_events.restype = ctypes.c_int
         L.ec_set_stage_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
         _lib = L
@@ -205,6 +215,59 @@ def token_coverage(slot: torch.Tensor, group_offsets, capacity, d_model: int = 6
     _check(lib().ec_token_coverage(P.ref, _ptr(slot) if N else None, _ptr(cnt) if N else None,
                                    _ptr(dropped), _stream()))
     return cnt, dropped
+
+
+def tc_capacity(group_lengths: Sequence[int], n_experts: int, top_k: int,
+                cf: float) -> np.ndarray:
+    """Token-choice capacity per (group, expert): min(L_g, ceil(cf k L_g / E)); cf <= 0: no cap."""
+    L = np.ascontiguousarray(np.asarray(group_lengths, dtype=np.int32))
+    out = np.empty(len(L), dtype=np.int32)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    _check(lib().ec_tc_capacity(len(L), L.ctypes.data_as(i32p), int(n_experts), int(top_k),
+                                float(cf), out.ctypes.data_as(i32p)))
+    return out
+
+
+def _tc_rmax(P: "Problem", top_k: int) -> int:
+    N, E = P.c.n_tokens, P.c.n_experts
+    return int(min(top_k * N, E * min(int(P.cap.sum()), N)))
+
+
+def tc_route(X, Wg, group_offsets, capacity, top_k: int, inv_temperature=1.0, d_ff: int = 64):
+    """Token-choice routing.  Returns S [N,E], G [N,E] (gates of kept pairs), slot [E,N]
+    (packed row or -1), expert_rows [E+1] and sel_token (token of each packed row)."""
+    P = Problem.of(X, Wg, d_ff, group_offsets, capacity, inv_temperature)
+    N, E = X.shape[0], Wg.shape[0]
+    dev = X.device
+    S = torch.empty((N, E), dtype=torch.float32, device=dev)
+    G = torch.empty((N, E), dtype=torch.float32, device=dev)
+    slot = torch.empty((E, N), dtype=torch.int32, device=dev)
+    rows = torch.empty((E + 1,), dtype=torch.int32, device=dev)
+    sel = torch.empty((max(_tc_rmax(P, top_k), 1),), dtype=torch.int32, device=dev)
+    n = lib().ec_tc_workspace_size(P.ref, int(top_k), 0)
+    if n == 0:
+        _check(2)
+    ws = _empty(n, dev)
+    _check(lib().ec_tc_route(P.ref, int(top_k), _ptr(X), _ptr(Wg), _ptr(S), _ptr(G), _ptr(slot),
+                             _ptr(rows), _ptr(sel), _ptr(ws), ws.numel(), _stream()))
+    return S, G, slot, rows, sel
+
+
+def tc_forward(X, Wg, W1, W3, W2, group_offsets, capacity, top_k: int, inv_temperature=1.0,
+               shared=None):
+    """Token-choice layer forward.  Returns Y [N,d] and expert_rows [E+1]."""
+    P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature, shared)
+    dev = X.device
+    Y = torch.empty_like(X)
+    rows = torch.empty((Wg.shape[0] + 1,), dtype=torch.int32, device=dev)
+    n = lib().ec_tc_workspace_size(P.ref, int(top_k), 1)
+    if n == 0:
+        _check(2)
+    ws = _empty(n, dev)
+    _check(lib().ec_tc_forward(P.ref, int(top_k), _ptr(X), _ptr(Wg), _ptr(W1), _ptr(W3), _ptr(W2),
+                               *_shared_ptrs(shared), _ptr(Y), _ptr(rows), _ptr(ws), ws.numel(),
+                               _stream()))
+    return Y, rows
 
 
 def _shared_ptrs(shared):

@@ -21,7 +21,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libecmoe.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["router.hip", "topk.hip", "movement.hip", "gemm.hip", "ec_api.cpp"]
+SOURCES = ["router.hip", "topk.hip", "tc.hip", "movement.hip", "gemm.hip", "ec_api.cpp"]
 
 
 def hipcc() -> str:
@@ -34,7 +34,7 @@ def hipcc() -> str:
 def flags(debug: bool):
     f = ["--offload-arch=gfx950", "-std=c++17", "-fPIC", "-O3",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-I", os.path.join(ROOT, "include"), "-Wno-unused-result"]
+         "-I", os.path.join(ROOT, "include"), "-Wno-unused-result", "-Werror=uninitialized"]
     if debug:
         f += ["-g"]
     return f

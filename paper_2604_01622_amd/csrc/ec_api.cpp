@@ -42,7 +42,9 @@ struct Plan {
   size_t esz = 0;      // storage bytes per element
 };
 
-int validate(const ec_problem* p, Plan* out) {
+// ec_buffers: check the sizes of the [E, K_tot, .] expert buffers of expert
+// choice (token choice packs its pairs and checks its own bound).
+int validate(const ec_problem* p, Plan* out, bool ec_buffers = true) {
   g_last_error.clear();
   if (!p) return fail(EC_ERR_ARG, "problem is NULL");
   if (p->dtype != EC_F32 && p->dtype != EC_BF16)
@@ -79,7 +81,7 @@ int validate(const ec_problem* p, Plan* out) {
     return fail(EC_ERR_SHAPE, "group_offsets[G] = %d != n_tokens = %lld", off[p->n_groups],
                 (long long)p->n_tokens);
   const int64_t maxw = p->d_model > p->d_ff ? p->d_model : p->d_ff;
-  if ((int64_t)p->n_experts * K * 2 * maxw >= ((int64_t)1 << 31) ||
+  if ((ec_buffers && (int64_t)p->n_experts * K * 2 * maxw >= ((int64_t)1 << 31)) ||
       (int64_t)p->n_experts * p->n_tokens >= ((int64_t)1 << 31) ||
       p->n_tokens * 2 * (int64_t)(p->d_shared > p->d_model ? p->d_shared : p->d_model) >=
           ((int64_t)1 << 31))
@@ -248,6 +250,100 @@ int enqueue_route(const ec_problem* p, const Plan& P, const void* X, const void*
       ++tab.n;
     }
     EC_HIP(ec::launch_topk(ST, P.N, P.E, (int)P.K, tab, sel, gate, slot, st));
+  }
+  EC_HIP(mark(2, st));
+  return EC_OK;
+}
+
+// ---- token choice -------------------------------------------------------------
+
+int tc_validate(const ec_problem* p, int top_k, Plan* P, long* rmax, int* rmax_e) {
+  EC_TRY(validate(p, P, false));
+  if (top_k < 1 || top_k > P->E)
+    return fail(EC_ERR_ARG, "top_k must be in [1, n_experts] (got %d)", top_k);
+  // kept pairs: at most top_k per token and sum_g cap_g per expert
+  long r = (long)top_k * P->N;
+  const long per_e = P->K < P->N ? P->K : P->N;
+  if ((long)P->E * per_e < r) r = (long)P->E * per_e;
+  const long w = P->d > P->h ? P->d : P->h;
+  if (r * w >= ((long)1 << 31))
+    return fail(EC_ERR_SHAPE, "too many token-expert pairs for 32-bit element indices");
+  *rmax = r;
+  *rmax_e = (int)per_e;
+  return EC_OK;
+}
+
+struct TcRouteWs {
+  float* ST;
+  int32_t* cnt;
+  int32_t* seg;
+  int32_t* tiles13;
+  int32_t* tiles2;
+};
+
+TcRouteWs carve_tc_route(Carve& c, const Plan& P) {
+  TcRouteWs w;
+  w.ST = (float*)c.take((size_t)P.E * P.N * 4);
+  w.cnt = (int32_t*)c.take((size_t)P.G * P.E * 4);
+  w.seg = (int32_t*)c.take((size_t)P.G * P.E * 4);
+  w.tiles13 = (int32_t*)c.take((size_t)(P.E + 1) * 4);
+  w.tiles2 = (int32_t*)c.take((size_t)(P.E + 1) * 4);
+  return w;
+}
+
+struct TcFwdWs {
+  float* S;
+  float* G;
+  int32_t* slot;
+  int32_t* rows;
+  int32_t* sel;
+  void* Xe;
+  void* A;
+  void* O;
+  void* As;
+};
+
+TcFwdWs carve_tc_fwd(Carve& c, const Plan& P, long rmax) {
+  TcFwdWs w;
+  w.S = (float*)c.take((size_t)P.N * P.E * 4);
+  w.G = (float*)c.take((size_t)P.N * P.E * 4);
+  w.slot = (int32_t*)c.take((size_t)P.E * P.N * 4);
+  w.rows = (int32_t*)c.take((size_t)(P.E + 1) * 4);
+  w.sel = (int32_t*)c.take((size_t)rmax * 4);
+  w.Xe = c.take((size_t)rmax * P.d * P.esz);
+  w.A = c.take((size_t)rmax * P.h * P.esz);
+  w.O = c.take((size_t)rmax * P.d * P.esz);
+  w.As = P.hs ? c.take((size_t)P.N * P.hs * P.esz) : nullptr;
+  return w;
+}
+
+// Router, row top-k, per-(group, expert) counts, offsets and placement.
+int enqueue_tc_route(const ec_problem* p, const Plan& P, int top_k, const void* X, const void* Wg,
+                     float* S, float* G, int32_t* slot, int32_t* rows, int32_t* sel,
+                     const TcRouteWs& w, hipStream_t st) {
+  EC_HIP(mark(0, st));
+  EC_HIP(ec::launch_router_softmax(P.dtype, X, Wg, S, w.ST, P.N, P.d, P.E, p->inv_temperature,
+                                   st));
+  EC_HIP(mark(1, st));
+  EC_HIP(ec::launch_tc_topk(S, P.N, P.E, top_k, G, slot, st));
+  ec::GroupTable tab;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int g0 = 0; g0 < P.G; g0 += ec::TOPK_MAX_GROUPS) {
+      tab.n = 0;
+      for (int g = g0; g < P.G && g < g0 + ec::TOPK_MAX_GROUPS; ++g) {
+        tab.off[tab.n] = p->group_offsets[g];
+        tab.len[tab.n] = p->group_offsets[g + 1] - p->group_offsets[g];
+        tab.k[tab.n] = p->capacity[g];
+        tab.seg[tab.n] = 0;
+        ++tab.n;
+      }
+      if (pass == 0) EC_HIP(ec::launch_tc_count(slot, P.N, P.E, tab, g0, w.cnt, st));
+      else EC_HIP(ec::launch_tc_place(slot, G, P.N, P.E, tab, g0, w.seg, sel, st));
+    }
+    if (pass == 0)
+      EC_HIP(ec::launch_tc_offsets(w.cnt, P.G, P.E, ec::TC_BM, ec::tc_col_blocks_w13(P.h),
+                                   ec::tc_col_blocks_w2(P.d), rows, w.seg, w.tiles13, w.tiles2,
+                                   st));
   }
   EC_HIP(mark(2, st));
   return EC_OK;
@@ -548,6 +644,113 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   EC_HIP(mark(12, stream));
   EC_HIP(ec::launch_router_dwg(P.dtype, dZop, X, dWg, w.part, w.splits, N, E, P.EP, d, stream));
   EC_HIP(mark(13, stream));
+  return EC_OK;
+}
+
+int ec_tc_capacity(int32_t n_groups, const int32_t* group_lengths, int32_t n_experts,
+                   int32_t top_k, double cf, int32_t* cap_out) {
+  g_last_error.clear();
+  if (n_groups < 0 || !group_lengths || !cap_out) return fail(EC_ERR_ARG, "bad arguments");
+  if (n_experts < 1 || top_k < 1 || top_k > n_experts)
+    return fail(EC_ERR_ARG, "need 1 <= top_k <= n_experts");
+  if (!std::isfinite(cf)) return fail(EC_ERR_ARG, "capacity factor must be finite");
+  for (int g = 0; g < n_groups; ++g) {
+    const int L = group_lengths[g];
+    if (L < 0) return fail(EC_ERR_SHAPE, "group length %d < 0", L);
+    double c = cf <= 0 ? (double)L : std::ceil(cf * top_k * (double)L / n_experts - 1e-9);
+    if (c > L) c = L;
+    if (c < 0) c = 0;
+    cap_out[g] = (int32_t)c;
+  }
+  return EC_OK;
+}
+
+size_t ec_tc_workspace_size(const ec_problem* p, int32_t top_k, int mode) {
+  Plan P;
+  long rmax;
+  int rmax_e;
+  if (tc_validate(p, top_k, &P, &rmax, &rmax_e) != EC_OK) return 0;
+  Carve c(nullptr);
+  carve_tc_route(c, P);
+  if (mode == 1) carve_tc_fwd(c, P, rmax);
+  else if (mode != 0) { fail(EC_ERR_ARG, "unknown workspace mode %d", mode); return 0; }
+  return c.used;
+}
+
+int ec_tc_route(const ec_problem* p, int32_t top_k, const void* X, const void* Wg, float* S,
+                float* G, int32_t* slot, int32_t* expert_rows, int32_t* sel_token, void* ws,
+                size_t ws_bytes, hipStream_t stream) {
+  Plan P;
+  long rmax;
+  int rmax_e;
+  EC_TRY(tc_validate(p, top_k, &P, &rmax, &rmax_e));
+  EC_TRY(check_ptr(X, "X"));
+  EC_TRY(check_ptr(Wg, "Wg"));
+  EC_TRY(check_ptr(S, "S", P.N == 0));
+  EC_TRY(check_ptr(G, "G", P.N == 0));
+  EC_TRY(check_ptr(slot, "slot", P.N == 0));
+  EC_TRY(check_ptr(expert_rows, "expert_rows"));
+  EC_TRY(check_ptr(sel_token, "sel_token", rmax == 0));
+  Carve m(nullptr);
+  carve_tc_route(m, P);
+  EC_TRY(check_ptr(ws, "workspace"));
+  if (ws_bytes < m.used)
+    return fail(EC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, m.used);
+  Carve c(ws);
+  const TcRouteWs w = carve_tc_route(c, P);
+  if (P.N == 0) return ec::launch_zero(expert_rows, (size_t)(P.E + 1) * 4, stream) == hipSuccess
+                           ? EC_OK : fail(EC_ERR_HIP, "zero fill failed");
+  return enqueue_tc_route(p, P, top_k, X, Wg, S, G, slot, expert_rows, sel_token, w, stream);
+}
+
+int ec_tc_forward(const ec_problem* p, int32_t top_k, const void* X, const void* Wg,
+                  const void* W1, const void* W3, const void* W2, const void* Ws1,
+                  const void* Ws3, const void* Ws2, void* Y, int32_t* expert_rows, void* ws,
+                  size_t ws_bytes, hipStream_t stream) {
+  Plan P;
+  long rmax;
+  int rmax_e;
+  EC_TRY(tc_validate(p, top_k, &P, &rmax, &rmax_e));
+  EC_TRY(check_ptr(X, "X"));
+  EC_TRY(check_ptr(Wg, "Wg"));
+  EC_TRY(check_ptr(W1, "W1"));
+  EC_TRY(check_ptr(W3, "W3"));
+  EC_TRY(check_ptr(W2, "W2"));
+  EC_TRY(check_ptr(Ws1, "Ws1", P.hs == 0));
+  EC_TRY(check_ptr(Ws3, "Ws3", P.hs == 0));
+  EC_TRY(check_ptr(Ws2, "Ws2", P.hs == 0));
+  EC_TRY(check_ptr(Y, "Y"));
+  EC_TRY(check_ptr(expert_rows, "expert_rows", true));
+  const size_t need = ec_tc_workspace_size(p, top_k, 1);
+  EC_TRY(check_ptr(ws, "workspace"));
+  if (ws_bytes < need)
+    return fail(EC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
+  if (P.N == 0) return EC_OK;
+  Carve c(ws);
+  const TcRouteWs rw = carve_tc_route(c, P);
+  const TcFwdWs w = carve_tc_fwd(c, P, rmax);
+  int32_t* rows = expert_rows ? expert_rows : w.rows;
+  EC_TRY(enqueue_tc_route(p, P, top_k, X, Wg, w.S, w.G, w.slot, rows, w.sel, rw, stream));
+  EC_HIP(ec::launch_gather(P.dtype, X, w.sel, w.Xe, rmax, P.d, P.N, stream, rows + P.E));
+  EC_HIP(mark(3, stream));
+  EC_HIP(ec::launch_gemm_w13_var(P.dtype, w.Xe, W1, W3, w.A, P.E, rows, rw.tiles13, rmax, rmax_e,
+                                 P.d, P.h, stream));
+  EC_HIP(mark(4, stream));
+  EC_HIP(ec::launch_gemm_w2_var(P.dtype, w.A, W2, w.O, P.E, rows, rw.tiles2, rmax, rmax_e, P.d,
+                                P.h, stream));
+  EC_HIP(mark(5, stream));
+  if (P.hs) {
+    EC_HIP(ec::launch_gemm_w13(P.dtype, X, Ws1, Ws3, w.As, nullptr, nullptr, 1, P.N, P.d, P.hs,
+                               stream, true));
+    EC_HIP(mark(6, stream));
+    EC_HIP(ec::launch_gemm_w2(P.dtype, w.As, Ws2, Y, 1, P.N, P.d, P.hs, stream, true));
+  } else {
+    EC_HIP(mark(6, stream));
+  }
+  EC_HIP(mark(7, stream));
+  EC_HIP(ec::launch_combine(P.dtype, w.O, w.G, w.slot, P.hs ? Y : nullptr, Y, P.N, P.E,
+                            (int)rmax, P.d, stream, 0));
+  EC_HIP(mark(8, stream));
   return EC_OK;
 }
 

@@ -28,14 +28,18 @@ hipError_t launch_router_softmax(int dtype, const void* X, const void* Wg, float
 hipError_t launch_topk(const float* ST, int N, int E, int K, const GroupTable& tab,
                        int32_t* sel_token, float* sel_gate, int32_t* slotT, hipStream_t st);
 
-// Xe[r, :] = X[sel_token[r], :] for all E*K rows.
+// Xe[r, :] = X[sel_token[r], :] for all rows (with rows_dev: for r < *rows_dev,
+// rows being an upper bound).
 hipError_t launch_gather(int dtype, const void* X, const int32_t* sel_token, void* Xe,
-                         long rows, int d, int N, hipStream_t st);
+                         long rows, int d, int N, hipStream_t st,
+                         const int32_t* rows_dev = nullptr);
 
-// Y[i, :] = Xr[i, :] (if Xr) + sum_j S[i,j] O[j, slotT[j,i], :] over experts j with
-// slotT[j,i] >= 0 (Xr may alias Y).
+// Y[i, :] = Xr[i, :] (if Xr) + sum_j S[i,j] O[j kstride + slotT[j,i], :] over experts j
+// with 0 <= slotT[j,i] < K (Xr may alias Y); kstride < 0 means K (one buffer of K
+// rows per expert), 0 means slot holds rows of one packed buffer.
 hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_t* slotT,
-                          const void* Xr, void* Y, int N, int E, int K, int d, hipStream_t st);
+                          const void* Xr, void* Y, int N, int E, int K, int d, hipStream_t st,
+                          long kstride = -1);
 
 // Backward gather: dO[j,r,:] = S[i,j] dY[i,:] and dS[i,j] = <dY[i,:], O[j,r,:]>,
 // i = sel_token[j,r]; dS [N,E] fp32 is zero for unselected pairs.
@@ -105,6 +109,36 @@ hipError_t launch_shared_dW2(int dtype, const void* dY, const void* A, void* dW2
                              int h, float* part, int splits, hipStream_t st);
 hipError_t launch_shared_dW13(int dtype, const void* dH, const void* X, void* dW1, void* dW3,
                               int N, int d, int h, float* part, int splits, hipStream_t st);
+
+// ---- token choice (the comparison policy): packed, data-dependent expert loads ----
+
+// Row block of the grouped GEMMs (the tile tables of the packed buffers count
+// ceil(M_e / TC_BM) row blocks per expert) and their column blocks.
+constexpr int TC_BM = 256;
+int tc_col_blocks_w13(int h);
+int tc_col_blocks_w2(int d);
+// G [N,E]: normalised gates of each token's top-k experts; flagT [E,N]: 1 if chosen.
+hipError_t launch_tc_topk(const float* S, int N, int E, int k, float* G, int32_t* flagT,
+                          hipStream_t st);
+// cnt[(g0+g) E + j] = min(tokens of group g that chose j, cap_g) for the table's groups.
+hipError_t launch_tc_count(const int32_t* flagT, int N, int E, const GroupTable& tab, int g0,
+                           int32_t* cnt, hipStream_t st);
+// Packed row offsets rows [E+1], per-(group, expert) row offsets seg [G,E] and the
+// tile offsets of the two grouped products (tiles13, tiles2 [E+1]).
+hipError_t launch_tc_offsets(const int32_t* cnt, int G, int E, int bm, int nt13, int nt2,
+                             int32_t* rows, int32_t* seg, int32_t* tiles13, int32_t* tiles2,
+                             hipStream_t st);
+// slotT: choice flags in, packed rows (-1: not kept) out; sel[row] = token; G zeroed
+// on dropped pairs.
+hipError_t launch_tc_place(int32_t* slotT, float* G, int N, int E, const GroupTable& tab, int g0,
+                           const int32_t* seg, int32_t* sel, hipStream_t st);
+// The forward products over packed rows: expert e owns rows [rows[e], rows[e+1]).
+hipError_t launch_gemm_w13_var(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
+                               int E, const int32_t* rows, const int32_t* tiles, long max_rows,
+                               int max_rows_per_expert, int d, int h, hipStream_t st);
+hipError_t launch_gemm_w2_var(int dtype, const void* A, const void* W2, void* O, int E,
+                              const int32_t* rows, const int32_t* tiles, long max_rows,
+                              int max_rows_per_expert, int d, int h, hipStream_t st);
 
 // Fill n int32/fp32/bytes with zero (a kernel, not a memset node).
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);

@@ -30,7 +30,7 @@ enum { EPI_STORE = 0, EPI_SWIGLU = 1, EPI_SWIGLU_BWD = 2, EPI_STORE_ADD = 3 };
 // Stage tags: every product gets its own kernel symbol, so that traces and
 // counters attribute each launch to its stage.
 enum { G_W13 = 1, G_W2, G_DA, G_DXE, G_DW2, G_DW13, G_ROUTER_DX, G_ROUTER_DWG,
-       G_SH_W13, G_SH_W2, G_SH_DA, G_SH_DXE, G_SH_DW2, G_SH_DW13 };
+       G_SH_W13, G_SH_W2, G_SH_DA, G_SH_DXE, G_SH_DW2, G_SH_DW13, G_TC_W13, G_TC_W2 };
 
 struct GemmParams {
   // A operand, element (m, k) of batch e:
@@ -60,6 +60,19 @@ struct GemmParams {
   void* H3;
   long h_bs;
   int ldh;
+  // Variable rows per batch (token choice): batch e owns rows
+  // [var_rows[e], var_rows[e+1]) of A, C and H (row strides lda, ldc, ldh) and
+  // tiles [var_tiles[e], var_tiles[e+1]) of the launch; both device arrays of
+  // batches + 1 entries, null for a uniform batch of M rows.
+  const int* var_rows;
+  const int* var_tiles;
+};
+
+// Where one output tile sits: batch, row and column block, the batch's rows,
+// and the element offsets of the batch in A, C and H.
+struct TileCoord {
+  int e, mt, nt, M;
+  size_t a_off, c_off, h_off;
 };
 
 // ------------------------------------------------------------------ bf16 MFMA, pipelined
@@ -117,7 +130,8 @@ __device__ __forceinline__ int km_swz(int k) { return (k & 3) << 2; }
 
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
           bool OUT_F32>
-__device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* smem) {
+__device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoord& tc,
+                                              char* smem) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int MB = WM / 32, NB = WN / 32;
@@ -131,22 +145,13 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
   constexpr int SLD = WN + 4;
   static_assert(EPI != EPI_SWIGLU || (NB % 2 == 0), "SwiGLU needs W1 and W3 blocks per wave");
   static_assert(EPI != EPI_SWIGLU || B_KC, "SwiGLU forward has K-contiguous weights");
-  const int per_b = p.MT * p.NT;
-  const int e = t / per_b;
-  const int rem = t - e * per_b;
-  // Tiles go in groups of GROUP_M row blocks, row block fastest inside a
-  // group: the workgroups resident on one XCD then share few A row blocks and
-  // B column blocks at a time (fewer L2 misses than a full column of row blocks).
-  constexpr int GROUP_M = 3;
-  const int grp = rem / (GROUP_M * p.NT), in_grp = rem - grp * GROUP_M * p.NT;
-  const int gm = (p.MT - grp * GROUP_M) < GROUP_M ? (p.MT - grp * GROUP_M) : GROUP_M;
-  const int mt = grp * GROUP_M + in_grp % gm, nt = in_grp / gm;
+  const int e = tc.e, mt = tc.mt, nt = tc.nt, M = tc.M;
   const int m0 = mt * BM;
   const int n0 = (EPI == EPI_SWIGLU) ? nt * (BN / 2) : nt * BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % WGM, wn = wave / WGM;
-  const bf16_t* Ab = reinterpret_cast<const bf16_t*>(p.A) + (size_t)e * p.a_bs;
+  const bf16_t* Ab = reinterpret_cast<const bf16_t*>(p.A) + tc.a_off;
   const bf16_t* Bb = reinterpret_cast<const bf16_t*>(p.B) + (size_t)e * p.b_bs;
   const bf16_t* B2b = p.B2 ? reinterpret_cast<const bf16_t*>(p.B2) + (size_t)e * p.b_bs : nullptr;
 
@@ -162,7 +167,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
     if constexpr (A_KC) {
       const int row = id / OA::CPR, lc = (id % OA::CPR) ^ kc_swz<KSTEP>(row);
       int r = m0 + row;
-      r = r < p.M ? r : p.M - 1;
+      r = r < M ? r : M - 1;
       a_src[q] = Ab + (size_t)r * p.lda + lc * 8;
     } else {
       const int row = id / OA::CPR, lc = (id % OA::CPR) ^ km_swz(row);
@@ -201,7 +206,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
         g = a_src[q] + kt * KSTEP;
       } else {
         const int k = kt * KSTEP + a_row[q];
-        g = (k < p.kv_a && a_col[q] < p.M) ? Ab + (size_t)k * p.lda + a_col[q] : g_zero_block;
+        g = (k < p.kv_a && a_col[q] < M) ? Ab + (size_t)k * p.lda + a_col[q] : g_zero_block;
       }
       dma16(g, base + (wave * OA::LOADS + q) * 1024);
     }
@@ -369,7 +374,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
       for (int q = 0; q < BWD_Q; ++q) {
         const int c = lane + q * 64;
         const int m = mb + c / BWD_CPR, n = n0 + wn * WN + (c % BWD_CPR) * 8;
-        const size_t ho = (m < p.M && n < p.N) ? (size_t)e * p.h_bs + (size_t)m * p.ldh + n : 0;
+        const size_t ho = (m < M && n < p.N) ? tc.h_off + (size_t)m * p.ldh + n : 0;
         h1raw[q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H1 + ho);
         h3raw[q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H3 + ho);
       }
@@ -392,14 +397,14 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
         const int row = c / CPR, cc = c % CPR;
         const int m = mbase + row;
         const int n = n0 + wn * WN + cc * 8;
-        if (m < p.M && n < p.N) {
+        if (m < M && n < p.N) {
           const float* v = stage_f + row * SLD + cc * 8;
           float vv[8];
 #pragma unroll
           for (int u = 0; u < 8; ++u) vv[u] = v[u];
           const bool second = m >= p.c_split;
           const int mm = second ? m - p.c_split : m;
-          const size_t off = (size_t)e * p.c_bs + (size_t)mm * p.ldc + n;
+          const size_t off = tc.c_off + (size_t)mm * p.ldc + n;
           if constexpr (OUT_F32) {
             float* dst = (float*)(second ? p.C2 : p.C) + off;
             if constexpr (EPI == EPI_STORE_ADD) {
@@ -430,7 +435,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
         const int row = c / CPR, cc = c % CPR;
         const int m = mbase + row;
         const int n = n0 + wn * HW + cc * 8;
-        if (c < 32 * CPR && m < p.M && n < p.N) {
+        if (c < 32 * CPR && m < M && n < p.N) {
           const float* v1 = stage_f + row * SLD + cc * 8;
           const float* v3 = v1 + HW;
           float a[8], h1[8], h3[8];
@@ -440,9 +445,9 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
             h3[u] = v3[u];
             a[u] = silu_f(h1[u]) * h3[u];
           }
-          Elem<bf16_t>::store8((bf16_t*)p.C + (size_t)e * p.c_bs + (size_t)m * p.ldc + n, a);
+          Elem<bf16_t>::store8((bf16_t*)p.C + tc.c_off + (size_t)m * p.ldc + n, a);
           if (p.H1) {
-            const size_t ho = (size_t)e * p.h_bs + (size_t)m * p.ldh + n;
+            const size_t ho = tc.h_off + (size_t)m * p.ldh + n;
             Elem<bf16_t>::store8((bf16_t*)p.H1 + ho, h1);
             Elem<bf16_t>::store8((bf16_t*)p.H3 + ho, h3);
           }
@@ -455,7 +460,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
         const int row = c / BWD_CPR, cc = c % BWD_CPR;
         const int m = mbase + row;
         const int n = n0 + wn * WN + cc * 8;
-        if (m < p.M && n < p.N) {
+        if (m < M && n < p.N) {
           const float* v = stage_f + row * SLD + cc * 8;
           float d1[8], d3[8];
 #pragma unroll
@@ -468,7 +473,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, int t, char* 
             d3[u] = da * h1 * sg;
             d1[u] = da * h3 * sg * (1.0f + h1 * (1.0f - sg));
           }
-          const size_t off = (size_t)e * p.c_bs + (size_t)m * p.ldc + n;
+          const size_t off = tc.c_off + (size_t)m * p.ldc + n;
           Elem<bf16_t>::store8((bf16_t*)p.C + off, d1);
           Elem<bf16_t>::store8((bf16_t*)p.C2 + off, d3);
         }
@@ -494,9 +499,51 @@ template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bo
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024)))
   char smem[dma_smem_bytes<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC>()];
-  const int t = xcd_tile_id(blockIdx.x, gridDim.x);
-  if (t >= p.batches * p.MT * p.NT) return;
-  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32>(p, t, smem);
+  TileCoord tc;
+  int rem, MT;
+  if (p.var_rows) {
+    // the tile count is known only on the device: the grid is an upper bound,
+    // and the XCD-contiguous numbering uses the actual count
+    const int total = p.var_tiles[p.batches];
+    const int per_xcd = (total + 7) >> 3;
+    const int j = blockIdx.x >> 3;
+    if (j >= per_xcd) return;
+    const int t = (blockIdx.x & 7) * per_xcd + j;
+    if (t >= total) return;
+    int lo = 0, hi = p.batches;          // var_tiles[lo] <= t < var_tiles[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (p.var_tiles[mid] <= t) lo = mid; else hi = mid;
+    }
+    const int row0 = p.var_rows[lo];
+    tc.e = lo;
+    tc.M = p.var_rows[lo + 1] - row0;
+    MT = (tc.M + BM - 1) / BM;
+    rem = t - p.var_tiles[lo];
+    tc.a_off = (size_t)row0 * p.lda;
+    tc.c_off = (size_t)row0 * p.ldc;
+    tc.h_off = (size_t)row0 * p.ldh;
+  } else {
+    const int t = xcd_tile_id(blockIdx.x, gridDim.x);
+    if (t >= p.batches * p.MT * p.NT) return;
+    const int per_b = p.MT * p.NT;
+    tc.e = t / per_b;
+    tc.M = p.M;
+    MT = p.MT;
+    rem = t - tc.e * per_b;
+    tc.a_off = (size_t)tc.e * p.a_bs;
+    tc.c_off = (size_t)tc.e * p.c_bs;
+    tc.h_off = (size_t)tc.e * p.h_bs;
+  }
+  // Tiles go in groups of GROUP_M row blocks, row block fastest inside a
+  // group: the workgroups resident on one XCD then share few A row blocks and
+  // B column blocks at a time (fewer L2 misses than a full column of row blocks).
+  constexpr int GROUP_M = 3;
+  const int grp = rem / (GROUP_M * p.NT), in_grp = rem - grp * GROUP_M * p.NT;
+  const int gm = (MT - grp * GROUP_M) < GROUP_M ? (MT - grp * GROUP_M) : GROUP_M;
+  tc.mt = grp * GROUP_M + in_grp % gm;
+  tc.nt = in_grp / gm;
+  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32>(p, tc, smem);
 }
 
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
@@ -506,6 +553,21 @@ hipError_t run_dma(GemmParams p, hipStream_t st) {
   p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
   const long ntile = (long)p.batches * p.MT * p.NT;
   if (ntile == 0) return hipSuccess;
+  const long grid = (ntile + 7) / 8 * 8;
+  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG>
+      <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
+  return hipGetLastError();
+}
+
+// Variable rows per batch (p.var_rows / p.var_tiles on the device): the grid
+// covers max_rows rows in total plus one partial row block per batch.
+template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
+          bool OUT_F32, int TAG>
+hipError_t run_dma_var(GemmParams p, long max_rows, hipStream_t st) {
+  p.MT = 0;
+  p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
+  const long ntile = ((max_rows + BM - 1) / BM + p.batches) * p.NT;
+  if (ntile == 0 || p.batches == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
   gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG>
       <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
@@ -525,7 +587,18 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p, int a_kc, i
   const int e = blockIdx.z;
   const int m0 = blockIdx.y * FT, n0 = blockIdx.x * FT;
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-  const float* A = (const float*)p.A + (size_t)e * p.a_bs;
+  // rows of this batch: uniform (M), or [var_rows[e], var_rows[e+1]) of packed buffers
+  int M = p.M;
+  size_t a_off = (size_t)e * p.a_bs, c_off = (size_t)e * p.c_bs, h_off = (size_t)e * p.h_bs;
+  if (p.var_rows) {
+    const int row0 = p.var_rows[e];
+    M = p.var_rows[e + 1] - row0;
+    a_off = (size_t)row0 * p.lda;
+    c_off = (size_t)row0 * p.ldc;
+    h_off = (size_t)row0 * p.ldh;
+  }
+  if (m0 >= M) return;
+  const float* A = (const float*)p.A + a_off;
   const float* B = (const float*)p.B + (size_t)e * p.b_bs;
   const float* B2 = p.B2 ? (const float*)p.B2 + (size_t)e * p.b_bs : nullptr;
   float acc[4][4] = {}, acc3[4][4] = {};
@@ -534,7 +607,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p, int a_kc, i
       const int kk = c / FT, r = c % FT;
       const int k = k0 + kk, m = m0 + r, n = n0 + r;
       float va = 0.f, vb = 0.f, vb3 = 0.f;
-      if (k < p.kv_a && m < p.M) va = a_kc ? A[(size_t)m * p.lda + k] : A[(size_t)k * p.lda + m];
+      if (k < p.kv_a && m < M) va = a_kc ? A[(size_t)m * p.lda + k] : A[(size_t)k * p.lda + m];
       if (k < p.kv_b && n < p.N) {
         if (b_kc) {
           vb = B[(size_t)n * p.ldb + k];
@@ -572,26 +645,26 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p, int a_kc, i
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
       const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + jj;
-      if (m >= p.M || n >= p.N) continue;
+      if (m >= M || n >= p.N) continue;
       if (EPI == EPI_STORE || EPI == EPI_STORE_ADD) {
         const bool second = m >= p.c_split;
         const int mm = second ? m - p.c_split : m;
-        float* dst = (float*)(second ? p.C2 : p.C) + (size_t)e * p.c_bs + (size_t)mm * p.ldc + n;
+        float* dst = (float*)(second ? p.C2 : p.C) + c_off + (size_t)mm * p.ldc + n;
         *dst = (EPI == EPI_STORE_ADD) ? *dst + acc[i][jj] : acc[i][jj];
       } else if (EPI == EPI_SWIGLU) {
         const float h1 = acc[i][jj], h3 = acc3[i][jj];
-        ((float*)p.C)[(size_t)e * p.c_bs + (size_t)m * p.ldc + n] = silu_f(h1) * h3;
+        ((float*)p.C)[c_off + (size_t)m * p.ldc + n] = silu_f(h1) * h3;
         if (p.H1) {
-          const size_t ho = (size_t)e * p.h_bs + (size_t)m * p.ldh + n;
+          const size_t ho = h_off + (size_t)m * p.ldh + n;
           ((float*)p.H1)[ho] = h1;
           ((float*)p.H3)[ho] = h3;
         }
       } else {
-        const size_t ho = (size_t)e * p.h_bs + (size_t)m * p.ldh + n;
+        const size_t ho = h_off + (size_t)m * p.ldh + n;
         const float h1 = ((const float*)p.H1)[ho], h3 = ((const float*)p.H3)[ho];
         const float da = acc[i][jj];
         const float sg = sigmoid_f(h1);
-        const size_t off = (size_t)e * p.c_bs + (size_t)m * p.ldc + n;
+        const size_t off = c_off + (size_t)m * p.ldc + n;
         ((float*)p.C)[off] = da * h3 * sg * (1.0f + h1 * (1.0f - sg));
         ((float*)p.C2)[off] = da * h1 * sg;
       }
@@ -862,6 +935,39 @@ hipError_t launch_shared_dW13(int dtype, const void* dH, const void* X, void* dW
   if (dtype == DT_F32) return launch_gemm_dW13(dtype, dH, X, dW1, dW3, 1, N, d, h, st);
   return run_wgrad_splitk<G_SH_DW13>(dH, 2 * h, X, d, 2 * h, d, N, dW1, dW3, h, d, part, splits,
                                      st);
+}
+
+int tc_col_blocks_w13(int h) { return (h + 127) / 128; }
+int tc_col_blocks_w2(int d) { return (d + 255) / 256; }
+
+hipError_t launch_gemm_w13_var(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
+                               int E, const int32_t* rows, const int32_t* tiles, long max_rows,
+                               int max_rows_per_expert, int d, int h, hipStream_t st) {
+  GemmParams p = base_params();
+  p.A = Xe; p.lda = d;
+  p.B = W1; p.B2 = W3; p.b_bs = (long)h * d; p.ldb = d;
+  p.M = max_rows_per_expert; p.N = h; p.K = d; p.kv_a = d; p.kv_b = d; p.batches = E;
+  p.C = A; p.ldc = h; p.ldh = h;
+  p.var_rows = rows; p.var_tiles = tiles;
+  if (max_rows == 0) return hipSuccess;
+  if (dtype == DT_F32) return run_f32<EPI_SWIGLU>(p, 1, 1, st);
+  return run_dma_var<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_TC_W13>(p, max_rows,
+                                                                                     st);
+}
+
+hipError_t launch_gemm_w2_var(int dtype, const void* A, const void* W2, void* O, int E,
+                              const int32_t* rows, const int32_t* tiles, long max_rows,
+                              int max_rows_per_expert, int d, int h, hipStream_t st) {
+  GemmParams p = base_params();
+  p.A = A; p.lda = h;
+  p.B = W2; p.b_bs = (long)d * h; p.ldb = h;
+  p.M = max_rows_per_expert; p.N = d; p.K = h; p.kv_a = h; p.kv_b = h; p.batches = E;
+  p.C = O; p.ldc = d;
+  p.var_rows = rows; p.var_tiles = tiles;
+  if (max_rows == 0) return hipSuccess;
+  if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
+  return run_dma_var<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_TC_W2>(p, max_rows,
+                                                                                   st);
 }
 
 }  // namespace ec

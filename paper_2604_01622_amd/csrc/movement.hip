@@ -13,13 +13,16 @@ namespace {
 // ---------------------------------------------------------------- gather
 // One wave per expert row; 16-byte vectors, all loads of a row issued before
 // its stores.
+// With rows_dev the row count is read from device memory (rows is then the
+// launch's upper bound).
 template <int U>
 __global__ __launch_bounds__(256) void gather_kernel(const uint4* __restrict__ X,
                                                      const int32_t* __restrict__ sel,
                                                      uint4* __restrict__ Xe, long rows, int vpr,
-                                                     int N) {
+                                                     int N, const int32_t* rows_dev) {
   const int lane = threadIdx.x & 63;
   const long r = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (rows_dev && r >= *rows_dev) return;
   if (r >= rows) return;
   const int i = sel[r];
   if ((unsigned)i >= (unsigned)N) return;  // never for a valid selection
@@ -46,6 +49,7 @@ constexpr int CB_Q = 4;      // 8-element chunks per lane per column block
 
 // Builds, for one token, the ascending list of (expert, row) it was selected
 // by, with the gate values; returns the list length.  Lists are wave-private.
+// Rows at or past K are treated as unselected (never for a valid selection).
 template <int MAXE>
 __device__ __forceinline__ int token_expert_list(const int32_t* sslot, const float* sgate,
                                                  int t, int E, int K, int2* list, float* lgate) {
@@ -67,15 +71,17 @@ __device__ __forceinline__ int token_expert_list(const int32_t* sslot, const flo
   return n;
 }
 
-// Y[i] = (Xr[i] if Xr) + sum_j g_ij Src[j, slot_ij] in ascending j; with
-// S == nullptr the gates are 1 (backward combine of dXe).  Two expert rows are
-// loaded per step so that each lane keeps 8 16-byte loads in flight.
+// Y[i] = (Xr[i] if Xr) + sum_j g_ij Src[j kstride + slot_ij] in ascending j;
+// with S == nullptr the gates are 1 (backward combine of dXe).  kstride is the
+// rows of one expert's buffer (0 when slot holds rows of one packed buffer);
+// slot values are below K.  Two expert rows are loaded per step so that each
+// lane keeps 8 16-byte loads in flight.
 template <typename T, int MAXE>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
                                                       const float* __restrict__ S,
                                                       const int32_t* __restrict__ slotT,
                                                       const T* Xr, T* Y, int N, int E, int K,
-                                                      int d) {
+                                                      int d, long kstride) {
   __shared__ int32_t sslot[MAXE * CB_TOK];
   __shared__ float sgate[CB_TOK * MAXE];
   __shared__ int2 slist[4][MAXE];
@@ -115,8 +121,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
       for (; p + 2 <= n; p += 2) {
         const int2 jr0 = slist[wave][p], jr1 = slist[wave][p + 1];
         const float g0 = sglist[wave][p], g1 = sglist[wave][p + 1];
-        const T* src0 = Src + ((size_t)jr0.x * K + jr0.y) * d;
-        const T* src1 = Src + ((size_t)jr1.x * K + jr1.y) * d;
+        const T* src0 = Src + ((size_t)jr0.x * kstride + jr0.y) * d;
+        const T* src1 = Src + ((size_t)jr1.x * kstride + jr1.y) * d;
         typename Elem<T>::Raw v0[CB_Q], v1[CB_Q];
 #pragma unroll
         for (int q = 0; q < CB_Q; ++q) {
@@ -138,7 +144,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
       if (p < n) {
         const int2 jr = slist[wave][p];
         const float g = sglist[wave][p];
-        const T* src = Src + ((size_t)jr.x * K + jr.y) * d;
+        const T* src = Src + ((size_t)jr.x * kstride + jr.y) * d;
 #pragma unroll
         for (int q = 0; q < CB_Q; ++q) {
           const int c = c0 + q * 64 + lane;
@@ -157,14 +163,14 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
 
 template <typename T>
 hipError_t run_combine(const T* Src, const float* S, const int32_t* slotT, const T* Xr, T* Y,
-                       int N, int E, int K, int d, hipStream_t st) {
+                       int N, int E, int K, int d, hipStream_t st, long kstride) {
   const int grid = (N + CB_TOK - 1) / CB_TOK;
   if (E <= 64)
-    combine_kernel<T, 64><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d);
+    combine_kernel<T, 64><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
   else if (E <= 128)
-    combine_kernel<T, 128><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d);
+    combine_kernel<T, 128><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
   else
-    combine_kernel<T, 256><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d);
+    combine_kernel<T, 256><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
   return hipGetLastError();
 }
 
@@ -304,23 +310,25 @@ __global__ void zero_kernel(uint4* p, size_t n16, unsigned char* tail, size_t nt
 }  // namespace
 
 hipError_t launch_gather(int dtype, const void* X, const int32_t* sel_token, void* Xe, long rows,
-                         int d, int N, hipStream_t st) {
+                         int d, int N, hipStream_t st, const int32_t* rows_dev) {
   if (rows == 0) return hipSuccess;
   const int vpr = d * (dtype == DT_F32 ? 4 : 2) / 16;
   const long grid = (rows + 3) / 4;
   gather_kernel<4><<<dim3((unsigned)grid), 256, 0, st>>>((const uint4*)X, sel_token, (uint4*)Xe,
-                                                         rows, vpr, N);
+                                                         rows, vpr, N, rows_dev);
   return hipGetLastError();
 }
 
 hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_t* slotT,
-                          const void* Xr, void* Y, int N, int E, int K, int d, hipStream_t st) {
+                          const void* Xr, void* Y, int N, int E, int K, int d, hipStream_t st,
+                          long kstride) {
   if (N == 0) return hipSuccess;
+  if (kstride < 0) kstride = K;
   if (dtype == DT_F32)
     return run_combine<float>((const float*)O, S, slotT, (const float*)Xr, (float*)Y, N, E, K, d,
-                              st);
+                              st, kstride);
   return run_combine<bf16_t>((const bf16_t*)O, S, slotT, (const bf16_t*)Xr, (bf16_t*)Y, N, E, K,
-                             d, st);
+                             d, st, kstride);
 }
 
 hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, const void* Xr,
@@ -328,9 +336,9 @@ hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, 
   if (N == 0) return hipSuccess;
   if (dtype == DT_F32)
     return run_combine<float>((const float*)dXe, nullptr, slotT, (const float*)Xr, (float*)dX, N,
-                              E, K, d, st);
+                              E, K, d, st, K);
   return run_combine<bf16_t>((const bf16_t*)dXe, nullptr, slotT, (const bf16_t*)Xr, (bf16_t*)dX, N,
-                             E, K, d, st);
+                             E, K, d, st, K);
 }
 
 hipError_t launch_bwd_gather(int dtype, const void* dY, const void* O, const float* S,

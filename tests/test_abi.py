@@ -149,3 +149,26 @@ def test_capacity_rule_matches_oracle(sched):
     assert np.array_equal(got, ref.capacity_ref(lens, 64, c=8.0))
     # half-to-even on exact ties: L c / E = 2.5 -> 2 and 3.5 -> 4
     assert list(ec.capacity([5, 7], 2, c=1.0)) == [2, 4]
+
+
+@pytest.mark.parametrize("k,cf", [(8, 1.0), (8, 1.25), (2, 0.0), (1, 1.5), (4, 3.0)])
+def test_tc_capacity_matches_oracle(k, cf):
+    L = [2048, 100, 7, 0, 513]
+    assert np.array_equal(ec.tc_capacity(L, 64 if k == 8 else 8, k, cf),
+                          ref.tc_capacity_ref(L, 64 if k == 8 else 8, k, cf))
+
+
+def test_tc_validation():
+    L = ec.lib()
+    P = _problem()
+    ws = 1 << 30
+    assert L.ec_tc_route(P.ref, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, None) == EC_ERR_ARG
+    assert L.ec_tc_route(P.ref, 9, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, None) == EC_ERR_ARG
+    assert L.ec_tc_route(P.ref, 2, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, ws, None) == EC_ERR_ARG
+    assert L.ec_tc_route(P.ref, 2, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 64, None) == EC_ERR_WORKSPACE
+    assert L.ec_tc_workspace_size(P.ref, 2, 0) > 0
+    assert L.ec_tc_workspace_size(P.ref, 2, 1) > L.ec_tc_workspace_size(P.ref, 2, 0)
+    assert L.ec_tc_workspace_size(P.ref, 0, 1) == 0
+    st = L.ec_tc_forward(P.ref, 2, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, FAKE, None,
+                         FAKE, 64, None)
+    assert st == EC_ERR_WORKSPACE

@@ -18,6 +18,7 @@ from paper_2604_01622_amd import synth
 pytestmark = pytest.mark.gpu
 
 S_TOL = 1e-5
+FP32_TINY = float(np.finfo(np.float32).tiny)
 
 
 def out_tol(dtype):
@@ -339,3 +340,107 @@ def test_full_train_shared_bf16():
     errs["dWs2"] = rel_l2(out["dWs2"][:, units], s2)
     print("[errs]", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
     assert all(v <= 2e-2 for v in errs.values()), errs
+
+
+# ------------------------------------------------------------------ token choice (comparison policy)
+
+def check_tc(inp, caps, top_k, inv_tau=1.0, y_rows=None, S_rows=None):
+    """Token-choice routing and forward through the C interface: scores, the kept
+    pairs (bit-exact against the oracle's selection on the GPU's scores), the
+    packed layout, the gates, and the layer output."""
+    wl = inp.wl
+    off = wl.group_offsets
+    X, Wg, W1, W3, W2 = (dev(a) for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2))
+    S, G, slot, rows, sel = ec.tc_route(X, Wg, off, caps, top_k, inv_tau, d_ff=wl.d_ff)
+    Y, rows2 = ec.tc_forward(X, Wg, W1, W3, W2, off, caps, top_k, inv_tau)
+    torch.cuda.synchronize()
+    S_h, G_h, slot_h = S.cpu().numpy(), G.cpu().numpy(), slot.cpu().numpy()
+    rows_h, sel_h = rows.cpu().numpy(), sel.cpu().numpy()
+    assert np.array_equal(rows_h, rows2.cpu().numpy())
+    srows = np.arange(wl.n_tokens) if S_rows is None else S_rows
+    S_ref = ref.router_ref(np.asarray(inp.X)[srows], inp.Wg, inv_tau)
+    # relative error, with an absolute floor at fp32's smallest normal number
+    # (scores below it cannot carry a relative precision in fp32)
+    dS = np.abs(S_h[srows].astype(np.float64) - S_ref)
+    assert np.all(dS <= S_TOL * S_ref + FP32_TINY)
+    choice, gate, kept, trows = ref.tc_select_ref(S_h.astype(np.float64), off, top_k, caps)
+    # packed layout: expert j's kept tokens, ascending, at rows [rows[j], rows[j+1])
+    want_rows = np.concatenate([[0], np.cumsum([len(r) for r in trows])])
+    assert np.array_equal(rows_h, want_rows)
+    for j in range(wl.n_experts):
+        seg = np.arange(want_rows[j], want_rows[j + 1])
+        assert np.array_equal(sel_h[seg], trows[j])
+        exp_slot = np.full(wl.n_tokens, -1)
+        exp_slot[trows[j]] = seg
+        assert np.array_equal(slot_h[j], exp_slot)
+    # gates of the kept pairs; zero elsewhere
+    Gw = np.zeros_like(G_h, dtype=np.float64)
+    for r in range(top_k):
+        Gw[np.arange(wl.n_tokens), choice[:, r]] += np.where(kept[:, r], gate[:, r], 0.0)
+    assert np.array_equal(G_h != 0, Gw != 0)
+    nz = Gw != 0
+    assert np.max(np.abs(G_h[nz] - Gw[nz]) / Gw[nz]) <= 1e-6
+    Yh = host(Y)
+    if y_rows is None:
+        Y_ref = ref.tc_forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, top_k, caps,
+                                   inv_tau, selection=(choice, kept))["Y"]
+        err = rel_l2(Yh, Y_ref)
+    else:
+        Y_ref = ref.tc_forward_rows_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, choice, kept,
+                                        y_rows, inv_tau)
+        err = rel_l2(Yh[y_rows], Y_ref)
+    print(f"[errs] tc Y {err:.2e}; kept {kept.sum()} of {kept.size} pairs; "
+          f"loads max/mean {np.diff(rows_h).max() / max(np.diff(rows_h).mean(), 1e-9):.2f}",
+          flush=True)
+    assert err <= out_tol(wl.dtype), err
+    return rows_h, kept
+
+
+@pytest.mark.parametrize("top_k,cf", [(2, 1.0), (2, 0.0), (8, 0.0)])
+def test_tc_ragged_bf16(top_k, cf):
+    wl = synth.small("tc", [300, 212], 128, 8, 192, seed=50, capacity_factor=1.0)
+    inp = synth.draw(wl)
+    caps = ec.tc_capacity(wl.group_lengths, 8, top_k, cf)
+    assert np.array_equal(caps, ref.tc_capacity_ref(wl.group_lengths, 8, top_k, cf))
+    rows, kept = check_tc(inp, caps, top_k)
+    if cf > 0:
+        assert not kept.all()            # the cap drops pairs in this case
+
+
+def test_tc_top1_odd_experts():
+    wl = synth.small("tc1", [257, 100], 64, 17, 64, seed=51, capacity_factor=1.0)
+    inp = synth.draw(wl)
+    check_tc(inp, ec.tc_capacity(wl.group_lengths, 17, 1, 1.25), 1)
+
+
+def test_tc_f32():
+    wl = synth.small("tcf", [128, 70], 64, 8, 128, dtype="f32", seed=52, capacity_factor=1.0)
+    inp = synth.draw(wl)
+    check_tc(inp, ec.tc_capacity(wl.group_lengths, 8, 2, 1.0), 2)
+
+
+def test_tc_skewed_router_with_empty_experts():
+    # router rows of very different norms: a few experts take most tokens and
+    # some none at all (zero-row experts in the grouped GEMM)
+    wl = synth.small("tcskew", [400, 300], 128, 16, 128, seed=53, capacity_factor=1.0)
+    inp = synth.draw(wl)
+    rng = np.random.default_rng(53)
+    scale = np.exp(rng.normal(0.0, 1.0, size=(16, 1)))
+    scale[[3, 9]] = 1e-3
+    inp.Wg[:] = synth.f32_to_bf16_bits((ref.widen(inp.Wg) * scale * 3).astype(np.float32))
+    for cf in (0.0, 1.0):
+        rows, kept = check_tc(inp, ec.tc_capacity(wl.group_lengths, 16, 2, cf), 2)
+        if cf == 0:
+            assert np.any(np.diff(rows) == 0)
+
+
+def test_full_tc_timestep_bf16():
+    wl = synth.TIMESTEP_BF16
+    print(f"[case] token choice on {wl.name}", flush=True)
+    inp = synth.draw(wl)
+    rng = np.random.default_rng(6)
+    srows = np.sort(rng.choice(wl.n_tokens, size=256, replace=False))
+    yrows = np.sort(rng.choice(wl.n_tokens, size=16, replace=False))
+    for cf in (1.0, 0.0):
+        caps = ec.tc_capacity(wl.group_lengths, wl.n_experts, 8, cf)
+        check_tc(inp, caps, 8, y_rows=yrows, S_rows=srows)

@@ -496,6 +496,20 @@ def test_tc_top1_is_argmax_expert():
         assert np.max(np.abs(tc["Y"][i] - want.numpy()[0])) < 1e-12
 
 
+def test_tc_restricted_and_override_forms_equal_full():
+    inp = _tiny_inputs([15, 9], 16, 5, 8, seed=44, dtype="bf16")
+    off, cap = inp.wl.group_offsets, [4, 3]
+    full = ref.tc_forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, 2, cap, 0.9)
+    again = ref.tc_forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, 2, cap, 0.9,
+                               selection=(full["choice"], full["kept"]))
+    assert np.max(np.abs(again["Y"] - full["Y"])) < 1e-12
+    rows = [0, 7, 14, 15, 23]
+    part = ref.tc_forward_rows_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, full["choice"],
+                                   full["kept"], rows, 0.9)
+    assert np.max(np.abs(part - full["Y"][rows])) < 1e-12
+    assert not full["kept"].all()                          # the caps drop pairs here
+
+
 def test_tc_capacity_rule():
     assert list(ref.tc_capacity_ref([2048, 100], 64, 8, 1.0)) == [256, 13]   # ceil(8 L / 64)
     assert list(ref.tc_capacity_ref([2048], 64, 8, 1.25)) == [320]
