@@ -167,6 +167,102 @@ def cpu_baseline(inp, caps, inv_tau, backward, budget_s=10.0):
             "seconds": dt}
 
 
+def run_tc(a):
+    """Token choice (the comparison policy, forward) on a workload's inputs, and expert
+    choice on the same inputs with the same number of token-expert pairs (c = top_k)."""
+    import torch
+    import paper_2604_01622_amd as ec
+    from paper_2604_01622_amd import binding, synth
+
+    wl = {"train": synth.TRAIN_BF16, "train_shared": synth.TRAIN_SHARED_BF16,
+          "static": synth.STATIC_BF16, "timestep": synth.TIMESTEP_BF16,
+          "fine": synth.FINE_BF16, "tiny": synth.TINY_F32}[a.workload]
+    torch.cuda.set_device(0)
+    log(f"[bench] drawing {wl.name}")
+    inp = synth.draw(wl, with_dy=False)
+    inv_tau = wl.inv_temperatures[0]
+    if a.router_skew > 0:
+        scale = np.exp(np.random.default_rng(99).normal(0.0, a.router_skew, (wl.n_experts, 1)))
+        w = inp.Wg.view(np.uint16).astype(np.uint32) << 16 if wl.dtype == "bf16" else None
+        wf = w.view(np.float32) if w is not None else inp.Wg
+        inp.Wg[:] = (synth.f32_to_bf16_bits((wf * scale).astype(np.float32)) if wl.dtype == "bf16"
+                     else (wf * scale).astype(np.float32))
+
+    def dev(x):
+        if x.dtype == np.uint16:
+            return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(x).cuda()
+
+    X, Wg, W1, W3, W2 = (dev(x) for x in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2))
+    shared = None if inp.shared is None else tuple(dev(w) for w in inp.shared)
+    N, d, E, h = wl.n_tokens, wl.d_model, wl.n_experts, wl.d_ff
+    L = np.asarray(wl.group_lengths)
+    caps = ec.tc_capacity(L, E, a.top_k, a.cf)
+    tc = ec.TcLayer(X, Wg, W1, W3, W2, wl.group_offsets, caps, a.top_k, inv_tau, shared)
+    ec_caps = ec.capacity(L, E, c=float(a.top_k))
+    ecl = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, ec_caps, inv_tau, training=False,
+                   shared=shared)
+
+    def timed(fn, events=None):
+        for _ in range(a.warmup):
+            fn()
+        torch.cuda.synchronize()
+        evs = [binding.StageEvents(len(binding.FORWARD_STAGES)) for _ in range(a.steps)]
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for i in range(a.steps):
+            evs[i].arm()
+            fn()
+        binding.StageEvents.disarm()
+        s1.record()
+        torch.cuda.synchronize()
+        ms = s0.elapsed_time(s1) / a.steps
+        st = {n: float(np.mean(col)) for n, col in
+              zip(binding.FORWARD_STAGES, zip(*[e.durations_ms() for e in evs]))}
+        return ms, st
+
+    log(f"[bench] token choice top-{a.top_k}, cf {a.cf}")
+    ms_tc, st_tc = timed(tc.forward)
+    rows = tc.rows.cpu().numpy().astype(np.int64)
+    loads = np.diff(rows)
+    R = int(rows[-1])
+    log("[bench] expert choice, same pairs")
+    ms_ec, st_ec = timed(ecl.forward)
+    Kec = int(np.sum(ec_caps))
+    shards = loads.reshape(8, -1).sum(axis=1) if E % 8 == 0 else None
+    esz = 2 if wl.dtype == "bf16" else 4
+
+    def gemm_stats(st, pairs):
+        out = {}
+        for n, fl in (("gemm_w13_swiglu", 4 * pairs * d * h), ("gemm_w2", 2 * pairs * d * h)):
+            out[n] = {"ms": round(st[n], 4), "tflops": round(fl / (st[n] * 1e-3) / 1e12, 1)}
+        for n in ("router", "topk", "gather", "combine"):
+            out[n] = {"ms": round(st[n], 4)}
+        return out
+
+    out = {"metric": METRIC, "value": round(N / (ms_tc * 1e-3), 1), "unit": "tokens/s",
+           "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_tc, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+           "data": "synthetic (seeded normal inputs and random-init weights)",
+           "config": {"workload": f"{wl.name}_tc_top{a.top_k}_cf{a.cf:g}_skew{a.router_skew:g}",
+                      "pass": "fwd",
+                      "routing": "token choice", "top_k": a.top_k, "capacity_factor": a.cf,
+                      "tokens": N, "d_model": d, "experts": E, "d_ff": h,
+                      "cap_per_group": [int(x) for x in caps]},
+           "stages": gemm_stats(st_tc, R),
+           "token_choice": {"pairs_kept": R, "pairs_chosen": a.top_k * N,
+                            "dropped_fraction": round(1 - R / (a.top_k * N), 5),
+                            "load_max_over_mean": round(float(loads.max() / loads.mean()), 4),
+                            "load_min": int(loads.min()), "load_max": int(loads.max()),
+                            "ep8_shard_max_over_mean": (None if shards is None else
+                                                        round(float(shards.max() / shards.mean()), 4))},
+           "expert_choice_same_pairs": {"tokens_per_s": round(N / (ms_ec * 1e-3), 1),
+                                        "ms": round(ms_ec, 4), "pairs": E * Kec,
+                                        "load_max_over_mean": 1.0,
+                                        "stages": gemm_stats(st_ec, E * Kec)}}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -174,6 +270,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="train",
                     choices=["train", "train_shared", "static", "timestep", "fine", "tiny"])
+    ap.add_argument("--routing", default="ec", choices=["ec", "tc"],
+                    help="tc: the token-choice comparison policy (forward), beside expert choice "
+                         "with the same number of token-expert pairs")
+    ap.add_argument("--top-k", type=int, default=8, help="token choice: experts per token")
+    ap.add_argument("--cf", type=float, default=1.0,
+                    help="token choice: capacity factor (<= 0: dropless)")
+    ap.add_argument("--router-skew", type=float, default=0.0,
+                    help="token choice: scale router rows by exp(N(0, s)) (uneven expert loads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forward-only", action="store_true")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -181,6 +285,11 @@ def main():
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
                     help="write profiles/traffic_<stage>.json from two --pmc runs and exit")
     a = ap.parse_args()
+    if a.routing == "tc" and not a.traffic_from:
+        if a.gpus != 1:
+            print("bench.py runs on exactly one GPU", file=sys.stderr)
+            sys.exit(2)
+        return run_tc(a)
     if a.traffic_from:
         recs = traffic_from(a.traffic_from[0], a.traffic_from[1], a.workload)
         for st, r in recs.items():

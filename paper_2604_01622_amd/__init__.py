@@ -19,7 +19,8 @@ from .binding import (  # noqa: F401
     tc_route,
     tc_forward,
     Layer,
+    TcLayer,
 )
 
-__all__ = ["ECError", "Problem", "Layer", "route", "forward", "backward", "capacity",
+__all__ = ["ECError", "Problem", "Layer", "TcLayer", "route", "forward", "backward", "capacity",
            "saved_views", "token_coverage", "tc_capacity", "tc_route", "tc_forward", "lib"]

@@ -373,6 +373,32 @@ class Layer:
         return self.dX, self.dWg, self.dW1, self.dW3, self.dW2
 
 
+class TcLayer:
+    """Pre-planned token-choice forward (the comparison policy): workspace and outputs
+    allocated once."""
+
+    def __init__(self, X, Wg, W1, W3, W2, group_offsets, capacity, top_k: int,
+                 inv_temperature=1.0, shared=None):
+        self.X, self.Wg, self.W1, self.W3, self.W2 = X, Wg, W1, W3, W2
+        self.shared = shared
+        self.top_k = int(top_k)
+        self.P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature, shared)
+        dev = X.device
+        self.Y = torch.empty_like(X)
+        self.rows = torch.empty((Wg.shape[0] + 1,), dtype=torch.int32, device=dev)
+        n = lib().ec_tc_workspace_size(self.P.ref, self.top_k, 1)
+        if n == 0:
+            _check(2)
+        self.ws = _empty(n, dev)
+
+    def forward(self):
+        _check(lib().ec_tc_forward(self.P.ref, self.top_k, _ptr(self.X), _ptr(self.Wg),
+                                   _ptr(self.W1), _ptr(self.W3), _ptr(self.W2),
+                                   *_shared_ptrs(self.shared), _ptr(self.Y), _ptr(self.rows),
+                                   _ptr(self.ws), self.ws.numel(), _stream()))
+        return self.Y
+
+
 FORWARD_STAGES = ("router", "topk", "gather", "gemm_w13_swiglu", "gemm_w2", "shared_w13_swiglu",
                   "shared_w2", "combine")
 BACKWARD_STAGES = ("bwd_gather", "gemm_dA_swiglu_bwd", "gemm_dW2", "gemm_dXe", "gemm_dW13",
