@@ -3,12 +3,14 @@
 // and its transpose ST [E, N]; the column top-k reads ST so that each
 // (group, expert) column is contiguous.
 //
-// bf16: one workgroup = 64 tokens, 4 waves x 16 tokens.  Each wave streams its
-// own 16 token rows straight from HBM into MFMA A-fragments (every X element is
-// used by exactly one wave, so it never touches LDS); the router matrix is
-// staged through LDS in 64-wide K chunks (double buffered) and shared by the
-// 4 waves.  v_mfma_f32_16x16x32_bf16 with fp32 accumulation; softmax in the
-// epilogue with the 16 lanes that hold one token's logits.
+// bf16: one workgroup = 64 tokens, 4 groups of 16 tokens, each group split
+// over KS waves that take disjoint K ranges.  Each wave streams its 16 token
+// rows straight from HBM into MFMA A-fragments (every X element is used by
+// exactly one wave, so it never touches LDS); the router matrix is staged
+// through LDS in 64-wide K chunks (double buffered per split) and shared by the
+// 4 groups.  v_mfma_f32_16x16x32_bf16 with fp32 accumulation; the splits are
+// summed in a fixed order through LDS, then softmax in the epilogue with the 16
+// lanes that hold one token's logits.
 #include "ec_common.h"
 #include "ec_kernels.h"
 
@@ -20,118 +22,165 @@ constexpr int RT_ROWS = 64;   // tokens per workgroup
 constexpr int RT_KC = 64;     // K chunk
 constexpr int RT_LDK = RT_KC + 8;  // padded LDS row (bf16 elements)
 
+// K splits per workgroup: the 64 tokens' 4 wave-rows of 16 tokens are each
+// repeated KS times over disjoint K ranges, so that KS * 4 waves stream X
+// concurrently (more loads in flight per CU); fewer splits for many experts
+// keep the router-matrix LDS tiles within 160 KiB.
+template <int ET> struct RouterCfg { static constexpr int KS = ET <= 4 ? 4 : (ET <= 8 ? 2 : 1); };
+
 template <int ET>
-__global__ __launch_bounds__(256) void router_softmax_bf16_kernel(
+constexpr int router_lds_bytes() {
+  constexpr int KS = RouterCfg<ET>::KS;
+  constexpr int w = KS * 2 * ET * 16 * RT_LDK * 2;     // router tiles
+  constexpr int r = KS > 1 ? KS * 4 * 64 * ET * 4 * 4 : 0;   // split partial sums
+  return w > r ? w : r;
+}
+
+template <int ET>
+__global__ __launch_bounds__(256 * RouterCfg<ET>::KS) void router_softmax_bf16_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wg, float* __restrict__ S,
     float* __restrict__ ST, int N, int d, int E, float inv_tau) {
   constexpr int EP = ET * 16;
-  __shared__ __attribute__((aligned(16))) bf16_t sW[2][EP * RT_LDK];
+  constexpr int KS = RouterCfg<ET>::KS;
+  constexpr int NT = 256 * KS;
+  __shared__ __attribute__((aligned(16))) char smem[router_lds_bytes<ET>()];
   __shared__ float sT[EP][RT_ROWS + 1];
+  bf16_t* sW = reinterpret_cast<bf16_t*>(smem);   // [KS][2][EP * RT_LDK]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  const int tg = wave & 3, ks = wave >> 2;       // token group, K split
   const int row0 = blockIdx.x * RT_ROWS;
-  const int myrow = row0 + wave * 16 + (lane & 15);
+  const int myrow = row0 + tg * 16 + (lane & 15);
   const int xrow = myrow < N ? myrow : N - 1;
   const bf16_t* xp = X + (size_t)xrow * d + (lane >> 4) * 16;
+  const int nk = d / RT_KC;
+  const int cps = (nk + KS - 1) / KS;            // chunks per split
+  // chunk c of split q, or -1 past the split's share
+  auto chunk_of = [&](int q, int i) { const int c = q * cps + i; return c < nk ? c : -1; };
 
-  // Wg chunk loader: EP rows x 8 chunks of 16 bytes
-  auto load_w = [&](int kc, uint4* regs) {
+  // router tiles of iteration i for every split: KS * EP rows x 8 chunks of 16 B
+  constexpr int WPT = (KS * EP * 8 + NT - 1) / NT;
+  auto load_w = [&](int i, uint4* regs) {
 #pragma unroll
-    for (int q = 0; q < (EP * 8 + 255) / 256; ++q) {
-      const int c = tid + q * 256;
-      if (c < EP * 8) {
-        const int r = c >> 3, ch = c & 7;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (r < E) v = *reinterpret_cast<const uint4*>(Wg + (size_t)r * d + kc + ch * 8);
-        regs[q] = v;
-      }
+    for (int q = 0; q < WPT; ++q) {
+      const int c = (tid + q * NT) % (KS * EP * 8);
+      const int sp = c / (EP * 8), r = (c >> 3) % EP, ch = c & 7;
+      const int kc = chunk_of(sp, i);
+      const bool ok = r < E && kc >= 0;
+      const uint4 v = *reinterpret_cast<const uint4*>(
+          Wg + (size_t)(r < E ? r : E - 1) * d + (kc >= 0 ? kc : 0) * RT_KC + ch * 8);
+      regs[q] = ok ? v : make_uint4(0, 0, 0, 0);
     }
   };
   auto store_w = [&](int buf, const uint4* regs) {
 #pragma unroll
-    for (int q = 0; q < (EP * 8 + 255) / 256; ++q) {
-      const int c = tid + q * 256;
-      if (c < EP * 8) {
-        const int r = c >> 3, ch = c & 7;
-        *reinterpret_cast<uint4*>(&sW[buf][r * RT_LDK + ch * 8]) = regs[q];
+    for (int q = 0; q < WPT; ++q) {
+      const int c = tid + q * NT;
+      if (c < KS * EP * 8) {
+        const int sp = c / (EP * 8), r = (c >> 3) % EP, ch = c & 7;
+        *reinterpret_cast<uint4*>(&sW[(sp * 2 + buf) * EP * RT_LDK + r * RT_LDK + ch * 8]) = regs[q];
       }
     }
+  };
+  auto load_x = [&](int i, uint4& a, uint4& b) {
+    const int kc = chunk_of(ks, i);
+    const bf16_t* q = xp + (kc >= 0 ? kc : 0) * RT_KC;
+    a = *reinterpret_cast<const uint4*>(q);
+    b = *reinterpret_cast<const uint4*>(q + 8);
   };
 
   f32x4 acc[ET];
 #pragma unroll
   for (int t = 0; t < ET; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  uint4 wreg[(EP * 8 + 255) / 256];
+  uint4 wreg[WPT];
   load_w(0, wreg);
-  uint4 xa0 = *reinterpret_cast<const uint4*>(xp);
-  uint4 xa1 = *reinterpret_cast<const uint4*>(xp + 8);
+  uint4 xa0, xa1;
+  load_x(0, xa0, xa1);
   store_w(0, wreg);
   __syncthreads();
 
-  const int nk = d / RT_KC;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    uint4 xb0 = xa0, xb1 = xa1;
-    if (kt + 1 < nk) {
-      load_w((kt + 1) * RT_KC, wreg);
-      xa0 = *reinterpret_cast<const uint4*>(xp + (kt + 1) * RT_KC);
-      xa1 = *reinterpret_cast<const uint4*>(xp + (kt + 1) * RT_KC + 8);
-    }
-    const bf16x8 a0 = __builtin_bit_cast(bf16x8, xb0);
-    const bf16x8 a1 = __builtin_bit_cast(bf16x8, xb1);
+  for (int i = 0; i < cps; ++i) {
+    const int buf = i & 1;
+    const bool live = chunk_of(ks, i) >= 0;
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    const bf16x8 a0 = __builtin_bit_cast(bf16x8, live ? xa0 : z);
+    const bf16x8 a1 = __builtin_bit_cast(bf16x8, live ? xa1 : z);
+    const int inext = i + 1 < cps ? i + 1 : i;
+    load_w(inext, wreg);
+    load_x(inext, xa0, xa1);
+    const bf16_t* sWb = &sW[(ks * 2 + buf) * EP * RT_LDK];
 #pragma unroll
     for (int t = 0; t < ET; ++t) {
-      const bf16_t* wp = &sW[buf][(t * 16 + (lane & 15)) * RT_LDK + (lane >> 4) * 16];
+      const bf16_t* wp = &sWb[(t * 16 + (lane & 15)) * RT_LDK + (lane >> 4) * 16];
       const bf16x8 b0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(wp));
       const bf16x8 b1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(wp + 8));
       acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc[t], 0, 0, 0);
       acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc[t], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_w(buf ^ 1, wreg);
+    store_w(buf ^ 1, wreg);
     __syncthreads();
   }
 
-  // Epilogue: lane holds logits of tokens 4*(lane/16)+i (i = 0..3) of this
-  // wave's 16, for experts t*16 + lane%16.
-  const int col = lane & 15;
+  // sum the K splits of each token group (fixed order), in the lane layout of the
+  // accumulators: lane holds tokens 4*(lane/16)+i of its 16, experts t*16 + lane%16
+  if constexpr (KS > 1) {
+    float* red = reinterpret_cast<float*>(smem);   // [KS][4 groups][64 lanes][ET][4]
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int lr = wave * 16 + (lane >> 4) * 4 + i;  // local row in the workgroup
-    const int row = row0 + lr;
-    float v[ET];
-    float m = -INFINITY;
+    for (int t = 0; t < ET; ++t)
+      *reinterpret_cast<f32x4*>(&red[(((ks * 4 + tg) * 64 + lane) * ET + t) * 4]) = acc[t];
+    __syncthreads();
+    if (ks == 0) {
 #pragma unroll
-    for (int t = 0; t < ET; ++t) {
-      const bool ok = t * 16 + col < E;
-      v[t] = ok ? acc[t][i] * inv_tau : -INFINITY;
-      m = fmaxf(m, v[t]);
+      for (int t = 0; t < ET; ++t) {
+        f32x4 v = acc[t];
+        for (int q = 1; q < KS; ++q)
+          v += *reinterpret_cast<const f32x4*>(&red[(((q * 4 + tg) * 64 + lane) * ET + t) * 4]);
+        acc[t] = v;
+      }
     }
+  }
+
+  if (ks == 0) {
+    const int col = lane & 15;
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-    float s = 0.f;
+    for (int i = 0; i < 4; ++i) {
+      const int lr = tg * 16 + (lane >> 4) * 4 + i;  // local row in the workgroup
+      const int row = row0 + lr;
+      float v[ET];
+      float m = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < ET; ++t) {
-      v[t] = (t * 16 + col < E) ? expf(v[t] - m) : 0.f;
-      s += v[t];
-    }
+      for (int t = 0; t < ET; ++t) {
+        const bool ok = t * 16 + col < E;
+        v[t] = ok ? acc[t][i] * inv_tau : -INFINITY;
+        m = fmaxf(m, v[t]);
+      }
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o, 64);
+      for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+      float s = 0.f;
 #pragma unroll
-    for (int t = 0; t < ET; ++t) {
-      const int e = t * 16 + col;
-      const float p = v[t] / s;
-      if (e < E) {
-        if (row < N) S[(size_t)row * E + e] = p;
-        sT[e][lr] = p;
+      for (int t = 0; t < ET; ++t) {
+        v[t] = (t * 16 + col < E) ? expf(v[t] - m) : 0.f;
+        s += v[t];
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o, 64);
+#pragma unroll
+      for (int t = 0; t < ET; ++t) {
+        const int e = t * 16 + col;
+        const float p = v[t] / s;
+        if (e < E) {
+          if (row < N) S[(size_t)row * E + e] = p;
+          sT[e][lr] = p;
+        }
       }
     }
   }
   __syncthreads();
   // transposed, coalesced write of ST[e][row0 .. row0+64)
-  for (int c = tid; c < E * RT_ROWS; c += 256) {
+  for (int c = tid; c < E * RT_ROWS; c += NT) {
     const int e = c / RT_ROWS, r = c % RT_ROWS;
     if (row0 + r < N) ST[(size_t)e * N + row0 + r] = sT[e][r];
   }
@@ -215,15 +264,20 @@ hipError_t launch_router_softmax(int dtype, const void* X, const void* Wg, float
   const bf16_t* x = (const bf16_t*)X;
   const bf16_t* w = (const bf16_t*)Wg;
   if (E <= 16)
-    router_softmax_bf16_kernel<1><<<grid, 256, 0, st>>>(x, w, S, ST, N, d, E, inv_tau);
+    router_softmax_bf16_kernel<1><<<grid, 256 * RouterCfg<1>::KS, 0, st>>>(x, w, S, ST, N, d, E,
+                                                                          inv_tau);
   else if (E <= 32)
-    router_softmax_bf16_kernel<2><<<grid, 256, 0, st>>>(x, w, S, ST, N, d, E, inv_tau);
+    router_softmax_bf16_kernel<2><<<grid, 256 * RouterCfg<2>::KS, 0, st>>>(x, w, S, ST, N, d, E,
+                                                                          inv_tau);
   else if (E <= 64)
-    router_softmax_bf16_kernel<4><<<grid, 256, 0, st>>>(x, w, S, ST, N, d, E, inv_tau);
+    router_softmax_bf16_kernel<4><<<grid, 256 * RouterCfg<4>::KS, 0, st>>>(x, w, S, ST, N, d, E,
+                                                                          inv_tau);
   else if (E <= 128)
-    router_softmax_bf16_kernel<8><<<grid, 256, 0, st>>>(x, w, S, ST, N, d, E, inv_tau);
+    router_softmax_bf16_kernel<8><<<grid, 256 * RouterCfg<8>::KS, 0, st>>>(x, w, S, ST, N, d, E,
+                                                                          inv_tau);
   else
-    router_softmax_bf16_kernel<16><<<grid, 256, 0, st>>>(x, w, S, ST, N, d, E, inv_tau);
+    router_softmax_bf16_kernel<16><<<grid, 256 * RouterCfg<16>::KS, 0, st>>>(x, w, S, ST, N, d, E,
+                                                                          inv_tau);
   return hipGetLastError();
 }
 
