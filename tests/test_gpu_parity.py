@@ -444,3 +444,40 @@ def test_full_tc_timestep_bf16():
     for cf in (1.0, 0.0):
         caps = ec.tc_capacity(wl.group_lengths, wl.n_experts, 8, cf)
         check_tc(inp, caps, 8, y_rows=yrows, S_rows=srows)
+
+
+# ------------------------------------------------------------------ randomised shapes
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_problems(seed):
+    rng = np.random.default_rng(1000 + seed)
+    G = int(rng.integers(1, 5))
+    lens = [int(x) for x in rng.integers(0, 500, size=G)]
+    if sum(lens) == 0:
+        lens[0] = 7
+    d = 64 * int(rng.integers(1, 7))
+    E = int(rng.integers(1, 41))
+    h = 64 * int(rng.integers(1, 7))
+    dtype = "f32" if seed % 4 == 3 else "bf16"
+    d_shared = 64 * int(rng.integers(0, 4))
+    if rng.random() < 0.5:
+        kw = dict(capacity_factor=float(rng.uniform(0.5, 4.0)))
+    else:
+        kw = dict(c_min=float(rng.uniform(0.5, 2.0)), c_max=float(rng.uniform(2.0, 6.0)))
+    wl = synth.small(f"rnd{seed}", lens, d, E, h, dtype=dtype, seed=2000 + seed, backward=True,
+                     inv_temperature=float(rng.choice([0.5, 1.0, 2.0])), d_shared=d_shared, **kw)
+    print(f"[case] lens={lens} d={d} E={E} h={h} {dtype} shared={d_shared} {kw}", flush=True)
+    full_case(wl)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_token_choice(seed):
+    rng = np.random.default_rng(3000 + seed)
+    lens = [int(x) for x in rng.integers(1, 400, size=int(rng.integers(1, 4)))]
+    d, h = 64 * int(rng.integers(1, 5)), 64 * int(rng.integers(1, 5))
+    E = int(rng.integers(2, 33))
+    k = int(rng.integers(1, min(E, 8) + 1))
+    cf = float(rng.choice([0.0, 1.0, 1.5]))
+    wl = synth.small(f"tcrnd{seed}", lens, d, E, h, seed=4000 + seed, capacity_factor=1.0)
+    print(f"[case] tc lens={lens} d={d} E={E} h={h} k={k} cf={cf}", flush=True)
+    check_tc(synth.draw(wl), ec.tc_capacity(lens, E, k, cf), k)
