@@ -12,12 +12,14 @@
 // operands sit in LDS as 128-byte rows with XOR-swizzled 16-byte chunks
 // (conflict-free fragment reads); K-major operands (the backward's transposed
 // products) stay K-major in LDS and are read with the transposing
-// ds_read_b64_tr_b16.  Each k-step issues half its MFMAs, then the next
-// step's fragment reads (and at a stage end the barrier and the refill), then
-// the other half, so LDS latency hides behind MFMAs in flight.  Tiles are
+// ds_read_b64_tr_b16.  The MFMAs of each k-step alternate with the next
+// step's fragment reads (and at a stage end with the refill's DMA, after the
+// barrier), so LDS latency hides behind MFMAs in flight.  Tiles are
 // numbered so that consecutive ones share an expert and stay on one XCD.
 //
 // fp32: a plain LDS-tiled FMA kernel with the same operand conventions.
+#include <type_traits>
+
 #include "ec_common.h"
 #include "ec_kernels.h"
 
@@ -333,28 +335,56 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
                                                               acc[mi][ni], 0, 0, 0);
     }
   };
-  for (int kt = 0; kt < KT; ++kt) {
+  // Fragment-read instructions per 16-wide k step (a K-major fragment takes
+  // two).  Inside a stage the MFMAs on the current fragments alternate with
+  // the reads of the next ones (one MFMA, one read, ...).  At a stage end: half
+  // the MFMAs, then this wave's waits and the barrier, then the other half
+  // alternating with the refill's DMA and the next stage's first reads.  The
+  // steps that refill a stage and the last STAGES steps that do not are two
+  // loops, so that no branch splits an interleaved group.
+  constexpr int NRD = MB * (A_KC ? 1 : 2) + NB * (B_KC ? 1 : 2);
+  constexpr int HALF = NMF / 2;
+  auto kstep = [&](int kt, auto refill) {
+    constexpr bool RF = decltype(refill)::value;
     const int stage = kt % STAGES;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int cur = kk & 1;
-      mfma_range(cur, 0, NMF / 2);
-      __builtin_amdgcn_sched_barrier(0);
       if (kk + 1 < KK) {
+        mfma_range(cur, 0, NMF);
         load_frags(cur ^ 1, stage, kk + 1);
+#pragma unroll
+        for (int q = 0; q < NRD; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NMF > NRD ? NMF - NRD : 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       } else {
-        // after the final step this reads a stale stage, harmlessly, which
-        // keeps the loop body uniform
+        mfma_range(cur, 0, HALF);
+        __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): this wave's reads are done
         if (kt + 1 < KT) wait_younger(KT - 2 - kt < STAGES - 2 ? KT - 2 - kt : STAGES - 2);
         __builtin_amdgcn_s_barrier();
-        if (kt + STAGES < KT) issue(kt + STAGES, stage);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_range(cur, HALF, NMF);
+        if constexpr (RF) issue(kt + STAGES, stage);
+        // after the final step this reads a stale stage, harmlessly
         load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
+#pragma unroll
+        for (int q = 0; q < HALF; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // MFMA
+          if constexpr (RF) __builtin_amdgcn_sched_group_barrier(0x020, (LOADS + HALF - 1) / HALF, 0);  // DMA
+          __builtin_amdgcn_sched_group_barrier(0x100, (NRD + HALF - 1) / HALF, 0);     // LDS read
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_range(cur, NMF / 2, NMF);
-      __builtin_amdgcn_sched_barrier(0);
     }
+  };
+  {
+    int kt = 0;
+    for (; kt + STAGES < KT; ++kt) kstep(kt, std::true_type{});
+    for (; kt < KT; ++kt) kstep(kt, std::false_type{});
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   __syncthreads();
