@@ -42,6 +42,7 @@ GEMM_TAGS = {"gemm_w13_swiglu": 1, "gemm_w2": 2, "gemm_dA_swiglu_bwd": 3, "gemm_
              "shared_dW2": 13, "shared_dW13": 14}
 KERNEL_SOURCES = ["paper_2604_01622_amd/csrc/gemm.hip", "paper_2604_01622_amd/csrc/ec_common.h"]
 CALIB_BYTES = 1 << 30   # plain elementwise copy used to scale the byte counters
+FLUSH_BYTES = 512 << 20  # cold-cache steps: twice the 256 MiB last-level (MALL) cache
 
 
 def sources_hash():
@@ -94,6 +95,17 @@ def traffic_from(fetch_db, write_db, workload):
                     "dispatches": len(vals), "sources_sha256_16": sources_hash(),
                     "workload": workload}
     return recs
+
+
+def _rocm_version():
+    """ROCm release of the runtime, from the installation's version file (None if absent)."""
+    for path in ("/opt/rocm/.info/version", "/opt/rocm/.info/version-dev"):
+        try:
+            with open(path) as f:
+                return f.read().strip()
+        except OSError:
+            pass
+    return None
 
 
 def log(*a):
@@ -280,6 +292,8 @@ def main():
                     help="token choice: scale router rows by exp(N(0, s)) (uneven expert loads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forward-only", action="store_true")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the cold-cache steps (a 512 MiB buffer overwritten before each)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="run one plain 1 GiB elementwise copy first (scales --pmc byte counters)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
@@ -451,6 +465,29 @@ def main():
         fms = start.elapsed_time(end) / a.steps
         out["forward_only"] = {"tokens_per_s": round(N / (fms * 1e-3), 1), "ms": round(fms, 4)}
         del inf
+
+    if not a.no_cold:
+        # cold caches: overwrite a buffer twice the size of the MALL before every
+        # step (outside the timed events), then the step alone; median over steps
+        log("[bench] cold-cache steps")
+        flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(a.steps)]
+        for i in range(a.steps):
+            flush.fill_(float(i))
+            evs[i][0].record()
+            step()
+            evs[i][1].record()
+        torch.cuda.synchronize()
+        cms = float(np.median([s0.elapsed_time(s1) for s0, s1 in evs]))
+        out["cold_cache"] = {"ms_median": round(cms, 4), "tokens_per_s": round(N / (cms * 1e-3), 1),
+                             "flush_bytes": FLUSH_BYTES}
+        del flush
+
+    props = torch.cuda.get_device_properties(0)
+    out["env"] = {"device": props.name, "gfx": getattr(props, "gcnArchName", None),
+                  "hip": torch.version.hip, "torch": torch.__version__,
+                  "rocm": _rocm_version()}
 
     if not a.no_cpu_baseline:
         log("[bench] cpu baseline (oracle on a sample)")

@@ -44,8 +44,12 @@ __global__ __launch_bounds__(256) void gather_kernel(const uint4* __restrict__ X
 }
 
 // ---------------------------------------------------------------- combine
-constexpr int CB_TOK = 16;   // tokens per workgroup (4 per wave)
+constexpr int CB_TOK = 4;    // tokens per workgroup (one per wave)
 constexpr int CB_Q = 4;      // 8-element chunks per lane per column block
+
+// A row of zeros as wide as the widest fp32 row the library accepts (d <= 16384):
+// the padding rows of a combine step read it (it stays zero).
+__device__ __attribute__((aligned(16))) uint4 cb_zero_row[16384 * 4 / 16];
 
 // Builds, for one token, the ascending list of (expert, row) it was selected
 // by, with the gate values; returns the list length.  Lists are wave-private.
@@ -74,14 +78,17 @@ __device__ __forceinline__ int token_expert_list(const int32_t* sslot, const flo
 // Y[i] = (Xr[i] if Xr) + sum_j g_ij Src[j kstride + slot_ij] in ascending j;
 // with S == nullptr the gates are 1 (backward combine of dXe).  kstride is the
 // rows of one expert's buffer (0 when slot holds rows of one packed buffer);
-// slot values are below K.  Two expert rows are loaded per step so that each
-// lane keeps 8 16-byte loads in flight.
+// slot values are below K.  Each step loads U expert rows (16 or 8 16-byte
+// loads per lane in flight) with no branch between the loads and their FMAs:
+// entries past the token's last expert read the zero row with gate 0, and lanes
+// past the row's end read its last chunk and store nothing.
 template <typename T, int MAXE>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
                                                       const float* __restrict__ S,
                                                       const int32_t* __restrict__ slotT,
                                                       const T* Xr, T* Y, int N, int E, int K,
                                                       int d, long kstride) {
+  constexpr int U = sizeof(T) == 2 ? 4 : 2;   // expert rows per step
   __shared__ int32_t sslot[MAXE * CB_TOK];
   __shared__ float sgate[CB_TOK * MAXE];
   __shared__ int2 slist[4][MAXE];
@@ -106,50 +113,39 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
     const int n = token_expert_list<MAXE>(sslot, S ? sgate : nullptr, t, E, K, slist[wave],
                                           sglist[wave]);
     for (int c0 = 0; c0 < nch; c0 += 64 * CB_Q) {
-      float acc[CB_Q][8];
+      int cc[CB_Q];
 #pragma unroll
       for (int q = 0; q < CB_Q; ++q) {
         const int c = c0 + q * 64 + lane;
-        if (Xr && c < nch) {
-          Elem<T>::load8(Xr + (size_t)i * d + c * 8, acc[q]);
+        cc[q] = c < nch ? c : nch - 1;
+      }
+      float acc[CB_Q][8];
+#pragma unroll
+      for (int q = 0; q < CB_Q; ++q) {
+        if (Xr) {
+          Elem<T>::load8(Xr + (size_t)i * d + cc[q] * 8, acc[q]);
         } else {
 #pragma unroll
           for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
         }
       }
-      int p = 0;
-      for (; p + 2 <= n; p += 2) {
-        const int2 jr0 = slist[wave][p], jr1 = slist[wave][p + 1];
-        const float g0 = sglist[wave][p], g1 = sglist[wave][p + 1];
-        const T* src0 = Src + ((size_t)jr0.x * kstride + jr0.y) * d;
-        const T* src1 = Src + ((size_t)jr1.x * kstride + jr1.y) * d;
-        typename Elem<T>::Raw v0[CB_Q], v1[CB_Q];
+      for (int p = 0; p < n; p += U) {
+        typename Elem<T>::Raw v[U][CB_Q];
+        float g[U];
 #pragma unroll
-        for (int q = 0; q < CB_Q; ++q) {
-          const int c = c0 + q * 64 + lane;
-          if (c < nch) {
-            v0[q] = Elem<T>::load_raw(src0 + c * 8);
-            v1[q] = Elem<T>::load_raw(src1 + c * 8);
-          }
+        for (int u = 0; u < U; ++u) {
+          const bool pad = p + u >= n;
+          const int2 jr = slist[wave][pad ? n - 1 : p + u];
+          const T* src = pad ? reinterpret_cast<const T*>(cb_zero_row)
+                             : Src + ((size_t)jr.x * kstride + jr.y) * d;
+          g[u] = pad ? 0.f : sglist[wave][p + u];
+#pragma unroll
+          for (int q = 0; q < CB_Q; ++q) v[u][q] = Elem<T>::load_raw(src + cc[q] * 8);
         }
 #pragma unroll
-        for (int q = 0; q < CB_Q; ++q) {
-          const int c = c0 + q * 64 + lane;
-          if (c < nch) {
-            Elem<T>::fma_raw(acc[q], g0, v0[q]);   // ascending expert order
-            Elem<T>::fma_raw(acc[q], g1, v1[q]);
-          }
-        }
-      }
-      if (p < n) {
-        const int2 jr = slist[wave][p];
-        const float g = sglist[wave][p];
-        const T* src = Src + ((size_t)jr.x * kstride + jr.y) * d;
+        for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int q = 0; q < CB_Q; ++q) {
-          const int c = c0 + q * 64 + lane;
-          if (c < nch) Elem<T>::fma_raw(acc[q], g, Elem<T>::load_raw(src + c * 8));
-        }
+          for (int q = 0; q < CB_Q; ++q) Elem<T>::fma_raw(acc[q], g[u], v[u][q]);   // ascending j
       }
 #pragma unroll
       for (int q = 0; q < CB_Q; ++q) {
