@@ -237,10 +237,12 @@ int ec_tc_forward(const ec_problem *p, int32_t top_k, const void *X, const void 
  * Stages of ec_moe_forward: 0 router+softmax, 1 top-k, 2 gather,
  *   3 W1/W3 grouped GEMM + SwiGLU, 4 W2 grouped GEMM, 5 shared W1/W3 + SwiGLU,
  *   6 shared W2, 7 combine (5 and 6 are empty without shared experts).
- * Stages of ec_moe_backward: 0 dY gather + gate gradient, 1 dA grouped GEMM +
- *   SwiGLU backward, 2 dW2, 3 dXe, 4 dW1/dW3, 5 router dZ, 6 router dX,
- *   7 shared dA + SwiGLU backward, 8 shared dW2, 9 shared dX, 10 shared
- *   dW1/dW3 (7-10 empty without shared experts), 11 combine of dXe, 12 dWg.
+ * Stages of ec_moe_backward: 0 weight transposes (bf16: W2, W1, W3 and the
+ *   shared experts' weights, so that the dA and dX products read K-contiguous
+ *   weights; empty for fp32), 1 dY gather + gate gradient, 2 dA grouped GEMM +
+ *   SwiGLU backward, 3 dW2, 4 dXe, 5 dW1/dW3, 6 router dZ, 7 router dX,
+ *   8 shared dA + SwiGLU backward, 9 shared dW2, 10 shared dX, 11 shared
+ *   dW1/dW3 (8-11 empty without shared experts), 12 combine of dXe, 13 dWg.
  * Stages of ec_route: 0 router+softmax, 1 top-k.                              */
 int ec_set_stage_events(hipEvent_t *events /* HOST array */, int n_events);
 

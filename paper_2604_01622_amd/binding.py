@@ -401,9 +401,9 @@ class TcLayer:
 
 FORWARD_STAGES = ("router", "topk", "gather", "gemm_w13_swiglu", "gemm_w2", "shared_w13_swiglu",
                   "shared_w2", "combine")
-BACKWARD_STAGES = ("bwd_gather", "gemm_dA_swiglu_bwd", "gemm_dW2", "gemm_dXe", "gemm_dW13",
-                   "router_dz", "router_dx", "shared_dA_swiglu_bwd", "shared_dW2", "shared_dX",
-                   "shared_dW13", "bwd_combine", "router_dwg")
+BACKWARD_STAGES = ("weight_transpose", "bwd_gather", "gemm_dA_swiglu_bwd", "gemm_dW2",
+                   "gemm_dXe", "gemm_dW13", "router_dz", "router_dx", "shared_dA_swiglu_bwd",
+                   "shared_dW2", "shared_dX", "shared_dW13", "bwd_combine", "router_dwg")
 
 
 class StageEvents:

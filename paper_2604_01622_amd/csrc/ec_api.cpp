@@ -154,6 +154,12 @@ struct BwdWs {
   void* dHs;      // [N, 2 hs] shared experts' dH1 | dH3
   float* spart;   // split-K partials of the shared weight gradients
   int s_splits2, s_splits13;
+  // bf16 only: the weights transposed so that the dA and dX products read them
+  // K-contiguous
+  void* W2T;      // [E, h, d]
+  void* W13T;     // [E, d, 2h]: row n = column n of W1, then of W3
+  void* Ws2T;     // [hs, d]
+  void* Ws13T;    // [d, 2 hs]
 };
 
 BwdWs carve_bwd(Carve& c, const Plan& P) {
@@ -174,6 +180,15 @@ BwdWs carve_bwd(Carve& c, const Plan& P) {
     w.s_splits13 = ec::wgrad_splits(2 * P.hs, P.d, P.N);
     const size_t a = (size_t)w.s_splits2 * P.d * P.hs, b = (size_t)w.s_splits13 * 2 * P.hs * P.d;
     if (P.dtype == EC_BF16) w.spart = (float*)c.take((a > b ? a : b) * 4);
+  }
+  w.W2T = w.W13T = w.Ws2T = w.Ws13T = nullptr;
+  if (P.dtype == EC_BF16) {
+    w.W2T = c.take((size_t)P.E * P.h * P.d * 2);
+    w.W13T = c.take((size_t)P.E * P.d * 2 * P.h * 2);
+    if (P.hs) {
+      w.Ws2T = c.take((size_t)P.hs * P.d * 2);
+      w.Ws13T = c.take((size_t)P.d * 2 * P.hs * 2);
+    }
   }
   return w;
 }
@@ -603,30 +618,51 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   const int E = P.E, d = P.d, h = P.h, N = P.N, hs = P.hs;
   void* dXe = w.dO;  // dO is dead once dW2 is formed
   EC_HIP(mark(0, stream));
-  EC_HIP(ec::launch_bwd_gather(P.dtype, dY, s.O, s.S, s.sel, w.dO, w.dSp, N, E, M, d, stream));
+  if (P.dtype == EC_BF16) {
+    // the weights read K-major by dA = dO W2 and dXe = dH1 W1 + dH3 W3, transposed
+    // once per call so that both products read K-contiguous operands
+    if (M > 0) {
+      EC_HIP(ec::launch_transpose_bf16(W2, E, d, h, (long)d * h, w.W2T, d, (long)h * d, stream));
+      EC_HIP(ec::launch_transpose_bf16(W1, E, h, d, (long)h * d, w.W13T, 2 * h,
+                                       (long)d * 2 * h, stream));
+      EC_HIP(ec::launch_transpose_bf16(W3, E, h, d, (long)h * d, (uint16_t*)w.W13T + h, 2 * h,
+                                       (long)d * 2 * h, stream));
+    }
+    if (hs && N > 0) {
+      EC_HIP(ec::launch_transpose_bf16(Ws2, 1, d, hs, 0, w.Ws2T, d, 0, stream));
+      EC_HIP(ec::launch_transpose_bf16(Ws1, 1, hs, d, 0, w.Ws13T, 2 * hs, 0, stream));
+      EC_HIP(ec::launch_transpose_bf16(Ws3, 1, hs, d, 0, (uint16_t*)w.Ws13T + hs, 2 * hs, 0,
+                                       stream));
+    }
+  }
   EC_HIP(mark(1, stream));
-  EC_HIP(ec::launch_gemm_dA(P.dtype, w.dO, W2, s.H1, s.H3, w.dH, E, M, d, h, stream));
+  EC_HIP(ec::launch_bwd_gather(P.dtype, dY, s.O, s.S, s.sel, w.dO, w.dSp, N, E, M, d, stream));
   EC_HIP(mark(2, stream));
-  EC_HIP(ec::launch_gemm_dW2(P.dtype, w.dO, s.A, dW2, E, M, d, h, stream));
+  EC_HIP(ec::launch_gemm_dA(P.dtype, w.dO, W2, s.H1, s.H3, w.dH, E, M, d, h, stream, false,
+                            w.W2T));
   EC_HIP(mark(3, stream));
-  EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream));
+  EC_HIP(ec::launch_gemm_dW2(P.dtype, w.dO, s.A, dW2, E, M, d, h, stream));
   EC_HIP(mark(4, stream));
-  EC_HIP(ec::launch_gemm_dW13(P.dtype, w.dH, s.Xe, dW1, dW3, E, M, d, h, stream));
+  EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream, false, w.W13T));
   EC_HIP(mark(5, stream));
+  EC_HIP(ec::launch_gemm_dW13(P.dtype, w.dH, s.Xe, dW1, dW3, E, M, d, h, stream));
+  EC_HIP(mark(6, stream));
   EC_HIP(ec::launch_router_dz(s.S, w.dSp, s.slot, w.dZ, w.dZb, N, E, P.EP, M,
                               p->inv_temperature, stream));
-  EC_HIP(mark(6, stream));
+  EC_HIP(mark(7, stream));
   const void* dZop = P.dtype == EC_BF16 ? (const void*)w.dZb : (const void*)w.dZ;
   EC_HIP(ec::launch_router_dx(P.dtype, dZop, Wg, dX, N, E, P.EP, d, stream));
-  EC_HIP(mark(7, stream));
+  EC_HIP(mark(8, stream));
   if (hs && N > 0) {
     // shared experts: their output gradient is dY itself (no gate)
-    EC_HIP(ec::launch_gemm_dA(P.dtype, dY, Ws2, s.Hs1, s.Hs3, w.dHs, 1, N, d, hs, stream, true));
-    EC_HIP(mark(8, stream));
-    EC_HIP(ec::launch_shared_dW2(P.dtype, dY, s.As, dWs2, N, d, hs, w.spart, w.s_splits2, stream));
+    EC_HIP(ec::launch_gemm_dA(P.dtype, dY, Ws2, s.Hs1, s.Hs3, w.dHs, 1, N, d, hs, stream, true,
+                              w.Ws2T));
     EC_HIP(mark(9, stream));
-    EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dHs, Ws1, Ws3, dX, 1, N, d, hs, stream, true));
+    EC_HIP(ec::launch_shared_dW2(P.dtype, dY, s.As, dWs2, N, d, hs, w.spart, w.s_splits2, stream));
     EC_HIP(mark(10, stream));
+    EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dHs, Ws1, Ws3, dX, 1, N, d, hs, stream, true,
+                               w.Ws13T));
+    EC_HIP(mark(11, stream));
     EC_HIP(ec::launch_shared_dW13(P.dtype, w.dHs, X, dWs1, dWs3, N, d, hs, w.spart,
                                   w.s_splits13, stream));
   } else {
@@ -635,15 +671,15 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
       EC_HIP(ec::launch_zero(dWs3, (size_t)hs * d * P.esz, stream));
       EC_HIP(ec::launch_zero(dWs2, (size_t)hs * d * P.esz, stream));
     }
-    EC_HIP(mark(8, stream));
     EC_HIP(mark(9, stream));
     EC_HIP(mark(10, stream));
+    EC_HIP(mark(11, stream));
   }
-  EC_HIP(mark(11, stream));
-  EC_HIP(ec::launch_bwd_combine(P.dtype, dXe, s.slot, dX, dX, N, E, M, d, stream));
   EC_HIP(mark(12, stream));
-  EC_HIP(ec::launch_router_dwg(P.dtype, dZop, X, dWg, w.part, w.splits, N, E, P.EP, d, stream));
+  EC_HIP(ec::launch_bwd_combine(P.dtype, dXe, s.slot, dX, dX, N, E, M, d, stream));
   EC_HIP(mark(13, stream));
+  EC_HIP(ec::launch_router_dwg(P.dtype, dZop, X, dWg, w.part, w.splits, N, E, P.EP, d, stream));
+  EC_HIP(mark(14, stream));
   return EC_OK;
 }
 

@@ -79,13 +79,18 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
                           int h, hipStream_t st, bool shared = false);
 // dA = dO W2 and the SwiGLU backward: dH[:, 0:h] = dH1, dH[:, h:2h] = dH3 ([E,M,2h]).
+// W2T (bf16, may be null): W2 transposed, [E, h, d]; the product then reads
+// K-contiguous weights.
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
-                          bool shared = false);
+                          bool shared = false, const void* W2T = nullptr);
 // dXe = dH1 W1 + dH3 W3  ([E,M,d]).
 // shared: dXe += dH1 W1 + dH3 W3 (the shared experts' term added to dX).
+// W13T (bf16, may be null): [E, d, 2h], row n = column n of W1 then of W3; the
+// product then reads K-contiguous weights.
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
-                           int E, int M, int d, int h, hipStream_t st, bool shared = false);
+                           int E, int M, int d, int h, hipStream_t st, bool shared = false,
+                           const void* W13T = nullptr);
 // dW2 = dO^T A  ([E,d,h]).
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
                            int d, int h, hipStream_t st);
@@ -142,5 +147,9 @@ hipError_t launch_gemm_w2_var(int dtype, const void* A, const void* W2, void* O,
 
 // Fill n int32/fp32/bytes with zero (a kernel, not a memset node).
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);
+// dst[b][c][r] = src[b][r][c] for B bf16 matrices of R x C (R, C multiples of
+// 64); src_bs / dst_bs elements per matrix, dst rows of ldd elements.
+hipError_t launch_transpose_bf16(const void* src, int B, int R, int C, long src_bs, void* dst,
+                                 int ldd, long dst_bs, hipStream_t st);
 
 }  // namespace ec

@@ -776,7 +776,7 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
-                          bool shared) {
+                          bool shared, const void* W2T) {
   // dA[m, n] = sum_k dO[m, k] W2[k, n]  (k over d, n over h); epilogue -> dH1, dH3
   GemmParams p = base_params();
   p.A = dO; p.a_bs = (long)M * d; p.lda = d;
@@ -787,13 +787,20 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
   p.H1 = (void*)H1; p.H3 = (void*)H3; p.h_bs = (long)M * h; p.ldh = h;
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
+  if (W2T) {   // B[n, k] = W2T[n, k]: K-contiguous
+    p.B = W2T; p.b_bs = (long)h * d; p.ldb = d;
+    if (shared)
+      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
+    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_DA>(p, st);
+  }
   if (shared)
     return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_DA>(p, st);
 }
 
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
-                           int E, int M, int d, int h, hipStream_t st, bool shared) {
+                           int E, int M, int d, int h, hipStream_t st, bool shared,
+                           const void* W13T) {
   // dXe[m, n] = sum_k dH[m, k] W13[k, n], k < h from W1, k >= h from W3
   GemmParams p = base_params();
   p.A = dH; p.a_bs = (long)M * 2 * h; p.lda = 2 * h;
@@ -801,12 +808,17 @@ hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void
   p.M = M; p.N = d; p.K = 2 * h; p.kv_a = 2 * h; p.kv_b = 2 * h; p.batches = E;
   p.C = dXe; p.c_bs = (long)M * d; p.ldc = d;
   if (M == 0) return hipSuccess;
-  // the shared experts' input gradient is added to dX
-  if (shared) {
-    if (dtype == DT_F32) return run_f32<EPI_STORE_ADD>(p, 1, 0, st);
-    return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
+  if (dtype == DT_F32) return shared ? run_f32<EPI_STORE_ADD>(p, 1, 0, st)
+                                     : run_f32<EPI_STORE>(p, 1, 0, st);
+  if (W13T) {   // B[n, k] = W13T[n, k]: K-contiguous
+    p.B = W13T; p.B2 = nullptr; p.b_bs = (long)d * 2 * h; p.ldb = 2 * h; p.k_split = 1 << 30;
+    // the shared experts' input gradient is added to dX
+    if (shared)
+      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
+    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_DXE>(p, st);
   }
-  if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 0, st);
+  if (shared)
+    return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE, false, G_DXE>(p, st);
 }
 
