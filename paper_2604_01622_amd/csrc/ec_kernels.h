@@ -86,8 +86,8 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
                           bool shared = false, const void* W2T = nullptr);
 // dXe = dH1 W1 + dH3 W3  ([E,M,d]).
 // shared: dXe += dH1 W1 + dH3 W3 (the shared experts' term added to dX).
-// W13T (bf16, may be null): [E, d, 2h], row n = column n of W1 then of W3; the
-// product then reads K-contiguous weights.
+// W13T (required for bf16): [E, d, 2h], row n = column n of W1 then of W3, so
+// that the product reads K-contiguous weights.
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
                            int E, int M, int d, int h, hipStream_t st, bool shared = false,
                            const void* W13T = nullptr);

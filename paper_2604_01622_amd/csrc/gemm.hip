@@ -42,7 +42,8 @@ struct GemmParams {
   int lda;
   // B operand, element (n, k) of batch e:
   //   K-contiguous:  B[e*b_bs + n*ldb + k]  (SwiGLU: rows of W1 and W3 side by side)
-  //   N-contiguous:  B[e*b_bs + k*ldb + n] for k < k_split, else B2[e*b_bs + (k-k_split)*ldb + n]
+  //   N-contiguous:  B[e*b_bs + k*ldb + n]; the fp32 kernel reads rows k >= k_split
+  //                  from B2 instead (B2[e*b_bs + (k-k_split)*ldb + n])
   const void* B;
   const void* B2;
   long b_bs;
@@ -159,10 +160,16 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
 
   // ---- DMA sources.  Load q of a thread fills 1 KiB block (wave*L + q) of
   // the operand's stage area: 64 chunks, lane -> chunk.
-  const bf16_t* a_src[OA::LOADS];   // K-contiguous: fixed row pointer
-  int a_col[OA::LOADS], a_row[OA::LOADS];
+  // K-contiguous: the row pointer of the chunk, offset by kt * KSTEP per step.
+  // K-major: the chunk's address at k-step 0 (or the zero block for columns
+  // past the operand), advanced by KSTEP rows after every issue; rows past the
+  // valid K read the zero block instead.
+  const bf16_t* a_src[OA::LOADS];
+  int a_row[OA::LOADS];
+  long a_step[OA::LOADS];
   const bf16_t* b_src[OB::LOADS];
-  int b_col[OB::LOADS], b_row[OB::LOADS];
+  int b_row[OB::LOADS];
+  long b_step[OB::LOADS];
 #pragma unroll
   for (int q = 0; q < OA::LOADS; ++q) {
     const int id = (wave * OA::LOADS + q) * 64 + lane;
@@ -173,8 +180,10 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       a_src[q] = Ab + (size_t)r * p.lda + lc * 8;
     } else {
       const int row = id / OA::CPR, lc = (id % OA::CPR) ^ km_swz(row);
-      a_row[q] = row;                 // k within the step
-      a_col[q] = m0 + lc * 8;         // first column of the chunk
+      const int col = m0 + lc * 8;   // first column of the chunk
+      a_row[q] = row;                // k within the step
+      a_src[q] = col < M ? Ab + (size_t)row * p.lda + col : g_zero_block;
+      a_step[q] = col < M ? (long)KSTEP * p.lda : 0;
     }
   }
 #pragma unroll
@@ -195,10 +204,13 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       b_src[q] = rp + lc * 8;
     } else {
       const int row = id / OB::CPR, lc = (id % OB::CPR) ^ km_swz(row);
+      const int col = n0 + lc * 8;
       b_row[q] = row;
-      b_col[q] = n0 + lc * 8;
+      b_src[q] = col < p.N ? Bb + (size_t)row * p.ldb + col : g_zero_block;
+      b_step[q] = col < p.N ? (long)KSTEP * p.ldb : 0;
     }
   }
+  // Issues k-step kt; the calls come with kt = 0, 1, 2, ... in order.
   auto issue = [&](int kt, int stage) {
     char* base = smem + stage * STAGE_BYTES;
 #pragma unroll
@@ -207,8 +219,8 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       if constexpr (A_KC) {
         g = a_src[q] + kt * KSTEP;
       } else {
-        const int k = kt * KSTEP + a_row[q];
-        g = (k < p.kv_a && a_col[q] < M) ? Ab + (size_t)k * p.lda + a_col[q] : g_zero_block;
+        g = (kt * KSTEP + a_row[q] < p.kv_a) ? a_src[q] : g_zero_block;
+        a_src[q] += a_step[q];
       }
       dma16(g, base + (wave * OA::LOADS + q) * 1024);
     }
@@ -218,10 +230,8 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       if constexpr (B_KC) {
         g = b_src[q] + kt * KSTEP;
       } else {
-        const int k = kt * KSTEP + b_row[q];
-        const bf16_t* rowp = (k < p.k_split) ? Bb + (size_t)k * p.ldb
-                                             : B2b + (size_t)(k - p.k_split) * p.ldb;
-        g = (k < p.kv_b && b_col[q] < p.N) ? rowp + b_col[q] : g_zero_block;
+        g = (kt * KSTEP + b_row[q] < p.kv_b) ? b_src[q] : g_zero_block;
+        b_src[q] += b_step[q];
       }
       dma16(g, base + OA::BYTES + (wave * OB::LOADS + q) * 1024);
     }
@@ -390,20 +400,30 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   __syncthreads();
 
   // ---- epilogue: stage 32-row slices of the wave tile through LDS ----
+  // The accumulators of a slice go to LDS (fp32, row-major); then every lane
+  // reads its 16-byte output chunks back in batches of EQ with no branch
+  // between the reads (their LDS addresses always lie inside the slice), and
+  // only then converts and stores the chunks that fall inside the matrix.
   float* stage_f = reinterpret_cast<float*>(smem) + wave * 32 * SLD;
+  constexpr int HW = WN / 2;                                    // SwiGLU: outputs per row
+  constexpr int CPR = (EPI == EPI_SWIGLU) ? HW / 8 : WN / 8;    // chunks per slice row
+  constexpr int NCH = 32 * CPR;                                 // chunks per slice
+  constexpr int NQ = (NCH + 63) / 64;                           // chunks per lane
+  constexpr int EQ = (EPI == EPI_SWIGLU_BWD && NQ > 4) ? 4 : NQ;  // chunks per batch
+  static_assert(NQ % EQ == 0, "whole batches");
   // SwiGLU backward: this slice's H1/H3 chunks are loaded before the slice is
   // staged, so their latency overlaps the staging (rows or columns past the
   // matrix read element 0 and are not stored).
-  constexpr int BWD_CPR = WN / 8, BWD_Q = (EPI == EPI_SWIGLU_BWD) ? (32 * BWD_CPR) / 64 : 1;
-  u32x4 h1raw[BWD_Q], h3raw[BWD_Q];
+  constexpr int HQ = (EPI == EPI_SWIGLU_BWD) ? NQ : 1;
+  u32x4 h1raw[HQ], h3raw[HQ];
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
+    const int mbase = m0 + wm * WM + mi * 32;
     if constexpr (EPI == EPI_SWIGLU_BWD) {
-      const int mb = m0 + wm * WM + mi * 32;
 #pragma unroll
-      for (int q = 0; q < BWD_Q; ++q) {
+      for (int q = 0; q < NQ; ++q) {
         const int c = lane + q * 64;
-        const int m = mb + c / BWD_CPR, n = n0 + wn * WN + (c % BWD_CPR) * 8;
+        const int m = mbase + c / CPR, n = n0 + wn * WN + (c % CPR) * 8;
         const size_t ho = (m < M && n < p.N) ? tc.h_off + (size_t)m * p.ldh + n : 0;
         h1raw[q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H1 + ho);
         h3raw[q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H3 + ho);
@@ -418,20 +438,30 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       }
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
-    const int mbase = m0 + wm * WM + mi * 32;
-    if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_ADD) {
-      constexpr int CPR = WN / 8;
 #pragma unroll
-      for (int q = 0; q < (32 * CPR) / 64; ++q) {
+    for (int q0 = 0; q0 < NQ; q0 += EQ) {
+      // chunk q of this lane: slice row c / CPR, columns (c % CPR) * 8 .. + 7
+      float v[EQ][8], v3[EPI == EPI_SWIGLU ? EQ : 1][8];
+#pragma unroll
+      for (int e = 0; e < EQ; ++e) {
+        int c = lane + (q0 + e) * 64;
+        c = c < NCH ? c : NCH - 1;
+        const float* src = stage_f + (c / CPR) * SLD + (c % CPR) * 8;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[e][u] = src[u];
+        if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v3[e][u] = src[HW + u];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < EQ; ++e) {
+        const int q = q0 + e;
         const int c = lane + q * 64;
-        const int row = c / CPR, cc = c % CPR;
-        const int m = mbase + row;
-        const int n = n0 + wn * WN + cc * 8;
-        if (m < M && n < p.N) {
-          const float* v = stage_f + row * SLD + cc * 8;
-          float vv[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) vv[u] = v[u];
+        const int m = mbase + c / CPR;
+        const int n = n0 + wn * (EPI == EPI_SWIGLU ? HW : WN) + (c % CPR) * 8;
+        if (c >= NCH || m >= M || n >= p.N) continue;
+        if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_ADD) {
           const bool second = m >= p.c_split;
           const int mm = second ? m - p.c_split : m;
           const size_t off = tc.c_off + (size_t)mm * p.ldc + n;
@@ -441,64 +471,37 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
               float old[8];
               Elem<float>::load8(dst, old);
 #pragma unroll
-              for (int u = 0; u < 8; ++u) vv[u] += old[u];
+              for (int u = 0; u < 8; ++u) v[e][u] += old[u];
             }
-            Elem<float>::store8(dst, vv);
+            Elem<float>::store8(dst, v[e]);
           } else {
             bf16_t* dst = (bf16_t*)(second ? p.C2 : p.C) + off;
             if constexpr (EPI == EPI_STORE_ADD) {
               float old[8];
               Elem<bf16_t>::load8(dst, old);
 #pragma unroll
-              for (int u = 0; u < 8; ++u) vv[u] += old[u];
+              for (int u = 0; u < 8; ++u) v[e][u] += old[u];
             }
-            Elem<bf16_t>::store8(dst, vv);
+            Elem<bf16_t>::store8(dst, v[e]);
           }
-        }
-      }
-    } else if constexpr (EPI == EPI_SWIGLU) {
-      constexpr int HW = WN / 2;
-      constexpr int CPR = HW / 8;
+        } else if constexpr (EPI == EPI_SWIGLU) {
+          float a[8];
 #pragma unroll
-      for (int q = 0; q < (32 * CPR + 63) / 64; ++q) {
-        const int c = lane + q * 64;
-        const int row = c / CPR, cc = c % CPR;
-        const int m = mbase + row;
-        const int n = n0 + wn * HW + cc * 8;
-        if (c < 32 * CPR && m < M && n < p.N) {
-          const float* v1 = stage_f + row * SLD + cc * 8;
-          const float* v3 = v1 + HW;
-          float a[8], h1[8], h3[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            h1[u] = v1[u];
-            h3[u] = v3[u];
-            a[u] = silu_f(h1[u]) * h3[u];
-          }
+          for (int u = 0; u < 8; ++u) a[u] = silu_f(v[e][u]) * v3[e][u];
           Elem<bf16_t>::store8((bf16_t*)p.C + tc.c_off + (size_t)m * p.ldc + n, a);
           if (p.H1) {
             const size_t ho = tc.h_off + (size_t)m * p.ldh + n;
-            Elem<bf16_t>::store8((bf16_t*)p.H1 + ho, h1);
-            Elem<bf16_t>::store8((bf16_t*)p.H3 + ho, h3);
+            Elem<bf16_t>::store8((bf16_t*)p.H1 + ho, v[e]);
+            Elem<bf16_t>::store8((bf16_t*)p.H3 + ho, v3[e]);
           }
-        }
-      }
-    } else {  // EPI_SWIGLU_BWD
-#pragma unroll
-      for (int q = 0; q < BWD_Q; ++q) {
-        const int c = lane + q * 64;
-        const int row = c / BWD_CPR, cc = c % BWD_CPR;
-        const int m = mbase + row;
-        const int n = n0 + wn * WN + cc * 8;
-        if (m < M && n < p.N) {
-          const float* v = stage_f + row * SLD + cc * 8;
+        } else {  // EPI_SWIGLU_BWD
           float d1[8], d3[8];
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
             const uint32_t w1 = h1raw[q][u >> 1], w3 = h3raw[q][u >> 1];
             const float h1 = bf16_to_f32((u & 1) ? (w1 >> 16) : (w1 & 0xffffu));
             const float h3 = bf16_to_f32((u & 1) ? (w3 >> 16) : (w3 & 0xffffu));
-            const float da = v[u];
+            const float da = v[e][u];
             const float sg = sigmoid_f(h1);
             d3[u] = da * h1 * sg;
             d1[u] = da * h3 * sg * (1.0f + h1 * (1.0f - sg));
@@ -810,16 +813,13 @@ hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return shared ? run_f32<EPI_STORE_ADD>(p, 1, 0, st)
                                      : run_f32<EPI_STORE>(p, 1, 0, st);
-  if (W13T) {   // B[n, k] = W13T[n, k]: K-contiguous
-    p.B = W13T; p.B2 = nullptr; p.b_bs = (long)d * 2 * h; p.ldb = 2 * h; p.k_split = 1 << 30;
-    // the shared experts' input gradient is added to dX
-    if (shared)
-      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
-    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_DXE>(p, st);
-  }
+  // bf16 reads the transposed weights, B[n, k] = W13T[n, k] (K-contiguous)
+  if (!W13T) return hipErrorInvalidValue;
+  p.B = W13T; p.B2 = nullptr; p.b_bs = (long)d * 2 * h; p.ldb = 2 * h; p.k_split = 1 << 30;
+  // the shared experts' input gradient is added to dX
   if (shared)
-    return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
-  return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE, false, G_DXE>(p, st);
+    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_DXE>(p, st);
 }
 
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
