@@ -125,8 +125,6 @@ def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits, hs=0):
                             + (2 * P * h * s if save_h else 0)),
         "gemm_w2": (2 * P * d * h, P * h * s + E * d * h * s + P * d * s),
         "combine": (0, 2 * E * N * 4 + P * d * s + N * d * s),
-        # bf16: W2, W1, W3 (and the shared experts' weights) read and written once
-        "weight_transpose": (0, (2 * 3 * E * d * h + 2 * 3 * hs * d) * s if s == 2 else 0),
         "bwd_gather": (0, 3 * P * 4 + 3 * P * d * s),
         "gemm_dA_swiglu_bwd": (2 * P * d * h, P * d * s + E * d * h * s + 4 * P * h * s),
         "gemm_dW2": (2 * P * d * h, P * d * s + P * h * s + E * d * h * s),

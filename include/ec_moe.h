@@ -109,6 +109,12 @@ typedef struct {
   size_t Hs1;        /* dtype [N, hs]   shared experts' W1 projection           */
   size_t Hs3;        /* dtype [N, hs]   shared experts' W3 projection           */
   size_t As;         /* dtype [N, hs]   shared experts' SiLU(Hs1) * Hs3         */
+  /* bf16 only (offsets equal `total` for fp32): the weights transposed, written
+   * by the forward and read K-contiguous by the backward's dA and dX products. */
+  size_t W2T;        /* bf16 [E, h, d]  W2 transposed                           */
+  size_t W13T;       /* bf16 [E, d, 2h] row k = W1[:, k] then W3[:, k]          */
+  size_t Ws2T;       /* bf16 [hs, d]    Ws2 transposed                          */
+  size_t Ws13T;      /* bf16 [d, 2 hs]  row k = Ws1[:, k] then Ws3[:, k]        */
   size_t total;      /* bytes of the whole buffer                               */
 } ec_saved_layout;
 
@@ -169,7 +175,9 @@ int ec_token_coverage(const ec_problem *p, const int32_t *slot,
  *   Ws1, Ws3 [hs, d] dtype;  Ws2 [d, hs] dtype (NULL when d_shared = 0);
  *   Y [N, d] dtype out.
  * saved: NULL for inference, else ec_saved_layout.total bytes that receive the
- * activations the backward needs.  ws: ec_workspace_size(p, 1) bytes.         */
+ * activations the backward needs (for bf16 also the transposed expert weights,
+ * written by the W1/W3 and W2 products as their tiles pass through on-chip
+ * memory).  ws: ec_workspace_size(p, 1) bytes.                                 */
 int ec_moe_forward(const ec_problem *p, const void *X, const void *Wg,
                    const void *W1, const void *W3, const void *W2,
                    const void *Ws1, const void *Ws3, const void *Ws2, void *Y,
@@ -237,12 +245,10 @@ int ec_tc_forward(const ec_problem *p, int32_t top_k, const void *X, const void 
  * Stages of ec_moe_forward: 0 router+softmax, 1 top-k, 2 gather,
  *   3 W1/W3 grouped GEMM + SwiGLU, 4 W2 grouped GEMM, 5 shared W1/W3 + SwiGLU,
  *   6 shared W2, 7 combine (5 and 6 are empty without shared experts).
- * Stages of ec_moe_backward: 0 weight transposes (bf16: W2, W1, W3 and the
- *   shared experts' weights, so that the dA and dX products read K-contiguous
- *   weights; empty for fp32), 1 dY gather + gate gradient, 2 dA grouped GEMM +
- *   SwiGLU backward, 3 dW2, 4 dXe, 5 dW1/dW3, 6 router dZ, 7 router dX,
- *   8 shared dA + SwiGLU backward, 9 shared dW2, 10 shared dX, 11 shared
- *   dW1/dW3 (8-11 empty without shared experts), 12 combine of dXe, 13 dWg.
+ * Stages of ec_moe_backward: 0 dY gather + gate gradient, 1 dA grouped GEMM +
+ *   SwiGLU backward, 2 dW2, 3 dXe, 4 dW1/dW3, 5 router dZ, 6 router dX,
+ *   7 shared dA + SwiGLU backward, 8 shared dW2, 9 shared dX, 10 shared
+ *   dW1/dW3 (7-10 empty without shared experts), 11 combine of dXe, 12 dWg.
  * Stages of ec_route: 0 router+softmax, 1 top-k.                              */
 int ec_set_stage_events(hipEvent_t *events /* HOST array */, int n_events);
 

@@ -42,7 +42,8 @@ class _Problem(ctypes.Structure):
 
 class _SavedLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in ("S", "sel_token", "slot", "Xe", "H1", "H3", "A",
-                                               "O", "Hs1", "Hs3", "As", "total")]
+                                               "O", "Hs1", "Hs3", "As", "W2T", "W13T", "Ws2T",
+                                               "Ws13T", "total")]
 
 
 _lib = None
@@ -401,9 +402,9 @@ class TcLayer:
 
 FORWARD_STAGES = ("router", "topk", "gather", "gemm_w13_swiglu", "gemm_w2", "shared_w13_swiglu",
                   "shared_w2", "combine")
-BACKWARD_STAGES = ("weight_transpose", "bwd_gather", "gemm_dA_swiglu_bwd", "gemm_dW2",
-                   "gemm_dXe", "gemm_dW13", "router_dz", "router_dx", "shared_dA_swiglu_bwd",
-                   "shared_dW2", "shared_dX", "shared_dW13", "bwd_combine", "router_dwg")
+BACKWARD_STAGES = ("bwd_gather", "gemm_dA_swiglu_bwd", "gemm_dW2", "gemm_dXe", "gemm_dW13",
+                   "router_dz", "router_dx", "shared_dA_swiglu_bwd", "shared_dW2", "shared_dX",
+                   "shared_dW13", "bwd_combine", "router_dwg")
 
 
 class StageEvents:

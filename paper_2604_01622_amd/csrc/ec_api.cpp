@@ -124,6 +124,13 @@ struct Saved {
   void* Hs1;      // shared experts, [N, hs] each (null when there are none)
   void* Hs3;
   void* As;
+  // bf16 training only: the weights transposed, written by the forward's
+  // products as their tiles pass through LDS, read K-contiguous by the
+  // backward's dA and dX products (null otherwise)
+  void* W2T;      // [E, h, d]
+  void* W13T;     // [E, d, 2h]: row k = W1[:, k], then W3[:, k]
+  void* Ws2T;     // [hs, d]
+  void* Ws13T;    // [d, 2 hs]
 };
 
 Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
@@ -140,6 +147,11 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
   s.Hs1 = (with_h && sh) ? c.take(sh) : nullptr;
   s.Hs3 = (with_h && sh) ? c.take(sh) : nullptr;
   s.As = sh ? c.take(sh) : nullptr;
+  const bool wt = with_h && P.dtype == EC_BF16;
+  s.W2T = wt ? c.take((size_t)P.E * P.h * P.d * 2) : nullptr;
+  s.W13T = wt ? c.take((size_t)P.E * P.d * 2 * P.h * 2) : nullptr;
+  s.Ws2T = (wt && P.hs) ? c.take((size_t)P.hs * P.d * 2) : nullptr;
+  s.Ws13T = (wt && P.hs) ? c.take((size_t)P.d * 2 * P.hs * 2) : nullptr;
   return s;
 }
 
@@ -154,12 +166,6 @@ struct BwdWs {
   void* dHs;      // [N, 2 hs] shared experts' dH1 | dH3
   float* spart;   // split-K partials of the shared weight gradients
   int s_splits2, s_splits13;
-  // bf16 only: the weights transposed so that the dA and dX products read them
-  // K-contiguous
-  void* W2T;      // [E, h, d]
-  void* W13T;     // [E, d, 2h]: row n = column n of W1, then of W3
-  void* Ws2T;     // [hs, d]
-  void* Ws13T;    // [d, 2 hs]
 };
 
 BwdWs carve_bwd(Carve& c, const Plan& P) {
@@ -180,15 +186,6 @@ BwdWs carve_bwd(Carve& c, const Plan& P) {
     w.s_splits13 = ec::wgrad_splits(2 * P.hs, P.d, P.N);
     const size_t a = (size_t)w.s_splits2 * P.d * P.hs, b = (size_t)w.s_splits13 * 2 * P.hs * P.d;
     if (P.dtype == EC_BF16) w.spart = (float*)c.take((a > b ? a : b) * 4);
-  }
-  w.W2T = w.W13T = w.Ws2T = w.Ws13T = nullptr;
-  if (P.dtype == EC_BF16) {
-    w.W2T = c.take((size_t)P.E * P.h * P.d * 2);
-    w.W13T = c.take((size_t)P.E * P.d * 2 * P.h * 2);
-    if (P.hs) {
-      w.Ws2T = c.take((size_t)P.hs * P.d * 2);
-      w.Ws13T = c.take((size_t)P.d * 2 * P.hs * 2);
-    }
   }
   return w;
 }
@@ -429,6 +426,10 @@ int ec_saved_layout_of(const ec_problem* p, ec_saved_layout* out) {
   out->Hs1 = off(s.Hs1);
   out->Hs3 = off(s.Hs3);
   out->As = off(s.As);
+  out->W2T = off(s.W2T);
+  out->W13T = off(s.W13T);
+  out->Ws2T = off(s.Ws2T);
+  out->Ws13T = off(s.Ws13T);
   out->total = m.used;
   return EC_OK;
 }
@@ -556,17 +557,18 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
   const int M = (int)P.K;
   EC_HIP(ec::launch_gather(P.dtype, X, s.sel, s.Xe, (long)P.E * M, P.d, P.N, stream));
   EC_HIP(mark(3, stream));
-  EC_HIP(ec::launch_gemm_w13(P.dtype, s.Xe, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream));
+  EC_HIP(ec::launch_gemm_w13(P.dtype, s.Xe, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
+                             false, s.W13T));
   EC_HIP(mark(4, stream));
-  EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream));
+  EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream, false, s.W2T));
   EC_HIP(mark(5, stream));
   if (P.hs) {
     // shared experts on every token; their output goes to Y and the combine adds
     // the routed sum to it
     EC_HIP(ec::launch_gemm_w13(P.dtype, X, Ws1, Ws3, s.As, s.Hs1, s.Hs3, 1, P.N, P.d, P.hs,
-                               stream, true));
+                               stream, true, s.Ws13T));
     EC_HIP(mark(6, stream));
-    EC_HIP(ec::launch_gemm_w2(P.dtype, s.As, Ws2, Y, 1, P.N, P.d, P.hs, stream, true));
+    EC_HIP(ec::launch_gemm_w2(P.dtype, s.As, Ws2, Y, 1, P.N, P.d, P.hs, stream, true, s.Ws2T));
   } else {
     EC_HIP(mark(6, stream));
   }
@@ -617,52 +619,36 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   const int M = (int)P.K;
   const int E = P.E, d = P.d, h = P.h, N = P.N, hs = P.hs;
   void* dXe = w.dO;  // dO is dead once dW2 is formed
+  // bf16: dA = dO W2 and dXe = dH1 W1 + dH3 W3 read the transposed weights
+  // that the forward's products wrote into `saved`
   EC_HIP(mark(0, stream));
-  if (P.dtype == EC_BF16) {
-    // the weights read K-major by dA = dO W2 and dXe = dH1 W1 + dH3 W3, transposed
-    // once per call so that both products read K-contiguous operands
-    if (M > 0) {
-      EC_HIP(ec::launch_transpose_bf16(W2, E, d, h, (long)d * h, w.W2T, d, (long)h * d, stream));
-      EC_HIP(ec::launch_transpose_bf16(W1, E, h, d, (long)h * d, w.W13T, 2 * h,
-                                       (long)d * 2 * h, stream));
-      EC_HIP(ec::launch_transpose_bf16(W3, E, h, d, (long)h * d, (uint16_t*)w.W13T + h, 2 * h,
-                                       (long)d * 2 * h, stream));
-    }
-    if (hs && N > 0) {
-      EC_HIP(ec::launch_transpose_bf16(Ws2, 1, d, hs, 0, w.Ws2T, d, 0, stream));
-      EC_HIP(ec::launch_transpose_bf16(Ws1, 1, hs, d, 0, w.Ws13T, 2 * hs, 0, stream));
-      EC_HIP(ec::launch_transpose_bf16(Ws3, 1, hs, d, 0, (uint16_t*)w.Ws13T + hs, 2 * hs, 0,
-                                       stream));
-    }
-  }
-  EC_HIP(mark(1, stream));
   EC_HIP(ec::launch_bwd_gather(P.dtype, dY, s.O, s.S, s.sel, w.dO, w.dSp, N, E, M, d, stream));
-  EC_HIP(mark(2, stream));
+  EC_HIP(mark(1, stream));
   EC_HIP(ec::launch_gemm_dA(P.dtype, w.dO, W2, s.H1, s.H3, w.dH, E, M, d, h, stream, false,
-                            w.W2T));
-  EC_HIP(mark(3, stream));
+                            s.W2T));
+  EC_HIP(mark(2, stream));
   EC_HIP(ec::launch_gemm_dW2(P.dtype, w.dO, s.A, dW2, E, M, d, h, stream));
+  EC_HIP(mark(3, stream));
+  EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream, false, s.W13T));
   EC_HIP(mark(4, stream));
-  EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream, false, w.W13T));
-  EC_HIP(mark(5, stream));
   EC_HIP(ec::launch_gemm_dW13(P.dtype, w.dH, s.Xe, dW1, dW3, E, M, d, h, stream));
-  EC_HIP(mark(6, stream));
+  EC_HIP(mark(5, stream));
   EC_HIP(ec::launch_router_dz(s.S, w.dSp, s.slot, w.dZ, w.dZb, N, E, P.EP, M,
                               p->inv_temperature, stream));
-  EC_HIP(mark(7, stream));
+  EC_HIP(mark(6, stream));
   const void* dZop = P.dtype == EC_BF16 ? (const void*)w.dZb : (const void*)w.dZ;
   EC_HIP(ec::launch_router_dx(P.dtype, dZop, Wg, dX, N, E, P.EP, d, stream));
-  EC_HIP(mark(8, stream));
+  EC_HIP(mark(7, stream));
   if (hs && N > 0) {
     // shared experts: their output gradient is dY itself (no gate)
     EC_HIP(ec::launch_gemm_dA(P.dtype, dY, Ws2, s.Hs1, s.Hs3, w.dHs, 1, N, d, hs, stream, true,
-                              w.Ws2T));
-    EC_HIP(mark(9, stream));
+                              s.Ws2T));
+    EC_HIP(mark(8, stream));
     EC_HIP(ec::launch_shared_dW2(P.dtype, dY, s.As, dWs2, N, d, hs, w.spart, w.s_splits2, stream));
-    EC_HIP(mark(10, stream));
+    EC_HIP(mark(9, stream));
     EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dHs, Ws1, Ws3, dX, 1, N, d, hs, stream, true,
-                               w.Ws13T));
-    EC_HIP(mark(11, stream));
+                               s.Ws13T));
+    EC_HIP(mark(10, stream));
     EC_HIP(ec::launch_shared_dW13(P.dtype, w.dHs, X, dWs1, dWs3, N, d, hs, w.spart,
                                   w.s_splits13, stream));
   } else {
@@ -671,15 +657,15 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
       EC_HIP(ec::launch_zero(dWs3, (size_t)hs * d * P.esz, stream));
       EC_HIP(ec::launch_zero(dWs2, (size_t)hs * d * P.esz, stream));
     }
+    EC_HIP(mark(8, stream));
     EC_HIP(mark(9, stream));
     EC_HIP(mark(10, stream));
-    EC_HIP(mark(11, stream));
   }
-  EC_HIP(mark(12, stream));
+  EC_HIP(mark(11, stream));
   EC_HIP(ec::launch_bwd_combine(P.dtype, dXe, s.slot, dX, dX, N, E, M, d, stream));
-  EC_HIP(mark(13, stream));
+  EC_HIP(mark(12, stream));
   EC_HIP(ec::launch_router_dwg(P.dtype, dZop, X, dWg, w.part, w.splits, N, E, P.EP, d, stream));
-  EC_HIP(mark(14, stream));
+  EC_HIP(mark(13, stream));
   return EC_OK;
 }
 

@@ -72,15 +72,18 @@ int router_dwg_splits(int N, int E, int d);
 
 // H = Xe W1^T, Xe W3^T -> A = SiLU(H1) * H3 (and H1, H3 if non-null).
 // `shared`: the same product for the shared experts (own kernel symbol).
+// W13T (bf16, may be null): also written, [E, d, 2h], row k = W1[:, k] then
+// W3[:, k] (the transposed weights the backward's dX product reads).
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
-                           bool shared = false);
-// O = A W2^T.
+                           bool shared = false, void* W13T = nullptr);
+// O = A W2^T.  W2T (bf16, may be null): also written, [E, h, d] = W2 transposed
+// (what the backward's dA product reads).
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
-                          int h, hipStream_t st, bool shared = false);
+                          int h, hipStream_t st, bool shared = false, void* W2T = nullptr);
 // dA = dO W2 and the SwiGLU backward: dH[:, 0:h] = dH1, dH[:, h:2h] = dH3 ([E,M,2h]).
-// W2T (bf16, may be null): W2 transposed, [E, h, d]; the product then reads
-// K-contiguous weights.
+// W2T (bf16, may be null): W2 transposed, [E, h, d] (as launch_gemm_w2 writes
+// it); the product then reads K-contiguous weights.
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
                           bool shared = false, const void* W2T = nullptr);
@@ -147,9 +150,6 @@ hipError_t launch_gemm_w2_var(int dtype, const void* A, const void* W2, void* O,
 
 // Fill n int32/fp32/bytes with zero (a kernel, not a memset node).
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t st);
-// dst[b][c][r] = src[b][r][c] for B bf16 matrices of R x C (R, C multiples of
-// 64); src_bs / dst_bs elements per matrix, dst rows of ldd elements.
-hipError_t launch_transpose_bf16(const void* src, int B, int R, int C, long src_bs, void* dst,
-                                 int ldd, long dst_bs, hipStream_t st);
+
 
 }  // namespace ec

@@ -63,6 +63,14 @@ struct GemmParams {
   void* H3;
   long h_bs;
   int ldh;
+  // bf16 with K-contiguous B only (may be null): B transposed, written while its
+  // tiles pass through LDS, BT[e*bt_bs + k*ldbt + n] = B(n, k) (SwiGLU: W3's
+  // rows go to columns bt_split + n).  Row block mt writes the k-steps kt with
+  // kt % MT == mt of its column block, so each element is written once.
+  void* BT;
+  long bt_bs;
+  int ldbt;
+  int bt_split;
   // Variable rows per batch (token choice): batch e owns rows
   // [var_rows[e], var_rows[e+1]) of A, C and H (row strides lda, ldc, ldh) and
   // tiles [var_tiles[e], var_tiles[e+1]) of the launch; both device arrays of
@@ -74,7 +82,7 @@ struct GemmParams {
 // Where one output tile sits: batch, row and column block, the batch's rows,
 // and the element offsets of the batch in A, C and H.
 struct TileCoord {
-  int e, mt, nt, M;
+  int e, mt, nt, M, MT;
   size_t a_off, c_off, h_off;
 };
 
@@ -132,7 +140,7 @@ __device__ __forceinline__ int kc_swz(int row) {
 __device__ __forceinline__ int km_swz(int k) { return (k & 3) << 2; }
 
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32>
+          bool OUT_F32, bool WBT>
 __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoord& tc,
                                               char* smem) {
   constexpr int NT = 64 * WGM * WGN;
@@ -345,6 +353,46 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
                                                               acc[mi][ni], 0, 0, 0);
     }
   };
+  // The B tile of k-step kt (BN rows of KSTEP k, K-contiguous in LDS) written
+  // out transposed: each wave moves blocks of 32 rows x 16 k, two transposing
+  // reads (lane i gets k = kb + i of four rows each) and one 16-byte store of
+  // eight consecutive rows per lane.
+  auto write_bt = [&](int kt, int stage) {
+    if constexpr (WBT && B_KC && !OUT_F32) {
+      const char* sb = smem + stage * STAGE_BYTES + OA::BYTES;
+      bf16_t* bt = reinterpret_cast<bf16_t*>(p.BT) + (size_t)e * p.bt_bs;
+      constexpr int RB = BN / 32, KB = KSTEP / 16, WAVES = NT / 64;
+      static_assert((RB * KB) % WAVES == 0, "whole blocks per wave");
+#pragma unroll
+      for (int i = 0; i < RB * KB / WAVES; ++i) {
+        const int b = wave * (RB * KB / WAVES) + i;
+        const int rb = (b % RB) * 32, kb = (b / RB) * 16;
+        v4i16 v[2];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int n = rb + 8 * g16 + 4 * hf + (j16 >> 2);
+          const int kc = kb + 4 * (j16 & 3);
+          v[hf] = ds_read_tr16(sb + n * (KSTEP * 2) + (((kc >> 3) ^ kc_swz<KSTEP>(n)) << 4) +
+                               (kc & 7) * 2);
+        }
+        const int r0 = rb + 8 * g16;   // first of this lane's eight rows
+        int col;
+        bool ok;
+        if constexpr (EPI == EPI_SWIGLU) {
+          const int nn = n0 + r0 % (BN / 2);
+          col = (r0 < BN / 2 ? 0 : p.bt_split) + nn;
+          ok = nn < p.N;
+        } else {
+          col = n0 + r0;
+          ok = col < p.N;
+        }
+        if (ok)
+          *reinterpret_cast<u32x4*>(bt + (size_t)(kt * KSTEP + kb + j16) * p.ldbt + col) =
+              __builtin_bit_cast(u32x4, v);
+      }
+    }
+  };
+
   // Fragment-read instructions per 16-wide k step (a K-major fragment takes
   // two).  Inside a stage the MFMAs on the current fragments alternate with
   // the reads of the next ones (one MFMA, one read, ...).  At a stage end: half
@@ -357,6 +405,9 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   auto kstep = [&](int kt, auto refill) {
     constexpr bool RF = decltype(refill)::value;
     const int stage = kt % STAGES;
+    if constexpr (WBT) {
+      if (kt % tc.MT == mt) write_bt(kt, stage);
+    }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int cur = kk & 1;
@@ -528,7 +579,7 @@ constexpr int dma_smem_bytes() {
 // One output tile per workgroup; consecutive tile ids (same expert) are kept
 // on one XCD so that its L2 serves their shared A rows and B columns.
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32, int TAG>
+          bool OUT_F32, int TAG, bool WBT>
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024)))
   char smem[dma_smem_bytes<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC>()];
@@ -576,18 +627,21 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
   const int gm = (MT - grp * GROUP_M) < GROUP_M ? (MT - grp * GROUP_M) : GROUP_M;
   tc.mt = grp * GROUP_M + in_grp % gm;
   tc.nt = in_grp / gm;
-  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32>(p, tc, smem);
+  tc.MT = MT;
+  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, WBT>(p, tc, smem);
 }
 
+// WBT: the instantiation that also writes B transposed to p.BT (must be set).
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32, int TAG>
+          bool OUT_F32, int TAG, bool WBT = false>
 hipError_t run_dma(GemmParams p, hipStream_t st) {
+  if (WBT != (p.BT != nullptr)) return hipErrorInvalidValue;
   p.MT = (p.M + BM - 1) / BM;
   p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
   const long ntile = (long)p.batches * p.MT * p.NT;
   if (ntile == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
-  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG>
+  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, WBT>
       <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
   return hipGetLastError();
 }
@@ -602,7 +656,7 @@ hipError_t run_dma_var(GemmParams p, long max_rows, hipStream_t st) {
   const long ntile = ((max_rows + BM - 1) / BM + p.batches) * p.NT;
   if (ntile == 0 || p.batches == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
-  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG>
+  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, false>
       <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
   return hipGetLastError();
 }
@@ -751,28 +805,40 @@ __global__ void splitk_store_kernel(const float* __restrict__ part, int splits, 
 
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
-                           bool shared) {
+                           bool shared, void* W13T) {
   GemmParams p = base_params();
   p.A = Xe; p.a_bs = (long)M * d; p.lda = d;
   p.B = W1; p.B2 = W3; p.b_bs = (long)h * d; p.ldb = d;
   p.M = M; p.N = h; p.K = d; p.kv_a = d; p.kv_b = d; p.batches = E;
   p.C = A; p.c_bs = (long)M * h; p.ldc = h;
   p.H1 = H1; p.H3 = H3; p.h_bs = (long)M * h; p.ldh = h;
+  p.BT = W13T; p.bt_bs = (long)d * 2 * h; p.ldbt = 2 * h; p.bt_split = h;   // [E, d, 2h]
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU>(p, 1, 1, st);
+  if (W13T) {
+    if (shared)
+      return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13, true>(p, st);
+    return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, true>(p, st);
+  }
   if (shared) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13>(p, st);
   return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
 }
 
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
-                          int h, hipStream_t st, bool shared) {
+                          int h, hipStream_t st, bool shared, void* W2T) {
   GemmParams p = base_params();
   p.A = A; p.a_bs = (long)M * h; p.lda = h;
   p.B = W2; p.b_bs = (long)d * h; p.ldb = h;
   p.M = M; p.N = d; p.K = h; p.kv_a = h; p.kv_b = h; p.batches = E;
   p.C = O; p.c_bs = (long)M * d; p.ldc = d;
+  p.BT = W2T; p.bt_bs = (long)h * d; p.ldbt = d;   // [E, h, d]
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
+  if (W2T) {
+    if (shared)
+      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2, true>(p, st);
+    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2, true>(p, st);
+  }
   if (shared) return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
 }

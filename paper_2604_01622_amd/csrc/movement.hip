@@ -303,44 +303,6 @@ __global__ void zero_kernel(uint4* p, size_t n16, unsigned char* tail, size_t nt
   if (blockIdx.x == 0 && threadIdx.x < ntail) tail[threadIdx.x] = 0;
 }
 
-// ---------------------------------------------------------------- transpose
-// dst[b][c][r] = src[b][r][c] for a batch of R x C bf16 matrices (R, C
-// multiples of 64; src rows of C elements, src_bs elements per matrix; dst
-// rows of ldd elements, dst_bs per matrix).  One wave per 64 x 64 tile; each
-// lane moves an 8 x 8 block through its registers: eight 16-byte row loads,
-// eight 16-byte column stores (8 lanes cover 128 contiguous bytes of a row on
-// both sides).
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ src,
-                                                             long src_bs, int C,
-                                                             uint16_t* __restrict__ dst,
-                                                             long dst_bs, int ldd, int tiles_r,
-                                                             int tiles_c, long n_tiles) {
-  const long tile = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (tile >= n_tiles) return;
-  const int lane = threadIdx.x & 63;
-  const long per_b = (long)tiles_r * tiles_c;
-  const long b = tile / per_b;
-  const int rem = (int)(tile - b * per_b);
-  const int r0 = (rem / tiles_c) * 64 + (lane >> 3) * 8;
-  const int c0 = (rem % tiles_c) * 64 + (lane & 7) * 8;
-  const uint16_t* sp = src + b * src_bs + (size_t)r0 * C + c0;
-  uint4 in[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) in[q] = *reinterpret_cast<const uint4*>(sp + (size_t)q * C);
-  uint16_t* dp = dst + b * dst_bs + (size_t)c0 * ldd + r0;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    // column c0 + j of rows r0 .. r0 + 7: half j of every loaded row
-    uint32_t w[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t a = (&in[2 * q].x)[j >> 1], b2 = (&in[2 * q + 1].x)[j >> 1];
-      w[q] = (j & 1) ? ((a >> 16) | (b2 & 0xffff0000u)) : ((a & 0xffffu) | (b2 << 16));
-    }
-    *reinterpret_cast<uint4*>(dp + (size_t)j * ldd) = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-}
-
 }  // namespace
 
 hipError_t launch_gather(int dtype, const void* X, const int32_t* sel_token, void* Xe, long rows,
@@ -423,17 +385,6 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t st) {
   if (blocks > 4096) blocks = 4096;
   if (blocks == 0) blocks = 1;
   zero_kernel<<<(unsigned)blocks, 256, 0, st>>>((uint4*)p, n16, (unsigned char*)p + n16 * 16, ntail);
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_bf16(const void* src, int B, int R, int C, long src_bs, void* dst,
-                                 int ldd, long dst_bs, hipStream_t st) {
-  if (R % 64 || C % 64 || B < 0) return hipErrorInvalidValue;
-  const int tr = R / 64, tc = C / 64;
-  const long n = (long)B * tr * tc;
-  if (n == 0) return hipSuccess;
-  transpose_bf16_kernel<<<(unsigned)((n + 3) / 4), 256, 0, st>>>(
-      (const uint16_t*)src, src_bs, C, (uint16_t*)dst, dst_bs, ldd, tr, tc, n);
   return hipGetLastError();
 }
 
