@@ -312,7 +312,8 @@ def backward(X, Wg, W1, W3, W2, dY, saved, group_offsets, capacity, inv_temperat
 
 
 def saved_views(saved: torch.Tensor, P: Problem) -> dict:
-    """Typed views into a saved-activation buffer (S, sel_token, slot, Xe, H1, H3, A, O)."""
+    """Typed views into a saved-activation buffer (S, sel_token, slot, Xe, H1, H3, A, O, the
+    shared experts' activations, and for bf16 the transposed weights)."""
     lay = P.saved_layout()
     N, d, E, h, K = P.c.n_tokens, P.c.d_model, P.c.n_experts, P.c.d_ff, P.K
     dt = P.dtype
@@ -322,7 +323,7 @@ def saved_views(saved: torch.Tensor, P: Problem) -> dict:
         n = int(np.prod(shape))
         return saved[off:off + n * esize].view(dtype).view(*shape)
 
-    return {"S": view(lay["S"], (N, E), torch.float32, 4),
+    out = {"S": view(lay["S"], (N, E), torch.float32, 4),
             "sel_token": view(lay["sel_token"], (E, K), torch.int32, 4),
             "slot": view(lay["slot"], (E, N), torch.int32, 4),
             "Xe": view(lay["Xe"], (E, K, d), dt, es), "H1": view(lay["H1"], (E, K, h), dt, es),
@@ -331,6 +332,14 @@ def saved_views(saved: torch.Tensor, P: Problem) -> dict:
             "Hs1": view(lay["Hs1"], (N, P.c.d_shared), dt, es),
             "Hs3": view(lay["Hs3"], (N, P.c.d_shared), dt, es),
             "As": view(lay["As"], (N, P.c.d_shared), dt, es)}
+    if dt == torch.bfloat16:   # the transposed weights the training forward writes
+        hs = P.c.d_shared
+        out["W2T"] = view(lay["W2T"], (E, h, d), dt, es)
+        out["W13T"] = view(lay["W13T"], (E, d, 2 * h), dt, es)
+        if hs:
+            out["Ws2T"] = view(lay["Ws2T"], (hs, d), dt, es)
+            out["Ws13T"] = view(lay["Ws13T"], (d, 2 * hs), dt, es)
+    return out
 
 
 class Layer:
