@@ -138,7 +138,9 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
   s.S = (float*)c.take((size_t)P.N * P.E * 4);
   s.sel = (int32_t*)c.take((size_t)P.E * P.K * 4);
   s.slot = (int32_t*)c.take((size_t)P.E * P.N * 4);
-  s.Xe = c.take((size_t)P.E * P.K * P.d * P.esz);
+  // bf16 inference reads the selected rows of X inside the W1/W3 product and
+  // needs no gathered copy
+  s.Xe = (with_h || P.dtype != EC_BF16) ? c.take((size_t)P.E * P.K * P.d * P.esz) : nullptr;
   s.H1 = with_h ? c.take((size_t)P.E * P.K * P.h * P.esz) : nullptr;
   s.H3 = with_h ? c.take((size_t)P.E * P.K * P.h * P.esz) : nullptr;
   s.A = c.take((size_t)P.E * P.K * P.h * P.esz);
@@ -322,7 +324,7 @@ TcFwdWs carve_tc_fwd(Carve& c, const Plan& P, long rmax) {
   w.slot = (int32_t*)c.take((size_t)P.E * P.N * 4);
   w.rows = (int32_t*)c.take((size_t)(P.E + 1) * 4);
   w.sel = (int32_t*)c.take((size_t)rmax * 4);
-  w.Xe = c.take((size_t)rmax * P.d * P.esz);
+  w.Xe = P.dtype == EC_BF16 ? nullptr : c.take((size_t)rmax * P.d * P.esz);   // fp32 only
   w.A = c.take((size_t)rmax * P.h * P.esz);
   w.O = c.take((size_t)rmax * P.d * P.esz);
   w.As = P.hs ? c.take((size_t)P.N * P.hs * P.esz) : nullptr;
@@ -555,10 +557,18 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
   }
   EC_TRY(enqueue_route(p, P, X, Wg, s.S, ST, s.sel, nullptr, s.slot, stream));
   const int M = (int)P.K;
-  EC_HIP(ec::launch_gather(P.dtype, X, s.sel, s.Xe, (long)P.E * M, P.d, P.N, stream));
-  EC_HIP(mark(3, stream));
-  EC_HIP(ec::launch_gemm_w13(P.dtype, s.Xe, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
-                             false, s.W13T));
+  if (P.dtype == EC_BF16) {
+    // the W1/W3 product reads the selected rows of X itself (the gather stage is
+    // empty); for the backward it also writes them out as Xe
+    EC_HIP(mark(3, stream));
+    EC_HIP(ec::launch_gemm_w13(P.dtype, X, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
+                               false, s.W13T, s.sel, saved ? s.Xe : nullptr));
+  } else {
+    EC_HIP(ec::launch_gather(P.dtype, X, s.sel, s.Xe, (long)P.E * M, P.d, P.N, stream));
+    EC_HIP(mark(3, stream));
+    EC_HIP(ec::launch_gemm_w13(P.dtype, s.Xe, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
+                               false, s.W13T));
+  }
   EC_HIP(mark(4, stream));
   EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream, false, s.W2T));
   EC_HIP(mark(5, stream));
@@ -753,10 +763,17 @@ int ec_tc_forward(const ec_problem* p, int32_t top_k, const void* X, const void*
   const TcFwdWs w = carve_tc_fwd(c, P, rmax);
   int32_t* rows = expert_rows ? expert_rows : w.rows;
   EC_TRY(enqueue_tc_route(p, P, top_k, X, Wg, w.S, w.G, w.slot, rows, w.sel, rw, stream));
-  EC_HIP(ec::launch_gather(P.dtype, X, w.sel, w.Xe, rmax, P.d, P.N, stream, rows + P.E));
-  EC_HIP(mark(3, stream));
-  EC_HIP(ec::launch_gemm_w13_var(P.dtype, w.Xe, W1, W3, w.A, P.E, rows, rw.tiles13, rmax, rmax_e,
-                                 P.d, P.h, stream));
+  if (P.dtype == EC_BF16) {
+    // the W1/W3 product reads the kept rows of X itself (empty gather stage)
+    EC_HIP(mark(3, stream));
+    EC_HIP(ec::launch_gemm_w13_var(P.dtype, X, W1, W3, w.A, P.E, rows, rw.tiles13, rmax, rmax_e,
+                                   P.d, P.h, stream, w.sel));
+  } else {
+    EC_HIP(ec::launch_gather(P.dtype, X, w.sel, w.Xe, rmax, P.d, P.N, stream, rows + P.E));
+    EC_HIP(mark(3, stream));
+    EC_HIP(ec::launch_gemm_w13_var(P.dtype, w.Xe, W1, W3, w.A, P.E, rows, rw.tiles13, rmax,
+                                   rmax_e, P.d, P.h, stream));
+  }
   EC_HIP(mark(4, stream));
   EC_HIP(ec::launch_gemm_w2_var(P.dtype, w.A, W2, w.O, P.E, rows, rw.tiles2, rmax, rmax_e, P.d,
                                 P.h, stream));

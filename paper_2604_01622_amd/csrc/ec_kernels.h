@@ -74,9 +74,13 @@ int router_dwg_splits(int N, int E, int d);
 // `shared`: the same product for the shared experts (own kernel symbol).
 // W13T (bf16, may be null): also written, [E, d, 2h], row k = W1[:, k] then
 // W3[:, k] (the transposed weights the backward's dX product reads).
+// rows (bf16 routed experts, may be null): Xe is then X itself and row m of
+// expert e reads X[rows[e M + m]] (the gather happens in the operand load);
+// XeOut (may be null): the gathered rows are also written there, [E, M, d].
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
-                           bool shared = false, void* W13T = nullptr);
+                           bool shared = false, void* W13T = nullptr,
+                           const int32_t* rows = nullptr, void* XeOut = nullptr);
 // O = A W2^T.  W2T (bf16, may be null): also written, [E, h, d] = W2 transposed
 // (what the backward's dA product reads).
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
@@ -141,9 +145,11 @@ hipError_t launch_tc_offsets(const int32_t* cnt, int G, int E, int bm, int nt13,
 hipError_t launch_tc_place(int32_t* slotT, float* G, int N, int E, const GroupTable& tab, int g0,
                            const int32_t* seg, int32_t* sel, hipStream_t st);
 // The forward products over packed rows: expert e owns rows [rows[e], rows[e+1]).
+// sel (bf16, may be null): Xe is then X itself and packed row r reads X[sel[r]].
 hipError_t launch_gemm_w13_var(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                                int E, const int32_t* rows, const int32_t* tiles, long max_rows,
-                               int max_rows_per_expert, int d, int h, hipStream_t st);
+                               int max_rows_per_expert, int d, int h, hipStream_t st,
+                               const int32_t* sel = nullptr);
 hipError_t launch_gemm_w2_var(int dtype, const void* A, const void* W2, void* O, int E,
                               const int32_t* rows, const int32_t* tiles, long max_rows,
                               int max_rows_per_expert, int d, int h, hipStream_t st);

@@ -40,6 +40,12 @@ struct GemmParams {
   const void* A;
   long a_bs;
   int lda;
+  // bf16 K-contiguous A only (may be null): row m of batch e is row
+  // a_rows[e*a_rows_bs + r0 + m] of A itself (r0: the batch's first packed row
+  // with var_rows, else 0), so the gather of the selected tokens happens in the
+  // operand load
+  const int32_t* a_rows;
+  long a_rows_bs;
   // B operand, element (n, k) of batch e:
   //   K-contiguous:  B[e*b_bs + n*ldb + k]  (SwiGLU: rows of W1 and W3 side by side)
   //   N-contiguous:  B[e*b_bs + k*ldb + n]; the fp32 kernel reads rows k >= k_split
@@ -71,6 +77,12 @@ struct GemmParams {
   long bt_bs;
   int ldbt;
   int bt_split;
+  // bf16 K-contiguous A only (may be null): A copied out as its tiles pass through
+  // LDS, AC[e*ac_bs + m*ldac + k] = A(m, k) for m < M (with a_rows: the gathered
+  // rows).  Column block nt writes the k-steps kt with kt % NT == nt.
+  void* AC;
+  long ac_bs;
+  int ldac;
   // Variable rows per batch (token choice): batch e owns rows
   // [var_rows[e], var_rows[e+1]) of A, C and H (row strides lda, ldc, ldh) and
   // tiles [var_tiles[e], var_tiles[e+1]) of the launch; both device arrays of
@@ -82,7 +94,7 @@ struct GemmParams {
 // Where one output tile sits: batch, row and column block, the batch's rows,
 // and the element offsets of the batch in A, C and H.
 struct TileCoord {
-  int e, mt, nt, M, MT;
+  int e, mt, nt, M, MT, NT, row0;
   size_t a_off, c_off, h_off;
 };
 
@@ -139,8 +151,10 @@ __device__ __forceinline__ int kc_swz(int row) {
 }
 __device__ __forceinline__ int km_swz(int k) { return (k & 3) << 2; }
 
+// COPY bit 1: write B transposed to p.BT; bit 2: copy A to p.AC (both bf16,
+// K-contiguous operands; see GemmParams).
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32, bool WBT>
+          bool OUT_F32, int COPY>
 __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoord& tc,
                                               char* smem) {
   constexpr int NT = 64 * WGM * WGN;
@@ -185,7 +199,12 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       const int row = id / OA::CPR, lc = (id % OA::CPR) ^ kc_swz<KSTEP>(row);
       int r = m0 + row;
       r = r < M ? r : M - 1;
-      a_src[q] = Ab + (size_t)r * p.lda + lc * 8;
+      if (p.a_rows) {
+        const int tok = p.a_rows[(size_t)e * p.a_rows_bs + tc.row0 + r];
+        a_src[q] = reinterpret_cast<const bf16_t*>(p.A) + (size_t)tok * p.lda + lc * 8;
+      } else {
+        a_src[q] = Ab + (size_t)r * p.lda + lc * 8;
+      }
     } else {
       const int row = id / OA::CPR, lc = (id % OA::CPR) ^ km_swz(row);
       const int col = m0 + lc * 8;   // first column of the chunk
@@ -358,7 +377,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // reads (lane i gets k = kb + i of four rows each) and one 16-byte store of
   // eight consecutive rows per lane.
   auto write_bt = [&](int kt, int stage) {
-    if constexpr (WBT && B_KC && !OUT_F32) {
+    if constexpr ((COPY & 1) && B_KC && !OUT_F32) {
       const char* sb = smem + stage * STAGE_BYTES + OA::BYTES;
       bf16_t* bt = reinterpret_cast<bf16_t*>(p.BT) + (size_t)e * p.bt_bs;
       constexpr int RB = BN / 32, KB = KSTEP / 16, WAVES = NT / 64;
@@ -393,6 +412,26 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     }
   };
 
+  // The A tile of k-step kt copied out row by row (16-byte chunks; rows past M
+  // are clamped duplicates and are not written).
+  auto write_ac = [&](int kt, int stage) {
+    if constexpr ((COPY & 2) && A_KC && !OUT_F32) {
+      const char* sa = smem + stage * STAGE_BYTES;
+      bf16_t* ac = reinterpret_cast<bf16_t*>(p.AC) + (size_t)e * p.ac_bs;
+      constexpr int CH = KSTEP / 8;
+      static_assert((BM * CH) % NT == 0, "whole chunks per thread");
+#pragma unroll
+      for (int i = 0; i < BM * CH / NT; ++i) {
+        const int id = i * NT + tid;
+        const int row = id / CH, c = id % CH;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(sa + row * (KSTEP * 2) +
+                                                        ((c ^ kc_swz<KSTEP>(row)) << 4));
+        if (m0 + row < M)
+          *reinterpret_cast<u32x4*>(ac + (size_t)(m0 + row) * p.ldac + kt * KSTEP + c * 8) = v;
+      }
+    }
+  };
+
   // Fragment-read instructions per 16-wide k step (a K-major fragment takes
   // two).  Inside a stage the MFMAs on the current fragments alternate with
   // the reads of the next ones (one MFMA, one read, ...).  At a stage end: half
@@ -405,8 +444,11 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   auto kstep = [&](int kt, auto refill) {
     constexpr bool RF = decltype(refill)::value;
     const int stage = kt % STAGES;
-    if constexpr (WBT) {
+    if constexpr (COPY & 1) {
       if (kt % tc.MT == mt) write_bt(kt, stage);
+    }
+    if constexpr (COPY & 2) {
+      if (kt % tc.NT == nt) write_ac(kt, stage);
     }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
@@ -579,7 +621,7 @@ constexpr int dma_smem_bytes() {
 // One output tile per workgroup; consecutive tile ids (same expert) are kept
 // on one XCD so that its L2 serves their shared A rows and B columns.
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32, int TAG, bool WBT>
+          bool OUT_F32, int TAG, int COPY>
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024)))
   char smem[dma_smem_bytes<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC>()];
@@ -601,6 +643,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
     }
     const int row0 = p.var_rows[lo];
     tc.e = lo;
+    tc.row0 = row0;
     tc.M = p.var_rows[lo + 1] - row0;
     MT = (tc.M + BM - 1) / BM;
     rem = t - p.var_tiles[lo];
@@ -612,6 +655,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
     if (t >= p.batches * p.MT * p.NT) return;
     const int per_b = p.MT * p.NT;
     tc.e = t / per_b;
+    tc.row0 = 0;
     tc.M = p.M;
     MT = p.MT;
     rem = t - tc.e * per_b;
@@ -628,20 +672,23 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
   tc.mt = grp * GROUP_M + in_grp % gm;
   tc.nt = in_grp / gm;
   tc.MT = MT;
-  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, WBT>(p, tc, smem);
+  tc.NT = p.NT;
+  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, COPY>(p, tc, smem);
 }
 
-// WBT: the instantiation that also writes B transposed to p.BT (must be set).
+// COPY: the instantiation that also writes B transposed (bit 1, p.BT) and/or
+// copies A out (bit 2, p.AC); the pointers must be set exactly for those bits.
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32, int TAG, bool WBT = false>
+          bool OUT_F32, int TAG, int COPY = 0>
 hipError_t run_dma(GemmParams p, hipStream_t st) {
-  if (WBT != (p.BT != nullptr)) return hipErrorInvalidValue;
+  if (((COPY & 1) != 0) != (p.BT != nullptr) || ((COPY & 2) != 0) != (p.AC != nullptr))
+    return hipErrorInvalidValue;
   p.MT = (p.M + BM - 1) / BM;
   p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
   const long ntile = (long)p.batches * p.MT * p.NT;
   if (ntile == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
-  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, WBT>
+  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, COPY>
       <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
   return hipGetLastError();
 }
@@ -656,7 +703,7 @@ hipError_t run_dma_var(GemmParams p, long max_rows, hipStream_t st) {
   const long ntile = ((max_rows + BM - 1) / BM + p.batches) * p.NT;
   if (ntile == 0 || p.batches == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
-  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, false>
+  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, 0>
       <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
   return hipGetLastError();
 }
@@ -805,22 +852,33 @@ __global__ void splitk_store_kernel(const float* __restrict__ part, int splits, 
 
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
-                           bool shared, void* W13T) {
+                           bool shared, void* W13T, const int32_t* rows, void* XeOut) {
   GemmParams p = base_params();
   p.A = Xe; p.a_bs = (long)M * d; p.lda = d;
+  if (rows) {   // Xe is X itself, row m of expert e is X[rows[e M + m]]
+    p.a_bs = 0; p.a_rows = rows; p.a_rows_bs = M;
+  }
+  p.AC = XeOut; p.ac_bs = (long)M * d; p.ldac = d;
   p.B = W1; p.B2 = W3; p.b_bs = (long)h * d; p.ldb = d;
   p.M = M; p.N = h; p.K = d; p.kv_a = d; p.kv_b = d; p.batches = E;
   p.C = A; p.c_bs = (long)M * h; p.ldc = h;
   p.H1 = H1; p.H3 = H3; p.h_bs = (long)M * h; p.ldh = h;
   p.BT = W13T; p.bt_bs = (long)d * 2 * h; p.ldbt = 2 * h; p.bt_split = h;   // [E, d, 2h]
   if (M == 0) return hipSuccess;
-  if (dtype == DT_F32) return run_f32<EPI_SWIGLU>(p, 1, 1, st);
-  if (W13T) {
-    if (shared)
-      return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13, true>(p, st);
-    return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, true>(p, st);
+  if (dtype == DT_F32) {
+    if (rows || XeOut) return hipErrorInvalidValue;   // fp32 reads a gathered Xe
+    return run_f32<EPI_SWIGLU>(p, 1, 1, st);
   }
-  if (shared) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13>(p, st);
+  if (shared) {
+    if (rows || XeOut) return hipErrorInvalidValue;   // the shared experts read X as is
+    if (W13T)
+      return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13, 1>(p, st);
+    return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13>(p, st);
+  }
+  if (W13T && XeOut)
+    return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, 3>(p, st);
+  if (W13T) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, 1>(p, st);
+  if (XeOut) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, 2>(p, st);
   return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
 }
 
@@ -836,8 +894,8 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
   if (W2T) {
     if (shared)
-      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2, true>(p, st);
-    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2, true>(p, st);
+      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2, 1>(p, st);
+    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2, 1>(p, st);
   }
   if (shared) return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
@@ -1050,9 +1108,14 @@ int tc_col_blocks_w2(int d) { return (d + 255) / 256; }
 
 hipError_t launch_gemm_w13_var(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                                int E, const int32_t* rows, const int32_t* tiles, long max_rows,
-                               int max_rows_per_expert, int d, int h, hipStream_t st) {
+                               int max_rows_per_expert, int d, int h, hipStream_t st,
+                               const int32_t* sel) {
   GemmParams p = base_params();
   p.A = Xe; p.lda = d;
+  if (sel) {   // Xe is X itself, packed row r is X[sel[r]]
+    if (dtype == DT_F32) return hipErrorInvalidValue;
+    p.a_rows = sel; p.a_rows_bs = 0;
+  }
   p.B = W1; p.B2 = W3; p.b_bs = (long)h * d; p.ldb = d;
   p.M = max_rows_per_expert; p.N = h; p.K = d; p.kv_a = d; p.kv_b = d; p.batches = E;
   p.C = A; p.ldc = h; p.ldh = h;
