@@ -7,6 +7,8 @@ Tolerances (stated by the layer's specification, derived for fp32 storage):
     accumulation), <= 1e-4 for fp32 storage (fp32 sums of up to a few
     thousand terms, unit roundoff 6e-8).
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -474,7 +476,8 @@ def test_full_tc_timestep_bf16():
 
 # ------------------------------------------------------------------ randomised shapes
 
-@pytest.mark.parametrize("seed", range(8))
+# EC_RANDOM_CASES / EC_RANDOM_TC_CASES widen the sweeps (defaults 8 and 4)
+@pytest.mark.parametrize("seed", range(int(os.environ.get("EC_RANDOM_CASES", "8"))))
 def test_random_problems(seed):
     rng = np.random.default_rng(1000 + seed)
     G = int(rng.integers(1, 5))
@@ -496,7 +499,7 @@ def test_random_problems(seed):
     full_case(wl)
 
 
-@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("seed", range(int(os.environ.get("EC_RANDOM_TC_CASES", "4"))))
 def test_random_token_choice(seed):
     rng = np.random.default_rng(3000 + seed)
     lens = [int(x) for x in rng.integers(1, 400, size=int(rng.integers(1, 4)))]
