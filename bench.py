@@ -54,10 +54,15 @@ def sources_hash():
 
 
 def stage_of_kernel(name):
-    m = re.search(r"gemm_dma_kernel<.*, (\d+)>\(", name)
+    """Stage of a gemm_dma_kernel instantiation from its stage-tag template argument
+    (the eleventh: BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, OPT)."""
+    m = re.search(r"gemm_dma_kernel<([^>]*)>", name)
     if not m:
         return None
-    tag = int(m.group(1))
+    args = [a.strip() for a in m.group(1).split(",")]
+    if len(args) < 11 or not args[10].isdigit():
+        return None
+    tag = int(args[10])
     return next((k for k, v in GEMM_TAGS.items() if v == tag), None)
 
 
@@ -88,6 +93,8 @@ def traffic_from(fetch_db, write_db, workload):
         st = stage_of_kernel(name)
         if st is None or name not in write:
             continue
+        if st in recs and recs[st]["dispatches"] >= len(vals):
+            continue   # another instantiation of the stage ran more often
         fb = sum(vals) / len(vals) * 1024.0 * f_fetch
         wb = sum(write[name]) / len(write[name]) * 1024.0 * f_write
         recs[st] = {"stage": st, "kernel": name, "fetch_bytes": fb, "write_bytes": wb,
