@@ -10,12 +10,18 @@
 // K advances 64 at a time through a 2-stage LDS ring filled straight from
 // global memory by global_load_lds_dwordx4 (no VGPR staging).  K-contiguous
 // operands sit in LDS as 128-byte rows with XOR-swizzled 16-byte chunks
-// (conflict-free fragment reads); K-major operands (the backward's transposed
-// products) stay K-major in LDS and are read with the transposing
-// ds_read_b64_tr_b16.  The MFMAs of each k-step alternate with the next
-// step's fragment reads (and at a stage end with the refill's DMA, after the
-// barrier), so LDS latency hides behind MFMAs in flight.  Tiles are
+// (conflict-free fragment reads); K-major operands (the weight gradients'
+// token-row contractions) stay K-major in LDS and are read with the
+// transposing ds_read_b64_tr_b16.  The MFMAs of each k-step alternate with the
+// next step's fragment reads (and at a stage end with the refill's DMA, after
+// the barrier), so LDS latency hides behind MFMAs in flight.  Tiles are
 // numbered so that consecutive ones share an expert and stay on one XCD.
+//
+// The W1/W3 product gathers its A rows (the selected tokens) in the operand
+// load.  In the training forward the W1/W3 and W2 products also copy tiles
+// out of LDS as they pass: the gathered rows (for the dW1/dW3 product) and the
+// weights transposed (so that the backward's dX and dA products read them
+// K-contiguous).
 //
 // fp32: a plain LDS-tiled FMA kernel with the same operand conventions.
 #include <type_traits>
