@@ -46,10 +46,15 @@ FLUSH_BYTES = 512 << 20  # cold-cache steps: twice the 256 MiB last-level (MALL)
 
 
 def sources_hash():
+    """Hash of the GEMM sources' code (comments and whitespace removed), so that the
+    stored traffic counters stay valid across comment-only edits."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
+            src = fh.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
     return h.hexdigest()[:16]
 
 
