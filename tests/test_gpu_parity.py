@@ -236,6 +236,28 @@ def test_deterministic():
         assert np.array_equal(a[n], b[n]), n
 
 
+def test_deterministic_full_training_step():
+    """At the benchmark's size the training step gives bit-identical outputs on
+    repeated runs (no atomics: every sum has a fixed order), and the inference
+    forward agrees bit for bit with the training forward."""
+    wl = synth.TRAIN_BF16
+    print(f"[case] {wl.name} determinism", flush=True)
+    inp = synth.draw(wl, with_dy=True)
+    caps = caps_for(wl, inp)
+    X, Wg, W1, W3, W2, dY = (dev(a) for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY))
+    layer = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, wl.inv_temperatures[0],
+                     training=True)
+    runs = []
+    for _ in range(2):
+        y = layer.forward().clone()
+        runs.append([y] + [t.clone() for t in layer.backward(dY)])
+    torch.cuda.synchronize()
+    for n, a, b in zip(("Y",) + GRADS, runs[0], runs[1]):
+        assert torch.equal(a, b), n
+    inf = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, wl.inv_temperatures[0])
+    assert torch.equal(inf.forward(), runs[0][0])
+
+
 # ------------------------------------------------------------------ full-size workloads
 # Same launch configuration as the benchmark; the oracle checks the selection
 # everywhere, the scores on sampled rows and the outputs on sampled tokens.
