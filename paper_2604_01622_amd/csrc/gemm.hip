@@ -510,24 +510,29 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   constexpr int NQ = (NCH + 63) / 64;                           // chunks per lane
   constexpr int EQ = (EPI == EPI_SWIGLU_BWD && NQ > 4) ? 4 : NQ;  // chunks per batch
   static_assert(NQ % EQ == 0, "whole batches");
-  // SwiGLU backward: this slice's H1/H3 chunks are loaded before the slice is
-  // staged, so their latency overlaps the staging (rows or columns past the
-  // matrix read element 0 and are not stored).
+  // SwiGLU backward: the H1/H3 chunks of slice 0 are loaded before it is
+  // staged; those of slice mi + 1 batch by batch as slice mi's batches finish
+  // with theirs, so their latency overlaps slice mi's work (rows or columns past
+  // the matrix read element 0 and are not stored).
   constexpr int HQ = (EPI == EPI_SWIGLU_BWD) ? NQ : 1;
-  u32x4 h1raw[HQ], h3raw[HQ];
+  u32x4 h1raw[2][HQ], h3raw[2][HQ];
+  auto load_h = [&](int mi, int q) {
+    if constexpr (EPI == EPI_SWIGLU_BWD) {
+      const int mb = m0 + wm * WM + mi * 32;
+      const int c = lane + q * 64;
+      const int m = mb + c / CPR, n = n0 + wn * WN + (c % CPR) * 8;
+      const size_t ho = (m < M && n < p.N) ? tc.h_off + (size_t)m * p.ldh + n : 0;
+      h1raw[mi & 1][q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H1 + ho);
+      h3raw[mi & 1][q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H3 + ho);
+    }
+  };
+  if constexpr (EPI == EPI_SWIGLU_BWD) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) load_h(0, q);
+  }
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
     const int mbase = m0 + wm * WM + mi * 32;
-    if constexpr (EPI == EPI_SWIGLU_BWD) {
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int c = lane + q * 64;
-        const int m = mbase + c / CPR, n = n0 + wn * WN + (c % CPR) * 8;
-        const size_t ho = (m < M && n < p.N) ? tc.h_off + (size_t)m * p.ldh + n : 0;
-        h1raw[q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H1 + ho);
-        h3raw[q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H3 + ho);
-      }
-    }
 #pragma unroll
     for (int ni = 0; ni < NB; ++ni)
 #pragma unroll
@@ -597,7 +602,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
           float d1[8], d3[8];
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
-            const uint32_t w1 = h1raw[q][u >> 1], w3 = h3raw[q][u >> 1];
+            const uint32_t w1 = h1raw[mi & 1][q][u >> 1], w3 = h3raw[mi & 1][q][u >> 1];
             const float h1 = bf16_to_f32((u & 1) ? (w1 >> 16) : (w1 & 0xffffu));
             const float h3 = bf16_to_f32((u & 1) ? (w3 >> 16) : (w3 & 0xffffu));
             const float da = v[e][u];
@@ -608,6 +613,12 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
           const size_t off = tc.c_off + (size_t)m * p.ldc + n;
           Elem<bf16_t>::store8((bf16_t*)p.C + off, d1);
           Elem<bf16_t>::store8((bf16_t*)p.C2 + off, d3);
+        }
+      }
+      if constexpr (EPI == EPI_SWIGLU_BWD) {
+        if (mi + 1 < MB) {
+#pragma unroll
+          for (int e = 0; e < EQ; ++e) load_h(mi + 1, q0 + e);
         }
       }
     }
