@@ -304,6 +304,8 @@ def main():
                     help="token choice: scale router rows by exp(N(0, s)) (uneven expert loads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forward-only", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip timing the step as a replayed HIP graph")
     ap.add_argument("--no-cold", action="store_true",
                     help="skip the cold-cache steps (a 512 MiB buffer overwritten before each)")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -482,6 +484,31 @@ def main():
         fms = start.elapsed_time(end) / a.steps
         out["forward_only"] = {"tokens_per_s": round(N / (fms * 1e-3), 1), "ms": round(fms, 4)}
         del inf
+
+    if not a.no_graph:
+        # the same step captured once in a HIP graph and replayed (launch overhead gone)
+        try:
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                step()
+            torch.cuda.current_stream().wait_stream(side)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step()
+            for _ in range(a.warmup):
+                g.replay()
+            torch.cuda.synchronize()
+            start.record()
+            for _ in range(a.steps):
+                g.replay()
+            end.record()
+            torch.cuda.synchronize()
+            gms = start.elapsed_time(end) / a.steps
+            out["graph_replay"] = {"ms": round(gms, 4), "tokens_per_s": round(N / (gms * 1e-3), 1)}
+            del g
+        except Exception as exc:   # report, do not fail the benchmark line
+            out["graph_replay"] = {"error": str(exc)[:200]}
 
     if not a.no_cold:
         # cold caches: overwrite a buffer twice the size of the MALL before every

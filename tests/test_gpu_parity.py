@@ -258,6 +258,42 @@ def test_deterministic_full_training_step():
     assert torch.equal(inf.forward(), runs[0][0])
 
 
+@pytest.mark.parametrize("dtype,shared", [("bf16", 0), ("bf16", 128), ("f32", 0)])
+def test_graph_capture_replays(dtype, shared):
+    """A training step captured in a HIP graph replays to the eager results bit
+    for bit, replay after replay, with eager work between the replays (the
+    library enqueues kernels only, no memory-set nodes)."""
+    wl = synth.small("graph", [300, 212], 128, 8, 192, dtype=dtype, seed=44, capacity_factor=3.0,
+                     backward=True, d_shared=shared)
+    inp = synth.draw(wl, with_dy=True)
+    caps = caps_for(wl, inp)
+    X, Wg, W1, W3, W2, dY = (dev(a) for a in (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY))
+    sh = None if inp.shared is None else tuple(dev(w) for w in inp.shared)
+    layer = ec.Layer(X, Wg, W1, W3, W2, wl.group_offsets, caps, 1.0, training=True, shared=sh)
+
+    def step():
+        y = layer.forward()
+        return [y] + list(layer.backward(dY))
+
+    eager = [t.clone() for t in step()]
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):   # warm-up on the capture stream
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        outs = step()
+    for r in range(3):
+        for t in outs:
+            t.zero_()   # eager work between replays; the replay must rewrite everything
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(outs, eager)):
+            assert torch.equal(a, b), (r, i)
+
+
 # ------------------------------------------------------------------ full-size workloads
 # Same launch configuration as the benchmark; the oracle checks the selection
 # everywhere, the scores on sampled rows and the outputs on sampled tokens.
