@@ -186,7 +186,7 @@ __global__ __launch_bounds__(256 * RouterCfg<ET>::KS) void router_softmax_bf16_k
   }
 }
 
-// fp32 storage: plain fp32 FMA (exact products, fp32 sums in K order).
+// fp32 storage: plain fp32 FMA, fp32 sums of 32-wide K chunks added in K order.
 constexpr int RF_ROWS = 32;
 constexpr int RF_KC = 32;
 
@@ -218,9 +218,11 @@ __global__ __launch_bounds__(256) void router_softmax_f32_kernel(
       const int o = tid + q * 256;
       if (o < nout) {
         const int r = o / E, e = o % E;
-        float a = acc[q];
+        // two-level sum: each K chunk in its own partial, the partials added in
+        // K order (rounding error grows with the chunk and chunk counts, not d)
+        float a = 0.f;
         for (int k = 0; k < RF_KC; ++k) a = fmaf(sX[r][k], sW[e][k], a);
-        acc[q] = a;
+        acc[q] += a;
       }
     }
     __syncthreads();

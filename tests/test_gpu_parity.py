@@ -160,9 +160,19 @@ def test_temperature(inv_tau):
     full_case(wl, inv_tau=inv_tau)
 
 
-@pytest.mark.parametrize("E", [1, 5, 17, 200])
+@pytest.mark.parametrize("E", [1, 5, 17, 200, 256])
 def test_expert_counts(E):
     wl = synth.small(f"E{E}", [256, 129], 128, E, 64, seed=13, capacity_factor=min(2.0, E))
+    full_case(wl)
+
+
+@pytest.mark.parametrize("dtype,d,h", [("bf16", 16384, 64), ("bf16", 64, 16384),
+                                       ("f32", 16384, 64)])
+def test_maximum_widths(dtype, d, h):
+    # the widest model and hidden dimensions the interface accepts: 256 K-steps in
+    # the products that contract over them, 2048 chunks per combine row
+    wl = synth.small(f"wide_{dtype}_{d}_{h}", [130, 70], d, 3, h, dtype=dtype, seed=22,
+                     capacity_factor=1.5, backward=True)
     full_case(wl)
 
 
