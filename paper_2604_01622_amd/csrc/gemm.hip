@@ -180,7 +180,10 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   const int m0 = mt * BM;
   const int n0 = (EPI == EPI_SWIGLU) ? nt * (BN / 2) : nt * BN;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index is uniform: read into a scalar register so that the LDS
+  // destinations of the DMA loads (M0) are formed with scalar arithmetic
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % WGM, wn = wave / WGM;
   const bf16_t* Ab = reinterpret_cast<const bf16_t*>(p.A) + tc.a_off;
   const bf16_t* Bb = reinterpret_cast<const bf16_t*>(p.B) + (size_t)e * p.b_bs;
