@@ -287,6 +287,39 @@ def run_tc(a):
     print(json.dumps(out), flush=True)
 
 
+def vendor_gemm(E, M, d, h, warmup, steps, backward):
+    """torch.matmul (hipBLASLt) on the expert products' batched shapes, every
+    operand contiguous and row-major, seeded normal bf16 values: a reference for
+    the library's grouped GEMMs (same FLOPs, no gather, no fused epilogue)."""
+    import torch
+    shapes = {"gemm_w13_swiglu": (M, d, 2 * h), "gemm_w2": (M, h, d)}
+    if backward:
+        shapes.update({"gemm_dA_swiglu_bwd": (M, d, h), "gemm_dXe": (M, 2 * h, d),
+                       "gemm_dW2": (d, M, h), "gemm_dW13": (2 * h, M, d)})
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    res = {}
+    for name, (m, k, n) in shapes.items():
+        A = torch.randn(E, m, k, device="cuda", generator=gen).to(torch.bfloat16)
+        B = (torch.randn(E, k, n, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+        C = torch.empty(E, m, n, device="cuda", dtype=torch.bfloat16)
+        for _ in range(warmup):
+            torch.matmul(A, B, out=C)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(steps):
+            torch.matmul(A, B, out=C)
+        ev1.record()
+        torch.cuda.synchronize()
+        t = ev0.elapsed_time(ev1) / steps
+        fl = 2.0 * E * m * k * n
+        res[name] = {"ms": round(t, 4), "tflops": round(fl / (t * 1e-3) / 1e12, 1),
+                     "shape": f"{E} x ({m} x {k}) @ ({k} x {n})"}
+        del A, B, C
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -310,6 +343,9 @@ def main():
                     help="skip the cold-cache steps (a 512 MiB buffer overwritten before each)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="run one plain 1 GiB elementwise copy first (scales --pmc byte counters)")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="also time torch.matmul (hipBLASLt) on the same batched expert-product "
+                         "shapes, as a reference for the grouped GEMM figures")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
                     help="write profiles/traffic_<stage>.json from two --pmc runs and exit")
     a = ap.parse_args()
@@ -527,6 +563,9 @@ def main():
         out["cold_cache"] = {"ms_median": round(cms, 4), "tokens_per_s": round(N / (cms * 1e-3), 1),
                              "flush_bytes": FLUSH_BYTES}
         del flush
+
+    if a.vendor_gemm and esz == 2:
+        out["vendor_gemm"] = vendor_gemm(E, K, d, h, a.warmup, a.steps, backward)
 
     props = torch.cuda.get_device_properties(0)
     out["env"] = {"device": props.name, "gfx": getattr(props, "gcnArchName", None),
