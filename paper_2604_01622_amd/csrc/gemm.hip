@@ -377,7 +377,10 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     for (int q = 0; q < NMF; ++q) {
       if (q < lo || q >= hi) continue;
       const int mi = q / NB, ni = q % NB;
-      acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][mi], bfr[cur][ni],
+      // B fragment first: the 32 x 32 block comes out transposed, each lane
+      // holding four consecutive output columns of one row (16-byte staging
+      // writes in the epilogue)
+      acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][ni], af[cur][mi],
                                                               acc[mi][ni], 0, 0, 0);
     }
   };
@@ -536,13 +539,15 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
     const int mbase = m0 + wm * WM + mi * 32;
+    // acc[mi][ni][4 g + i] is row lane % 32 of the slice, column
+    // 32 ni + 8 g + 4 (lane / 32) + i
 #pragma unroll
     for (int ni = 0; ni < NB; ++ni)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        stage_f[row * SLD + ni * 32 + (lane & 31)] = acc[mi][ni][r];
-      }
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4*>(&stage_f[(lane & 31) * SLD + ni * 32 + g * 8 + (lane >> 5) * 4]) =
+            f32x4{acc[mi][ni][4 * g], acc[mi][ni][4 * g + 1], acc[mi][ni][4 * g + 2],
+                  acc[mi][ni][4 * g + 3]};
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
