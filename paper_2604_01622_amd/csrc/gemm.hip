@@ -247,10 +247,13 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     }
   }
   // Issues k-step kt; the calls come with kt = 0, 1, 2, ... in order.
-  auto issue = [&](int kt, int stage) {
+  // Loads [lo, hi) of k-step kt (A's loads first, then B's); each load of a
+  // k-step is issued exactly once and the k-steps in order.
+  auto issue_part = [&](int kt, int stage, int lo, int hi) {
     char* base = smem + stage * STAGE_BYTES;
 #pragma unroll
     for (int q = 0; q < OA::LOADS; ++q) {
+      if (q < lo || q >= hi) continue;
       const bf16_t* g;
       if constexpr (A_KC) {
         g = a_src[q] + kt * KSTEP;
@@ -262,6 +265,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     }
 #pragma unroll
     for (int q = 0; q < OB::LOADS; ++q) {
+      if (OA::LOADS + q < lo || OA::LOADS + q >= hi) continue;
       const bf16_t* g;
       if constexpr (B_KC) {
         g = b_src[q] + kt * KSTEP;
@@ -272,6 +276,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       dma16(g, base + OA::BYTES + (wave * OB::LOADS + q) * 1024);
     }
   };
+  auto issue = [&](int kt, int stage) { issue_part(kt, stage, 0, OA::LOADS + OB::LOADS); };
 
   auto b_lds_col = [&](int ni) -> int {
     if constexpr (EPI == EPI_SWIGLU) {
@@ -453,8 +458,16 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // loops, so that no branch splits an interleaved group.
   constexpr int NRD = MB * (A_KC ? 1 : 2) + NB * (B_KC ? 1 : 2);
   constexpr int HALF = NMF / 2;
-  auto kstep = [&](int kt, auto refill) {
+  // A stage's refill is issued in two parts: DMA_HEAD loads after the barrier
+  // that frees the stage, the rest in the next step's first sub-step (two
+  // stages only: the wait at every step end is then for all outstanding loads).
+  // K-contiguous operands only (the K-major products measured slower with it),
+  // and not with both copy-outs (registers would spill).
+  constexpr bool SPLIT_DMA = STAGES == 2 && KK > 1 && A_KC && B_KC && COPY != 3;
+  constexpr int DMA_HEAD = SPLIT_DMA ? LOADS / 2 : LOADS;
+  auto kstep = [&](int kt, auto refill, auto tail_part) {
     constexpr bool RF = decltype(refill)::value;
+    constexpr bool TAIL = SPLIT_DMA && decltype(tail_part)::value;
     const int stage = kt % STAGES;
     if constexpr (COPY & 1) {
       if (kt % tc.MT == mt) write_bt(kt, stage);
@@ -462,10 +475,23 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     if constexpr (COPY & 2) {
       if (kt % tc.NT == nt) write_ac(kt, stage);
     }
+    // TAIL: the second part of the previous step's refill goes out in this
+    // step's first 16-wide sub-step (it still has a whole step to land)
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int cur = kk & 1;
-      if (kk + 1 < KK) {
+      if (kk == 0 && TAIL) {
+        mfma_range(cur, 0, NMF);
+        issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, DMA_HEAD, LOADS);
+        load_frags(cur ^ 1, stage, kk + 1);
+#pragma unroll
+        for (int q = 0; q < NMF; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                 // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x010, (LOADS - DMA_HEAD + NMF - 1) / NMF, 0);  // DMA
+          __builtin_amdgcn_sched_group_barrier(0x100, (NRD + NMF - 1) / NMF, 0);             // LDS read
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      } else if (kk + 1 < KK) {
         mfma_range(cur, 0, NMF);
         load_frags(cur ^ 1, stage, kk + 1);
 #pragma unroll
@@ -483,23 +509,37 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
         mfma_range(cur, HALF, NMF);
-        if constexpr (RF) issue(kt + STAGES, stage);
+        if constexpr (RF) issue_part(kt + STAGES, stage, 0, DMA_HEAD);
         // after the final step this reads a stale stage, harmlessly
         load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
 #pragma unroll
         for (int q = 0; q < HALF; ++q) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // MFMA
-          if constexpr (RF) __builtin_amdgcn_sched_group_barrier(0x020, (LOADS + HALF - 1) / HALF, 0);  // DMA
+          if constexpr (RF) __builtin_amdgcn_sched_group_barrier(0x010, (DMA_HEAD + HALF - 1) / HALF, 0);  // DMA
           __builtin_amdgcn_sched_group_barrier(0x100, (NRD + HALF - 1) / HALF, 0);     // LDS read
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
   };
+  // Straight-line segments, so that no branch splits an interleaved group:
+  // step 0 (refill, no tail), steps that refill and finish the previous
+  // refill, the step that only finishes it, then the last steps.
   {
+    using T_ = std::true_type;
+    using F_ = std::false_type;
     int kt = 0;
-    for (; kt + STAGES < KT; ++kt) kstep(kt, std::true_type{});
-    for (; kt < KT; ++kt) kstep(kt, std::false_type{});
+    if constexpr (SPLIT_DMA) {
+      if (KT > STAGES) {
+        kstep(0, T_{}, F_{});
+        for (kt = 1; kt + STAGES < KT; ++kt) kstep(kt, T_{}, T_{});
+        kstep(kt, F_{}, T_{});
+        ++kt;
+      }
+    } else {
+      for (; kt + STAGES < KT; ++kt) kstep(kt, T_{}, F_{});
+    }
+    for (; kt < KT; ++kt) kstep(kt, F_{}, F_{});
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   __syncthreads();
