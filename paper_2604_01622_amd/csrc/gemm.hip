@@ -453,9 +453,9 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // two).  Inside a stage the MFMAs on the current fragments alternate with
   // the reads of the next ones (one MFMA, one read, ...).  At a stage end: half
   // the MFMAs, then this wave's waits and the barrier, then the other half
-  // alternating with the refill's DMA and the next stage's first reads.  The
-  // steps that refill a stage and the last STAGES steps that do not are two
-  // loops, so that no branch splits an interleaved group.
+  // alternating with the refill's DMA and the next stage's first reads.  Steps
+  // with and without a refill (or a refill's second half) run in separate
+  // straight-line segments, so that no branch splits an interleaved group.
   constexpr int NRD = MB * (A_KC ? 1 : 2) + NB * (B_KC ? 1 : 2);
   constexpr int HALF = NMF / 2;
   // A stage's refill is issued in two parts: DMA_HEAD loads after the barrier
@@ -464,7 +464,11 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // K-contiguous operands only (the K-major products measured slower with it),
   // and not with both copy-outs (registers would spill).
   constexpr bool SPLIT_DMA = STAGES == 2 && KK > 1 && A_KC && B_KC && COPY != 3;
+  // (measured: half after the barrier and half in one sub-step beats a quarter
+  // then three sub-steps, none after the barrier, or two tail sub-steps)
   constexpr int DMA_HEAD = SPLIT_DMA ? LOADS / 2 : LOADS;
+  constexpr int TAIL_SUBS = 1;
+  constexpr int TAIL_PER = (LOADS - DMA_HEAD + TAIL_SUBS - 1) / TAIL_SUBS;
   auto kstep = [&](int kt, auto refill, auto tail_part) {
     constexpr bool RF = decltype(refill)::value;
     constexpr bool TAIL = SPLIT_DMA && decltype(tail_part)::value;
@@ -480,14 +484,18 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int cur = kk & 1;
-      if (kk == 0 && TAIL) {
+      if (kk < TAIL_SUBS && TAIL) {
         mfma_range(cur, 0, NMF);
-        issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, DMA_HEAD, LOADS);
+        {
+          const int q0 = DMA_HEAD + kk * TAIL_PER;
+          const int q1 = q0 + TAIL_PER < LOADS ? q0 + TAIL_PER : LOADS;
+          issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, q0, q1);
+        }
         load_frags(cur ^ 1, stage, kk + 1);
 #pragma unroll
         for (int q = 0; q < NMF; ++q) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                 // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x010, (LOADS - DMA_HEAD + NMF - 1) / NMF, 0);  // DMA
+          __builtin_amdgcn_sched_group_barrier(0x010, (TAIL_PER + NMF - 1) / NMF, 0);         // DMA
           __builtin_amdgcn_sched_group_barrier(0x100, (NRD + NMF - 1) / NMF, 0);             // LDS read
         }
         __builtin_amdgcn_sched_barrier(0);
