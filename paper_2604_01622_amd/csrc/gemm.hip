@@ -249,7 +249,10 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // Issues k-step kt; the calls come with kt = 0, 1, 2, ... in order.
   // Loads [lo, hi) of k-step kt (A's loads first, then B's); each load of a
   // k-step is issued exactly once and the k-steps in order.
-  auto issue_part = [&](int kt, int stage, int lo, int hi) {
+  // K-major rows past the valid K read the zero block; with full_step (a step
+  // known to lie below both kv) the per-load check is skipped.
+  auto issue_part = [&](int kt, int stage, int lo, int hi, auto full_step) {
+    constexpr bool FULL = decltype(full_step)::value;
     char* base = smem + stage * STAGE_BYTES;
 #pragma unroll
     for (int q = 0; q < OA::LOADS; ++q) {
@@ -258,7 +261,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       if constexpr (A_KC) {
         g = a_src[q] + kt * KSTEP;
       } else {
-        g = (kt * KSTEP + a_row[q] < p.kv_a) ? a_src[q] : g_zero_block;
+        g = (FULL || kt * KSTEP + a_row[q] < p.kv_a) ? a_src[q] : g_zero_block;
         a_src[q] += a_step[q];
       }
       dma16(g, base + (wave * OA::LOADS + q) * 1024);
@@ -270,13 +273,15 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       if constexpr (B_KC) {
         g = b_src[q] + kt * KSTEP;
       } else {
-        g = (kt * KSTEP + b_row[q] < p.kv_b) ? b_src[q] : g_zero_block;
+        g = (FULL || kt * KSTEP + b_row[q] < p.kv_b) ? b_src[q] : g_zero_block;
         b_src[q] += b_step[q];
       }
       dma16(g, base + OA::BYTES + (wave * OB::LOADS + q) * 1024);
     }
   };
-  auto issue = [&](int kt, int stage) { issue_part(kt, stage, 0, OA::LOADS + OB::LOADS); };
+  auto issue = [&](int kt, int stage) {
+    issue_part(kt, stage, 0, OA::LOADS + OB::LOADS, std::false_type{});
+  };
 
   auto b_lds_col = [&](int ni) -> int {
     if constexpr (EPI == EPI_SWIGLU) {
@@ -469,7 +474,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   constexpr int DMA_HEAD = SPLIT_DMA ? LOADS / 2 : LOADS;
   constexpr int TAIL_SUBS = 1;
   constexpr int TAIL_PER = (LOADS - DMA_HEAD + TAIL_SUBS - 1) / TAIL_SUBS;
-  auto kstep = [&](int kt, auto refill, auto tail_part) {
+  auto kstep = [&](int kt, auto refill, auto tail_part, auto full_refill) {
     constexpr bool RF = decltype(refill)::value;
     constexpr bool TAIL = SPLIT_DMA && decltype(tail_part)::value;
     const int stage = kt % STAGES;
@@ -489,7 +494,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
         {
           const int q0 = DMA_HEAD + kk * TAIL_PER;
           const int q1 = q0 + TAIL_PER < LOADS ? q0 + TAIL_PER : LOADS;
-          issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, q0, q1);
+          issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, q0, q1, std::false_type{});
         }
         load_frags(cur ^ 1, stage, kk + 1);
 #pragma unroll
@@ -517,7 +522,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
         mfma_range(cur, HALF, NMF);
-        if constexpr (RF) issue_part(kt + STAGES, stage, 0, DMA_HEAD);
+        if constexpr (RF) issue_part(kt + STAGES, stage, 0, DMA_HEAD, full_refill);
         // after the final step this reads a stale stage, harmlessly
         load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
 #pragma unroll
@@ -539,15 +544,21 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     int kt = 0;
     if constexpr (SPLIT_DMA) {
       if (KT > STAGES) {
-        kstep(0, T_{}, F_{});
-        for (kt = 1; kt + STAGES < KT; ++kt) kstep(kt, T_{}, T_{});
-        kstep(kt, F_{}, T_{});
+        kstep(0, T_{}, F_{}, F_{});
+        for (kt = 1; kt + STAGES < KT; ++kt) kstep(kt, T_{}, T_{}, F_{});
+        kstep(kt, F_{}, T_{}, F_{});
         ++kt;
       }
     } else {
-      for (; kt + STAGES < KT; ++kt) kstep(kt, T_{}, F_{});
+      // refills of the steps below KT - 1 skip the K-major row check when
+      // every such step lies below both kv (the usual case: only the last
+      // step is ragged)
+      const bool full_ok = p.kv_a >= (KT - 1) * KSTEP && p.kv_b >= (KT - 1) * KSTEP;
+      const int n_full = full_ok ? KT - STAGES - 1 : 0;
+      for (; kt < n_full; ++kt) kstep(kt, T_{}, F_{}, T_{});
+      for (; kt + STAGES < KT; ++kt) kstep(kt, T_{}, F_{}, F_{});
     }
-    for (; kt < KT; ++kt) kstep(kt, F_{}, F_{});
+    for (; kt < KT; ++kt) kstep(kt, F_{}, F_{}, F_{});
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   __syncthreads();
