@@ -13,9 +13,13 @@
 // (conflict-free fragment reads); K-major operands (the weight gradients'
 // token-row contractions) stay K-major in LDS and are read with the
 // transposing ds_read_b64_tr_b16.  The MFMAs of each k-step alternate with the
-// next step's fragment reads (and at a stage end with the refill's DMA, after
-// the barrier), so LDS latency hides behind MFMAs in flight.  Tiles are
-// numbered so that consecutive ones share an expert and stay on one XCD.
+// next step's fragment reads and, once the barrier has freed a stage, with its
+// refill's DMA (for K-contiguous products half of it then, half in the next
+// step's first sub-step), so LDS latency hides behind MFMAs in flight.  The
+// MFMAs take the B fragment first, so each lane ends with four consecutive
+// output columns of a row, staged through LDS with 16-byte writes for
+// coalesced stores.  Tiles are numbered so that consecutive ones share an
+// expert and stay on one XCD.
 //
 // The W1/W3 product gathers its A rows (the selected tokens) in the operand
 // load.  In the training forward the W1/W3 and W2 products also copy tiles
