@@ -295,18 +295,22 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       return wn * WN + ni * 32;
     }
   };
-  // Fragment addressing.  K-contiguous: byte offset of the lane's row and its
-  // swizzle.  K-major: byte offset of the lane's column chunk (before the
-  // k-dependent swizzle) and the k row it starts at.
+  // Fragment addressing.  K-contiguous: lane l reads row base + l % 32 of the
+  // tile, base a multiple of 32 (uniform over the wave), so the row's chunk
+  // swizzle is one per-lane value combined with a uniform one and nothing per
+  // fragment is held in registers.  K-major: byte offset of the lane's column
+  // chunk (before the k-dependent swizzle) and the k row it starts at.
   const int g16 = lane >> 4, j16 = lane & 15;
-  int a_off[MB], a_sw[MB], b_off[NB], b_sw[NB];
+  const int l31 = lane & 31;
+  const int swz_lane = (l31 & 7) ^ (l31 >> 3);
+  auto kc_sw = [&](int base) -> int {
+    if constexpr (KSTEP == 64) return swz_lane ^ ((base >> 3) & 7);
+    else return kc_swz<KSTEP>(base + l31);
+  };
+  int a_off[A_KC ? 1 : MB], a_sw[A_KC ? 1 : MB], b_off[B_KC ? 1 : NB], b_sw[B_KC ? 1 : NB];
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi) {
-    if constexpr (A_KC) {
-      const int row = wm * WM + mi * 32 + (lane & 31);
-      a_off[mi] = row * KSTEP * 2;
-      a_sw[mi] = kc_swz<KSTEP>(row);
-    } else {
+    if constexpr (!A_KC) {
       const int col = wm * WM + mi * 32 + 16 * (g16 & 1) + 4 * (j16 & 3);
       a_off[mi] = col >> 3;           // logical chunk
       a_sw[mi] = (col & 7) * 2;       // byte offset inside the chunk
@@ -314,11 +318,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   }
 #pragma unroll
   for (int ni = 0; ni < NB; ++ni) {
-    if constexpr (B_KC) {
-      const int row = b_lds_col(ni) + (lane & 31);
-      b_off[ni] = row * KSTEP * 2;
-      b_sw[ni] = kc_swz<KSTEP>(row);
-    } else {
+    if constexpr (!B_KC) {
       const int col = b_lds_col(ni) + 16 * (g16 & 1) + 4 * (j16 & 3);
       b_off[ni] = col >> 3;
       b_sw[ni] = (col & 7) * 2;
@@ -340,19 +340,24 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     const int lc = kk * 2 + (lane >> 5);
 #pragma unroll
     for (int mi = 0; mi < MB; ++mi) {
-      if constexpr (A_KC)
+      if constexpr (A_KC) {
+        const int base = wm * WM + mi * 32;
         af[buf][mi] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(sa + a_off[mi] + ((lc ^ a_sw[mi]) << 4)));
-      else
+            bf16x8, *reinterpret_cast<const u32x4*>(sa + (base + l31) * (KSTEP * 2) +
+                                                    ((lc ^ kc_sw(base)) << 4)));
+      } else
         af[buf][mi] = km_frag(sa, BM * 2, a_off[mi], a_sw[mi], kk);
     }
 #pragma unroll
     for (int ni = 0; ni < NB; ++ni) {
-      if constexpr (B_KC)
+      if constexpr (B_KC) {
+        const int base = b_lds_col(ni);
         bfr[buf][ni] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(sbb + b_off[ni] + ((lc ^ b_sw[ni]) << 4)));
-      else
+            bf16x8, *reinterpret_cast<const u32x4*>(sbb + (base + l31) * (KSTEP * 2) +
+                                                    ((lc ^ kc_sw(base)) << 4)));
+      } else {
         bfr[buf][ni] = km_frag(sbb, BN * 2, b_off[ni], b_sw[ni], kk);
+      }
     }
   };
 
@@ -470,9 +475,8 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // A stage's refill is issued in two parts: DMA_HEAD loads after the barrier
   // that frees the stage, the rest in the next step's first sub-step (two
   // stages only: the wait at every step end is then for all outstanding loads).
-  // K-contiguous operands only (the K-major products measured slower with it),
-  // and not with both copy-outs (registers would spill).
-  constexpr bool SPLIT_DMA = STAGES == 2 && KK > 1 && A_KC && B_KC && COPY != 3;
+  // K-contiguous operands only (the K-major products measured slower with it).
+  constexpr bool SPLIT_DMA = STAGES == 2 && KK > 1 && A_KC && B_KC;
   // (measured: half after the barrier and half in one sub-step beats a quarter
   // then three sub-steps, none after the barrier, or two tail sub-steps)
   constexpr int DMA_HEAD = SPLIT_DMA ? LOADS / 2 : LOADS;
