@@ -297,9 +297,10 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   };
   // Fragment addressing.  K-contiguous: lane l reads row base + l % 32 of the
   // tile, base a multiple of 32 (uniform over the wave), so the row's chunk
-  // swizzle is one per-lane value combined with a uniform one and nothing per
-  // fragment is held in registers.  K-major: byte offset of the lane's column
-  // chunk (before the k-dependent swizzle) and the k row it starts at.
+  // swizzle is one per-lane value combined with a uniform one.  K-major: lane l
+  // reads 4 columns from column base + lp of k rows km_k and km_k + 4 (of each
+  // 16-wide step); with base a multiple of 32 the swizzled chunk is base / 8
+  // XOR a per-lane value.  Nothing per fragment is held in registers.
   const int g16 = lane >> 4, j16 = lane & 15;
   const int l31 = lane & 31;
   const int swz_lane = (l31 & 7) ^ (l31 >> 3);
@@ -307,30 +308,16 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     if constexpr (KSTEP == 64) return swz_lane ^ ((base >> 3) & 7);
     else return kc_swz<KSTEP>(base + l31);
   };
-  int a_off[A_KC ? 1 : MB], a_sw[A_KC ? 1 : MB], b_off[B_KC ? 1 : NB], b_sw[B_KC ? 1 : NB];
-#pragma unroll
-  for (int mi = 0; mi < MB; ++mi) {
-    if constexpr (!A_KC) {
-      const int col = wm * WM + mi * 32 + 16 * (g16 & 1) + 4 * (j16 & 3);
-      a_off[mi] = col >> 3;           // logical chunk
-      a_sw[mi] = (col & 7) * 2;       // byte offset inside the chunk
-    }
-  }
-#pragma unroll
-  for (int ni = 0; ni < NB; ++ni) {
-    if constexpr (!B_KC) {
-      const int col = b_lds_col(ni) + 16 * (g16 & 1) + 4 * (j16 & 3);
-      b_off[ni] = col >> 3;
-      b_sw[ni] = (col & 7) * 2;
-    }
-  }
   const int km_k = 8 * (g16 >> 1) + (j16 >> 2);   // k row (within a 16-step) of a K-major read
+  const int km_lp = 16 * (g16 & 1) + 4 * (j16 & 3);
+  const int km_inner = (km_lp & 7) * 2;             // byte offset inside the chunk
+  const int km_u = (km_lp >> 3) | km_swz(km_k);     // chunk bits from the lane and the k swizzle
 
   bf16x8 af[2][MB], bfr[2][NB];
-  auto km_frag = [&](const char* tile, int rowbytes, int chunk, int inner, int kk) -> bf16x8 {
-    const int k0 = kk * 16 + km_k, k1 = k0 + 4;
-    const v4i16 lo = ds_read_tr16(tile + k0 * rowbytes + ((chunk ^ km_swz(k0)) << 4) + inner);
-    const v4i16 hi = ds_read_tr16(tile + k1 * rowbytes + ((chunk ^ km_swz(k1)) << 4) + inner);
+  auto km_frag = [&](const char* tile, int rowbytes, int base, int kk) -> bf16x8 {
+    const char* p0 = tile + (kk * 16 + km_k) * rowbytes + (((base >> 3) ^ km_u) << 4) + km_inner;
+    const v4i16 lo = ds_read_tr16(p0);
+    const v4i16 hi = ds_read_tr16(p0 + 4 * rowbytes);
     const v4i16 both[2] = {lo, hi};
     return __builtin_bit_cast(bf16x8, both);
   };
@@ -346,7 +333,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
             bf16x8, *reinterpret_cast<const u32x4*>(sa + (base + l31) * (KSTEP * 2) +
                                                     ((lc ^ kc_sw(base)) << 4)));
       } else
-        af[buf][mi] = km_frag(sa, BM * 2, a_off[mi], a_sw[mi], kk);
+        af[buf][mi] = km_frag(sa, BM * 2, wm * WM + mi * 32, kk);
     }
 #pragma unroll
     for (int ni = 0; ni < NB; ++ni) {
@@ -356,7 +343,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
             bf16x8, *reinterpret_cast<const u32x4*>(sbb + (base + l31) * (KSTEP * 2) +
                                                     ((lc ^ kc_sw(base)) << 4)));
       } else {
-        bfr[buf][ni] = km_frag(sbb, BN * 2, b_off[ni], b_sw[ni], kk);
+        bfr[buf][ni] = km_frag(sbb, BN * 2, b_lds_col(ni), kk);
       }
     }
   };
