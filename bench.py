@@ -129,6 +129,7 @@ def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits, hs=0):
     of the shared experts)."""
     P = E * K
     s = esz
+    parts = (h + 63) // 64 if esz == 4 else (h + 127) // 128  # gate-gradient partials per row
     table = {
         "router": (2 * N * d * E, N * d * s + E * d * s + 2 * N * E * 4),
         "topk": (0, 2 * E * N * 4 + P * 4),
@@ -137,12 +138,13 @@ def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits, hs=0):
                             + (2 * P * h * s if save_h else 0)),
         "gemm_w2": (2 * P * d * h, P * h * s + E * d * h * s + P * d * s),
         "combine": (0, 2 * E * N * 4 + P * d * s + N * d * s),
-        "bwd_gather": (0, 3 * P * 4 + 3 * P * d * s),
-        "gemm_dA_swiglu_bwd": (2 * P * d * h, P * d * s + E * d * h * s + 4 * P * h * s),
+        "bwd_gather": (0, 2 * P * 4 + 2 * P * d * s),
+        "gemm_dA_swiglu_bwd": (2 * P * d * h, P * d * s + E * d * h * s + 4 * P * h * s
+                               + P * parts * 4),
         "gemm_dW2": (2 * P * d * h, P * d * s + P * h * s + E * d * h * s),
         "gemm_dXe": (4 * P * d * h, 2 * P * h * s + 2 * E * h * d * s + P * d * s),
         "gemm_dW13": (4 * P * d * h, 2 * P * h * s + P * d * s + 2 * E * h * d * s),
-        "router_dz": (0, 3 * N * E * 4 + P * 4 + N * EP * 2),
+        "router_dz": (0, 3 * N * E * 4 + P * parts * 4 + N * EP * 2),
         "router_dx": (2 * N * EP * d, N * EP * 2 + E * d * s + N * d * s),
         "bwd_combine": (0, E * N * 4 + P * d * s + 2 * N * d * s),
         "router_dwg": (2 * N * EP * d, N * EP * 2 + N * d * s + 2 * splits * E * d * 4),

@@ -159,7 +159,7 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
 
 struct BwdWs {
   void* dO;       // [E, K, d]; reused for dXe once dO is dead
-  float* dSp;     // [E, K]
+  float* dsp;     // [E, K, dsp_parts(h)] gate-gradient partials of the dA product
   void* dH;       // [E, K, 2h]
   float* dZ;      // [N, E]
   uint16_t* dZb;  // [N, EP] (bf16 only)
@@ -173,7 +173,7 @@ struct BwdWs {
 BwdWs carve_bwd(Carve& c, const Plan& P) {
   BwdWs w;
   w.dO = c.take((size_t)P.E * P.K * P.d * P.esz);
-  w.dSp = (float*)c.take((size_t)P.E * P.K * 4);
+  w.dsp = (float*)c.take((size_t)P.E * P.K * ec::dsp_parts(P.dtype, P.h) * 4);
   w.dH = c.take((size_t)P.E * P.K * 2 * P.h * P.esz);
   w.dZ = (float*)c.take((size_t)P.N * P.E * 4);
   w.dZb = P.dtype == EC_BF16 ? (uint16_t*)c.take((size_t)P.N * P.EP * 2) : nullptr;
@@ -632,10 +632,11 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   // bf16: dA = dO W2 and dXe = dH1 W1 + dH3 W3 read the transposed weights
   // that the forward's products wrote into `saved`
   EC_HIP(mark(0, stream));
-  EC_HIP(ec::launch_bwd_gather(P.dtype, dY, s.O, s.S, s.sel, w.dO, w.dSp, N, E, M, d, stream));
+  EC_HIP(ec::launch_bwd_gather(P.dtype, dY, s.S, s.sel, w.dO, N, E, M, d, stream));
   EC_HIP(mark(1, stream));
+  // dA's epilogue also sums dA * A per row: the gate's gradient (times the gate)
   EC_HIP(ec::launch_gemm_dA(P.dtype, w.dO, W2, s.H1, s.H3, w.dH, E, M, d, h, stream, false,
-                            s.W2T));
+                            s.W2T, w.dsp));
   EC_HIP(mark(2, stream));
   EC_HIP(ec::launch_gemm_dW2(P.dtype, w.dO, s.A, dW2, E, M, d, h, stream));
   EC_HIP(mark(3, stream));
@@ -643,7 +644,7 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   EC_HIP(mark(4, stream));
   EC_HIP(ec::launch_gemm_dW13(P.dtype, w.dH, s.Xe, dW1, dW3, E, M, d, h, stream));
   EC_HIP(mark(5, stream));
-  EC_HIP(ec::launch_router_dz(s.S, w.dSp, s.slot, w.dZ, w.dZb, N, E, P.EP, M,
+  EC_HIP(ec::launch_router_dz(s.S, w.dsp, ec::dsp_parts(P.dtype, h), s.slot, w.dZ, w.dZb, N, E, P.EP, M,
                               p->inv_temperature, stream));
   EC_HIP(mark(6, stream));
   const void* dZop = P.dtype == EC_BF16 ? (const void*)w.dZb : (const void*)w.dZ;

@@ -92,6 +92,23 @@ __device__ __forceinline__ float sigmoid_f(float z) {
 
 __device__ __forceinline__ float silu_f(float z) { return z * sigmoid_f(z); }
 
+// Sum over the 16 lanes of a DPP row (lanes 16 r .. 16 r + 15); every lane of
+// the row ends with the total.  Quad swaps (xor 1, xor 2) then row rotations
+// by 4 and 8 lanes, all in registers (no LDS permute).
+__device__ __forceinline__ float dpp_add(float t, int ctrl_id) {
+  int v = __builtin_bit_cast(int, t);
+  switch (ctrl_id) {
+    case 0: v = __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false); break;   // quad [1,0,3,2]
+    case 1: v = __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false); break;   // quad [2,3,0,1]
+    case 2: v = __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false); break;  // row_ror:4
+    default: v = __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false); break; // row_ror:8
+  }
+  return t + __builtin_bit_cast(float, v);
+}
+__device__ __forceinline__ float row16_sum(float t) {
+  return dpp_add(dpp_add(dpp_add(dpp_add(t, 0), 1), 2), 3);
+}
+
 // Order-preserving map from fp32 to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t f32_order_key(float f) {
   uint32_t u = __float_as_uint(f);

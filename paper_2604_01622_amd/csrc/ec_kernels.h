@@ -41,21 +41,21 @@ hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_
                           const void* Xr, void* Y, int N, int E, int K, int d, hipStream_t st,
                           long kstride = -1);
 
-// Backward gather: dO[j,r,:] = S[i,j] dY[i,:] and dS[i,j] = <dY[i,:], O[j,r,:]>,
-// i = sel_token[j,r]; dS [N,E] fp32 is zero for unselected pairs.
-hipError_t launch_bwd_gather(int dtype, const void* dY, const void* O, const float* S,
-                             const int32_t* sel_token, void* dO, float* dS, int N, int E, int K,
-                             int d, hipStream_t st);
+// Backward gather: dO[j,r,:] = S[i,j] dY[i,:], i = sel_token[j,r] (the gate's
+// gradient comes out of the dA product's epilogue instead).
+hipError_t launch_bwd_gather(int dtype, const void* dY, const float* S,
+                             const int32_t* sel_token, void* dO, int N, int E, int K, int d,
+                             hipStream_t st);
 
 // Backward combine: dX[i,:] = Xr[i,:] + sum_j dXe[j, slotT[j,i], :]  (Xr may alias dX).
 hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, const void* Xr,
                               void* dX, int N, int E, int K, int d, hipStream_t st);
 
-// Router backward, part 1: dZ = S * (dS - <S, dS>) / tau  [N,E] fp32, with
-// dS_ij = dSp[j, slot_ij] on the selection and 0 elsewhere; dZb (optional) is a
-// bf16 copy [N, EP] with zero columns E..EP-1.
-hipError_t launch_router_dz(const float* S, const float* dSp, const int32_t* slotT, float* dZ,
-                            uint16_t* dZb, int N, int E, int EP, int K, float inv_tau,
+// Router backward, part 1: dZ = S * (dS - <S, dS>) / tau  [N,E] fp32, from
+// S_ij dS_ij = sum over q of dsp[(j K + slot_ij) nparts + q] on the selection
+// (0 elsewhere); dZb (optional) is a bf16 copy [N, EP] with zero columns E..EP-1.
+hipError_t launch_router_dz(const float* S, const float* dsp, int nparts, const int32_t* slotT,
+                            float* dZ, uint16_t* dZb, int N, int E, int EP, int K, float inv_tau,
                             hipStream_t st);
 
 // Router backward, part 2: dX = dZ Wg  (bf16: dZ is the padded bf16 copy).
@@ -87,10 +87,15 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
                           int h, hipStream_t st, bool shared = false, void* W2T = nullptr);
 // dA = dO W2 and the SwiGLU backward: dH[:, 0:h] = dH1, dH[:, h:2h] = dH3 ([E,M,2h]).
 // W2T (bf16, may be null): W2 transposed, [E, h, d] (as launch_gemm_w2 writes
-// it); the product then reads K-contiguous weights.
+// it); the product then reads K-contiguous weights.  dsp (may be null):
+// [E M, dsp_parts(dtype, h)] fp32, per row and column block the sum of dA * A
+// (A = SiLU(H1) H3), whose row sum is the gate's gradient times the gate.
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
-                          bool shared = false, const void* W2T = nullptr);
+                          bool shared = false, const void* W2T = nullptr, float* dsp = nullptr);
+// gate-gradient partials per row of the dA product (blocks of 128 columns of
+// d_ff in bf16, 64 in fp32)
+int dsp_parts(int dtype, int h);
 // dXe = dH1 W1 + dH3 W3  ([E,M,d]).
 // shared: dXe += dH1 W1 + dH3 W3 (the shared experts' term added to dX).
 // W13T (required for bf16): [E, d, 2h], row n = column n of W1 then of W3, so

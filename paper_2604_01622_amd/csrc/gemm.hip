@@ -93,6 +93,14 @@ struct GemmParams {
   void* AC;
   long ac_bs;
   int ldac;
+  // SwiGLU backward only (may be null): the gate-gradient partials.  For row m
+  // of batch e and each column block q of the output (128 columns in the bf16
+  // kernel, 64 in the fp32 one), dsp[(e M + m) dsp_ld + q] = sum over the block
+  // of dA * A with A = SiLU(H1) H3 recomputed from the saved H1, H3 (dA = g dY
+  // W2 for a gated dO, so the sum over all blocks is g times the gate's
+  // gradient).
+  float* dsp;
+  int dsp_ld;
   // Variable rows per batch (token choice): batch e owns rows
   // [var_rows[e], var_rows[e+1]) of A, C and H (row strides lda, ldc, ldh) and
   // tiles [var_tiles[e], var_tiles[e+1]) of the launch; both device arrays of
@@ -570,6 +578,8 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   constexpr int NQ = (NCH + 63) / 64;                           // chunks per lane
   constexpr int EQ = (EPI == EPI_SWIGLU_BWD && NQ > 4) ? 4 : NQ;  // chunks per batch
   static_assert(NQ % EQ == 0, "whole batches");
+  static_assert(EPI != EPI_SWIGLU_BWD || (CPR == 16 && NCH % 64 == 0),
+                "the chunks of a 128-column block of a row sit in one 16-lane DPP row");
   // SwiGLU backward: the H1/H3 chunks of slice 0 are loaded before it is
   // staged; those of slice mi + 1 batch by batch as slice mi's batches finish
   // with theirs, so their latency overlaps slice mi's work (rows or columns past
@@ -620,6 +630,9 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
           for (int u = 0; u < 8; ++u) v3[e][u] = src[HW + u];
         }
       }
+      float dots[EPI == EPI_SWIGLU_BWD ? EQ : 1];
+#pragma unroll
+      for (int e = 0; e < (EPI == EPI_SWIGLU_BWD ? EQ : 1); ++e) dots[e] = 0.f;
 #pragma unroll
       for (int e = 0; e < EQ; ++e) {
         const int q = q0 + e;
@@ -662,6 +675,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
           }
         } else {  // EPI_SWIGLU_BWD
           float d1[8], d3[8];
+          float dot = 0.f;
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
             const uint32_t w1 = h1raw[mi & 1][q][u >> 1], w3 = h3raw[mi & 1][q][u >> 1];
@@ -669,15 +683,32 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
             const float h3 = bf16_to_f32((u & 1) ? (w3 >> 16) : (w3 & 0xffffu));
             const float da = v[e][u];
             const float sg = sigmoid_f(h1);
-            d3[u] = da * h1 * sg;
+            const float s1 = h1 * sg;   // SiLU(h1)
+            d3[u] = da * s1;
             d1[u] = da * h3 * sg * (1.0f + h1 * (1.0f - sg));
+            dot = fmaf(da, s1 * h3, dot);
           }
+          dots[e] = dot;
           const size_t off = tc.c_off + (size_t)m * p.ldc + n;
           Elem<bf16_t>::store8((bf16_t*)p.C + off, d1);
           Elem<bf16_t>::store8((bf16_t*)p.C2 + off, d3);
         }
       }
       if constexpr (EPI == EPI_SWIGLU_BWD) {
+        // gate-gradient partials: the 16 lanes of a DPP row hold the chunks of
+        // one row's 128-column block (columns past N hold clamped duplicates
+        // and count as zero)
+        if (p.dsp) {
+#pragma unroll
+          for (int e = 0; e < EQ; ++e) {
+            const int c = lane + (q0 + e) * 64;
+            const int m = mbase + c / CPR;
+            const int n = n0 + wn * WN + (c % CPR) * 8;
+            const float t = row16_sum(n < p.N ? dots[e] : 0.f);
+            if ((lane & 15) == 0 && m < M && n < p.N)
+              p.dsp[((size_t)tc.e * p.M + m) * p.dsp_ld + (n >> 7)] = t;
+          }
+        }
         if (mi + 1 < MB) {
 #pragma unroll
           for (int e = 0; e < EQ; ++e) load_h(mi + 1, q0 + e);
@@ -853,6 +884,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p, int a_kc, i
     }
     __syncthreads();
   }
+  float dsum[4] = {0.f, 0.f, 0.f, 0.f};   // SwiGLU backward: gate-gradient partials per row
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -880,8 +912,22 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p, int a_kc, i
         const size_t off = c_off + (size_t)m * p.ldc + n;
         ((float*)p.C)[off] = da * h3 * sg * (1.0f + h1 * (1.0f - sg));
         ((float*)p.C2)[off] = da * h1 * sg;
+        dsum[i] = fmaf(da, h1 * sg * h3, dsum[i]);
       }
     }
+  if (EPI == EPI_SWIGLU_BWD && p.dsp) {
+    // the 16 threads of a row (tx, consecutive lanes) hold its 64 columns
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float t = dsum[i];
+      t += __shfl_xor(t, 1, 64);
+      t += __shfl_xor(t, 2, 64);
+      t += __shfl_xor(t, 4, 64);
+      t += __shfl_xor(t, 8, 64);
+      const int m = m0 + ty * 4 + i;
+      if (tx == 0 && m < M) p.dsp[((size_t)e * p.M + m) * p.dsp_ld + blockIdx.x] = t;
+    }
+  }
 }
 
 template <int EPI>
@@ -928,6 +974,8 @@ __global__ void splitk_store_kernel(const float* __restrict__ part, int splits, 
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
+
+int dsp_parts(int dtype, int h) { return dtype == DT_F32 ? (h + 63) / 64 : (h + 127) / 128; }
 
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
@@ -982,7 +1030,7 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
-                          bool shared, const void* W2T) {
+                          bool shared, const void* W2T, float* dsp) {
   // dA[m, n] = sum_k dO[m, k] W2[k, n]  (k over d, n over h); epilogue -> dH1, dH3
   GemmParams p = base_params();
   p.A = dO; p.a_bs = (long)M * d; p.lda = d;
@@ -991,6 +1039,7 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
   const size_t esz = dtype == DT_F32 ? 4 : 2;
   p.C = dH; p.C2 = (char*)dH + (size_t)h * esz; p.c_bs = (long)M * 2 * h; p.ldc = 2 * h;
   p.H1 = (void*)H1; p.H3 = (void*)H3; p.h_bs = (long)M * h; p.ldh = h;
+  p.dsp = dsp; p.dsp_ld = dsp_parts(dtype, h);
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
   if (W2T) {   // B[n, k] = W2T[n, k]: K-contiguous

@@ -171,16 +171,13 @@ hipError_t run_combine(const T* Src, const float* S, const int32_t* slotT, const
 }
 
 // ---------------------------------------------------------------- backward gather
-// One wave per expert row (j, r), token i = sel[j, r]:
-//   dO[j, r] = S[i, j] dY[i],  dSp[j, r] = <dY[i], O[j, r]>.
+// One wave per expert row (j, r), token i = sel[j, r]: dO[j, r] = S[i, j] dY[i].
 template <typename T>
 __global__ __launch_bounds__(256) void bwd_gather_kernel(const T* __restrict__ dY,
-                                                         const T* __restrict__ O,
                                                          const float* __restrict__ S,
                                                          const int32_t* __restrict__ sel,
-                                                         T* __restrict__ dO,
-                                                         float* __restrict__ dSp, int N, int E,
-                                                         int K, int d) {
+                                                         T* __restrict__ dO, int N, int E, int K,
+                                                         int d) {
   const int lane = threadIdx.x & 63;
   const long r = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
   const long rows = (long)E * K;
@@ -190,36 +187,37 @@ __global__ __launch_bounds__(256) void bwd_gather_kernel(const T* __restrict__ d
   if ((unsigned)i >= (unsigned)N) return;  // never for a valid selection
   const float g = S[(size_t)i * E + j];
   const T* y = dY + (size_t)i * d;
-  const T* o = O + (size_t)r * d;
   T* out = dO + (size_t)r * d;
   const int nch = d >> 3;
-  float dot = 0.f;
-  for (int c = lane; c < nch; c += 64) {
-    float vy[8], vo[8];
-    Elem<T>::load8(y + c * 8, vy);
-    Elem<T>::load8(o + c * 8, vo);
+  for (int c0 = 0; c0 < nch; c0 += 128) {
+    // two 16-byte chunks per lane in flight before either is stored
+    float v0[8], v1[8];
+    const int c1 = c0 + lane, c2 = c0 + 64 + lane;
+    if (c1 < nch) Elem<T>::load8(y + c1 * 8, v0);
+    if (c2 < nch) Elem<T>::load8(y + c2 * 8, v1);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      dot = fmaf(vy[e], vo[e], dot);
-      vy[e] *= g;
+      v0[e] *= g;
+      v1[e] *= g;
     }
-    Elem<T>::store8(out + c * 8, vy);
+    if (c1 < nch) Elem<T>::store8(out + c1 * 8, v0);
+    if (c2 < nch) Elem<T>::store8(out + c2 * 8, v1);
   }
-#pragma unroll
-  for (int s = 32; s >= 1; s >>= 1) dot += __shfl_xor(dot, s, 64);
-  if (lane == 0) dSp[r] = dot;
 }
 
 // ---------------------------------------------------------------- router dZ
-// dZ[i, :] = S_i * (dS_i - <S_i, dS_i>) / tau with dS_ij = dSp[j, slot_ij] on
-// the selection and 0 elsewhere.  Writes fp32 dZ [N, E] and, if dZb is given,
+// dZ[i, :] = S_i * (dS_i - <S_i, dS_i>) / tau = (u_i - S_i sum_j u_ij) / tau with
+// u_ij = S_ij dS_ij: on the selection the sum of the dA product's partials of
+// row (j, slot_ij) (they carry the gate, since dO = S_ij dY_i), 0 off it; dS
+// itself is never formed.  Writes fp32 dZ [N, E] and, if dZb is given,
 // a bf16 copy [N, EP] whose columns E..EP-1 are zero.  A workgroup stages a
 // tile of `tok` (<= RZ_TOK) tokens through LDS so that every global access is
 // coalesced; the tile keeps the dynamic LDS under 64 KiB for any E <= 256.
 constexpr int RZ_TOK = 32;
 
 __global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict__ S,
-                                                        const float* __restrict__ dSp,
+                                                        const float* __restrict__ dsp,
+                                                        int nparts,
                                                         const int32_t* __restrict__ slotT,
                                                         float* __restrict__ dZ,
                                                         bf16_t* __restrict__ dZb, int N, int E,
@@ -227,7 +225,7 @@ __global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict_
   extern __shared__ float rz_lds[];
   const int LD = E + 1;
   float* sS = rz_lds;              // [tok][E+1]
-  float* sD = rz_lds + tok * LD;   // [tok][E+1]
+  float* sU = rz_lds + tok * LD;   // [tok][E+1]
   __shared__ float sdot[RZ_TOK];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i0 = blockIdx.x * tok;
@@ -238,17 +236,20 @@ __global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict_
   }
   for (int c = tid; c < E * tok; c += 256) {           // slot tile: tok tokens per expert
     const int j = c / tok, t = c % tok;
-    float ds = 0.f;
+    float u = 0.f;
     if (t < nt) {
       const int r = slotT[(size_t)j * N + i0 + t];
-      if (r >= 0 && r < K) ds = dSp[(size_t)j * K + r];
+      if (r >= 0 && r < K) {
+        const float* pp = dsp + ((size_t)j * K + r) * nparts;
+        for (int q = 0; q < nparts; ++q) u += pp[q];   // fixed order
+      }
     }
-    sD[t * LD + j] = ds;
+    sU[t * LD + j] = u;
   }
   __syncthreads();
-  for (int t = wave; t < nt; t += 4) {                 // <S_t, dS_t>, one wave per token
+  for (int t = wave; t < nt; t += 4) {                 // <S_t, dS_t> = sum_j u_tj, a wave per token
     float v = 0.f;
-    for (int j = lane; j < E; j += 64) v = fmaf(sS[t * LD + j], sD[t * LD + j], v);
+    for (int j = lane; j < E; j += 64) v += sU[t * LD + j];
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
     if (lane == 0) sdot[t] = v;
@@ -256,12 +257,12 @@ __global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict_
   __syncthreads();
   for (int c = tid; c < nt * E; c += 256) {
     const int t = c / E, j = c % E;
-    dZ[(size_t)i0 * E + c] = sS[t * LD + j] * (sD[t * LD + j] - sdot[t]) * inv_tau;
+    dZ[(size_t)i0 * E + c] = (sU[t * LD + j] - sS[t * LD + j] * sdot[t]) * inv_tau;
   }
   if (dZb) {
     for (int c = tid; c < nt * EP; c += 256) {
       const int t = c / EP, j = c % EP;
-      const float z = (j < E) ? sS[t * LD + j] * (sD[t * LD + j] - sdot[t]) * inv_tau : 0.f;
+      const float z = (j < E) ? (sU[t * LD + j] - sS[t * LD + j] * sdot[t]) * inv_tau : 0.f;
       dZb[(size_t)i0 * EP + c] = (bf16_t)f32_to_bf16(z);
     }
   }
@@ -337,29 +338,29 @@ hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, 
                              E, K, d, st, K);
 }
 
-hipError_t launch_bwd_gather(int dtype, const void* dY, const void* O, const float* S,
-                             const int32_t* sel_token, void* dO, float* dSp, int N, int E, int K,
-                             int d, hipStream_t st) {
+hipError_t launch_bwd_gather(int dtype, const void* dY, const float* S,
+                             const int32_t* sel_token, void* dO, int N, int E, int K, int d,
+                             hipStream_t st) {
   const long rows = (long)E * K;
   if (rows == 0) return hipSuccess;
   const long grid = (rows + 3) / 4;
   if (dtype == DT_F32)
     bwd_gather_kernel<float><<<dim3((unsigned)grid), 256, 0, st>>>(
-        (const float*)dY, (const float*)O, S, sel_token, (float*)dO, dSp, N, E, K, d);
+        (const float*)dY, S, sel_token, (float*)dO, N, E, K, d);
   else
     bwd_gather_kernel<bf16_t><<<dim3((unsigned)grid), 256, 0, st>>>(
-        (const bf16_t*)dY, (const bf16_t*)O, S, sel_token, (bf16_t*)dO, dSp, N, E, K, d);
+        (const bf16_t*)dY, S, sel_token, (bf16_t*)dO, N, E, K, d);
   return hipGetLastError();
 }
 
-hipError_t launch_router_dz(const float* S, const float* dSp, const int32_t* slotT, float* dZ,
-                            bf16_t* dZb, int N, int E, int EP, int K, float inv_tau,
+hipError_t launch_router_dz(const float* S, const float* dsp, int nparts, const int32_t* slotT,
+                            float* dZ, uint16_t* dZb, int N, int E, int EP, int K, float inv_tau,
                             hipStream_t st) {
   if (N == 0) return hipSuccess;
   const int tok = E > 128 ? RZ_TOK / 2 : RZ_TOK;
   const size_t lds = (size_t)2 * tok * (E + 1) * sizeof(float);
-  router_dz_kernel<<<(N + tok - 1) / tok, 256, lds, st>>>(S, dSp, slotT, dZ, dZb, N, E, EP, K,
-                                                           inv_tau, tok);
+  router_dz_kernel<<<(N + tok - 1) / tok, 256, lds, st>>>(S, dsp, nparts, slotT, dZ, dZb, N, E,
+                                                           EP, K, inv_tau, tok);
   return hipGetLastError();
 }
 
