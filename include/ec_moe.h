@@ -99,13 +99,14 @@ typedef struct {
 typedef struct {
   size_t S;          /* fp32  [N, E]    router scores                          */
   size_t sel_token;  /* int32 [E, K]    selected token of each expert row       */
+  size_t sel_gate;   /* fp32  [E, K]    its gate S[token, j]                    */
   size_t slot;       /* int32 [E, N]    [j, i]: row of token i in expert j's
                         buffer, or -1 if expert j did not select token i        */
   size_t Xe;         /* dtype [E, K, d] gathered tokens                         */
   size_t H1;         /* dtype [E, K, h] W1 projection                           */
   size_t H3;         /* dtype [E, K, h] W3 projection                           */
-  size_t A;          /* dtype [E, K, h] SiLU(H1) * H3                           */
-  size_t O;          /* dtype [E, K, d] expert outputs (not gate-scaled)        */
+  size_t A;          /* dtype [E, K, h] gate * SiLU(H1) * H3                    */
+  size_t O;          /* dtype [E, K, d] gate-weighted expert outputs A W2^T     */
   size_t Hs1;        /* dtype [N, hs]   shared experts' W1 projection           */
   size_t Hs3;        /* dtype [N, hs]   shared experts' W3 projection           */
   size_t As;         /* dtype [N, hs]   shared experts' SiLU(Hs1) * Hs3         */
@@ -245,8 +246,9 @@ int ec_tc_forward(const ec_problem *p, int32_t top_k, const void *X, const void 
  * Stages of ec_moe_forward: 0 router+softmax, 1 top-k, 2 gather,
  *   3 W1/W3 grouped GEMM + SwiGLU, 4 W2 grouped GEMM, 5 shared W1/W3 + SwiGLU,
  *   6 shared W2, 7 combine (5 and 6 are empty without shared experts).
- * Stages of ec_moe_backward: 0 dY gather + gate gradient, 1 dA grouped GEMM +
- *   SwiGLU backward, 2 dW2, 3 dXe, 4 dW1/dW3, 5 router dZ, 6 router dX,
+ * Stages of ec_moe_backward: 0 dY gather (empty for bf16: the dA product
+ *   reads the selected rows itself), 1 dA grouped GEMM + SwiGLU backward + gate
+ *   gradient partials, 2 dW2, 3 dXe, 4 dW1/dW3, 5 router dZ, 6 router dX,
  *   7 shared dA + SwiGLU backward, 8 shared dW2, 9 shared dX, 10 shared
  *   dW1/dW3 (7-10 empty without shared experts), 11 combine of dXe, 12 dWg.
  * Stages of ec_route: 0 router+softmax, 1 top-k.                              */

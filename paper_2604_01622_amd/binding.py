@@ -41,9 +41,9 @@ class _Problem(ctypes.Structure):
 
 
 class _SavedLayout(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_size_t) for n in ("S", "sel_token", "slot", "Xe", "H1", "H3", "A",
-                                               "O", "Hs1", "Hs3", "As", "W2T", "W13T", "Ws2T",
-                                               "Ws13T", "total")]
+    _fields_ = [(n, ctypes.c_size_t) for n in ("S", "sel_token", "sel_gate", "slot", "Xe", "H1",
+                                               "H3", "A", "O", "Hs1", "Hs3", "As", "W2T", "W13T",
+                                               "Ws2T", "Ws13T", "total")]
 
 
 _lib = None
@@ -312,8 +312,9 @@ def backward(X, Wg, W1, W3, W2, dY, saved, group_offsets, capacity, inv_temperat
 
 
 def saved_views(saved: torch.Tensor, P: Problem) -> dict:
-    """Typed views into a saved-activation buffer (S, sel_token, slot, Xe, H1, H3, A, O, the
-    shared experts' activations, and for bf16 the transposed weights)."""
+    """Typed views into a saved-activation buffer (S, sel_token, sel_gate, slot, Xe, H1, H3,
+    A (gate-scaled), O (gate-weighted), the shared experts' activations, and for bf16 the
+    transposed weights)."""
     lay = P.saved_layout()
     N, d, E, h, K = P.c.n_tokens, P.c.d_model, P.c.n_experts, P.c.d_ff, P.K
     dt = P.dtype
@@ -325,6 +326,7 @@ def saved_views(saved: torch.Tensor, P: Problem) -> dict:
 
     out = {"S": view(lay["S"], (N, E), torch.float32, 4),
             "sel_token": view(lay["sel_token"], (E, K), torch.int32, 4),
+            "sel_gate": view(lay["sel_gate"], (E, K), torch.float32, 4),
             "slot": view(lay["slot"], (E, N), torch.int32, 4),
             "Xe": view(lay["Xe"], (E, K, d), dt, es), "H1": view(lay["H1"], (E, K, h), dt, es),
             "H3": view(lay["H3"], (E, K, h), dt, es), "A": view(lay["A"], (E, K, h), dt, es),

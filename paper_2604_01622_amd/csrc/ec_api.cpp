@@ -115,6 +115,7 @@ struct Carve {
 struct Saved {
   float* S;
   int32_t* sel;
+  float* gate;    // [E, K] S at the selection: the row factors of the expert products
   int32_t* slot;
   void* Xe;
   void* H1;
@@ -137,6 +138,7 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
   Saved s;
   s.S = (float*)c.take((size_t)P.N * P.E * 4);
   s.sel = (int32_t*)c.take((size_t)P.E * P.K * 4);
+  s.gate = (float*)c.take((size_t)P.E * P.K * 4);
   s.slot = (int32_t*)c.take((size_t)P.E * P.N * 4);
   // bf16 inference reads the selected rows of X inside the W1/W3 product and
   // needs no gathered copy
@@ -158,7 +160,7 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
 }
 
 struct BwdWs {
-  void* dO;       // [E, K, d]; reused for dXe once dO is dead
+  void* dYe;      // [E, K, d] selected rows of dY; reused for dXe once dW2 is formed
   float* dsp;     // [E, K, dsp_parts(h)] gate-gradient partials of the dA product
   void* dH;       // [E, K, 2h]
   float* dZ;      // [N, E]
@@ -172,7 +174,7 @@ struct BwdWs {
 
 BwdWs carve_bwd(Carve& c, const Plan& P) {
   BwdWs w;
-  w.dO = c.take((size_t)P.E * P.K * P.d * P.esz);
+  w.dYe = c.take((size_t)P.E * P.K * P.d * P.esz);
   w.dsp = (float*)c.take((size_t)P.E * P.K * ec::dsp_parts(P.dtype, P.h) * 4);
   w.dH = c.take((size_t)P.E * P.K * 2 * P.h * P.esz);
   w.dZ = (float*)c.take((size_t)P.N * P.E * 4);
@@ -419,6 +421,7 @@ int ec_saved_layout_of(const ec_problem* p, ec_saved_layout* out) {
   auto off = [&](const void* q) -> size_t { return q ? (size_t)((const char*)q - base) : m.used; };
   out->S = off(s.S);
   out->sel_token = off(s.sel);
+  out->sel_gate = off(s.gate);
   out->slot = off(s.slot);
   out->Xe = off(s.Xe);
   out->H1 = off(s.H1);
@@ -555,19 +558,22 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
   } else {
     s = carve_saved(c, P, false);
   }
-  EC_TRY(enqueue_route(p, P, X, Wg, s.S, ST, s.sel, nullptr, s.slot, stream));
+  EC_TRY(enqueue_route(p, P, X, Wg, s.S, ST, s.sel, s.gate, s.slot, stream));
   const int M = (int)P.K;
+  // The gate multiplies each expert row inside the W1/W3 product's epilogue
+  // (A = g SiLU(H1) H3, so O = A W2^T is already gate-weighted and the combine
+  // adds rows with weight 1).
   if (P.dtype == EC_BF16) {
     // the W1/W3 product reads the selected rows of X itself (the gather stage is
     // empty); for the backward it also writes them out as Xe
     EC_HIP(mark(3, stream));
     EC_HIP(ec::launch_gemm_w13(P.dtype, X, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
-                               false, s.W13T, s.sel, saved ? s.Xe : nullptr));
+                               false, s.W13T, s.sel, saved ? s.Xe : nullptr, s.gate));
   } else {
     EC_HIP(ec::launch_gather(P.dtype, X, s.sel, s.Xe, (long)P.E * M, P.d, P.N, stream));
     EC_HIP(mark(3, stream));
     EC_HIP(ec::launch_gemm_w13(P.dtype, s.Xe, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
-                               false, s.W13T));
+                               false, s.W13T, nullptr, nullptr, s.gate));
   }
   EC_HIP(mark(4, stream));
   EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream, false, s.W2T));
@@ -583,8 +589,8 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
     EC_HIP(mark(6, stream));
   }
   EC_HIP(mark(7, stream));
-  EC_HIP(ec::launch_combine(P.dtype, s.O, s.S, s.slot, P.hs ? Y : nullptr, Y, P.N, P.E, M, P.d,
-                            stream));
+  EC_HIP(ec::launch_combine(P.dtype, s.O, nullptr, s.slot, P.hs ? Y : nullptr, Y, P.N, P.E, M,
+                            P.d, stream));
   EC_HIP(mark(8, stream));
   return EC_OK;
 }
@@ -628,17 +634,27 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   const BwdWs w = carve_bwd(c, P);
   const int M = (int)P.K;
   const int E = P.E, d = P.d, h = P.h, N = P.N, hs = P.hs;
-  void* dXe = w.dO;  // dO is dead once dW2 is formed
-  // bf16: dA = dO W2 and dXe = dH1 W1 + dH3 W3 read the transposed weights
-  // that the forward's products wrote into `saved`
+  void* dYe = w.dYe;  // [E, K, d] the selected rows of dY (not gate-scaled)
+  void* dXe = w.dYe;  // dYe is dead once dW2 is formed
+  // The saved A carries the gate (A = g SiLU(H1) H3), so dW2 = dYe^T A; the
+  // dA product scales its rows by g (dA = g dYe W2) and its epilogue also sums
+  // dA * SiLU(H1) H3 per row: the gate's gradient times the gate.
+  // bf16: dA and dXe = dH1 W1 + dH3 W3 read the transposed weights that the
+  // forward's products wrote into `saved`, and dA reads the selected rows of dY
+  // itself, writing them out as dYe for dW2 (the gather stage is empty).
   EC_HIP(mark(0, stream));
-  EC_HIP(ec::launch_bwd_gather(P.dtype, dY, s.S, s.sel, w.dO, N, E, M, d, stream));
-  EC_HIP(mark(1, stream));
-  // dA's epilogue also sums dA * A per row: the gate's gradient (times the gate)
-  EC_HIP(ec::launch_gemm_dA(P.dtype, w.dO, W2, s.H1, s.H3, w.dH, E, M, d, h, stream, false,
-                            s.W2T, w.dsp));
+  if (P.dtype == EC_BF16) {
+    EC_HIP(mark(1, stream));
+    EC_HIP(ec::launch_gemm_dA(P.dtype, dY, W2, s.H1, s.H3, w.dH, E, M, d, h, stream, false,
+                              s.W2T, w.dsp, s.sel, dYe, s.gate));
+  } else {
+    EC_HIP(ec::launch_gather(P.dtype, dY, s.sel, dYe, (long)E * M, d, N, stream));
+    EC_HIP(mark(1, stream));
+    EC_HIP(ec::launch_gemm_dA(P.dtype, dYe, W2, s.H1, s.H3, w.dH, E, M, d, h, stream, false,
+                              s.W2T, w.dsp, nullptr, nullptr, s.gate));
+  }
   EC_HIP(mark(2, stream));
-  EC_HIP(ec::launch_gemm_dW2(P.dtype, w.dO, s.A, dW2, E, M, d, h, stream));
+  EC_HIP(ec::launch_gemm_dW2(P.dtype, dYe, s.A, dW2, E, M, d, h, stream));
   EC_HIP(mark(3, stream));
   EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream, false, s.W13T));
   EC_HIP(mark(4, stream));

@@ -41,12 +41,6 @@ hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_
                           const void* Xr, void* Y, int N, int E, int K, int d, hipStream_t st,
                           long kstride = -1);
 
-// Backward gather: dO[j,r,:] = S[i,j] dY[i,:], i = sel_token[j,r] (the gate's
-// gradient comes out of the dA product's epilogue instead).
-hipError_t launch_bwd_gather(int dtype, const void* dY, const float* S,
-                             const int32_t* sel_token, void* dO, int N, int E, int K, int d,
-                             hipStream_t st);
-
 // Backward combine: dX[i,:] = Xr[i,:] + sum_j dXe[j, slotT[j,i], :]  (Xr may alias dX).
 hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, const void* Xr,
                               void* dX, int N, int E, int K, int d, hipStream_t st);
@@ -77,22 +71,31 @@ int router_dwg_splits(int N, int E, int d);
 // rows (bf16 routed experts, may be null): Xe is then X itself and row m of
 // expert e reads X[rows[e M + m]] (the gather happens in the operand load);
 // XeOut (may be null): the gathered rows are also written there, [E, M, d].
+// gate (may be null): [E, M] fp32, row m of expert e is written as
+// A = gate[e M + m] SiLU(H1) H3 (H1, H3 themselves unscaled).
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
                            bool shared = false, void* W13T = nullptr,
-                           const int32_t* rows = nullptr, void* XeOut = nullptr);
+                           const int32_t* rows = nullptr, void* XeOut = nullptr,
+                           const float* gate = nullptr);
 // O = A W2^T.  W2T (bf16, may be null): also written, [E, h, d] = W2 transposed
 // (what the backward's dA product reads).
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
                           int h, hipStream_t st, bool shared = false, void* W2T = nullptr);
-// dA = dO W2 and the SwiGLU backward: dH[:, 0:h] = dH1, dH[:, h:2h] = dH3 ([E,M,2h]).
+// dA = g dO W2 and the SwiGLU backward: dH[:, 0:h] = dH1, dH[:, h:2h] = dH3
+// ([E,M,2h]), g = gate[e M + m] per row (1 when gate is null).
 // W2T (bf16, may be null): W2 transposed, [E, h, d] (as launch_gemm_w2 writes
 // it); the product then reads K-contiguous weights.  dsp (may be null):
 // [E M, dsp_parts(dtype, h)] fp32, per row and column block the sum of dA * A
-// (A = SiLU(H1) H3), whose row sum is the gate's gradient times the gate.
+// (A = SiLU(H1) H3), whose row sum is the gate's gradient times the gate when
+// dO holds the rows of dY.  rows (bf16 with W2T, may be null): dO is then dY
+// itself and row m of expert e reads dY[rows[e M + m]]; dOut (bf16 with W2T,
+// may be null): those gathered rows are also written there, [E, M, d].
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
-                          bool shared = false, const void* W2T = nullptr, float* dsp = nullptr);
+                          bool shared = false, const void* W2T = nullptr, float* dsp = nullptr,
+                          const int32_t* rows = nullptr, void* dOut = nullptr,
+                          const float* gate = nullptr);
 // gate-gradient partials per row of the dA product (blocks of 128 columns of
 // d_ff in bf16, 64 in fp32)
 int dsp_parts(int dtype, int h);

@@ -93,12 +93,18 @@ struct GemmParams {
   void* AC;
   long ac_bs;
   int ldac;
+  // SwiGLU forward and backward, uniform batches only (may be null): a factor
+  // per output row, g = gate[e*gate_bs + m] for row m of batch e.  The forward
+  // writes A = g SiLU(H1) H3 (H1, H3 unscaled); the backward takes dA = g (the
+  // product) before the SwiGLU backward.
+  const float* gate;
+  long gate_bs;
   // SwiGLU backward only (may be null): the gate-gradient partials.  For row m
   // of batch e and each column block q of the output (128 columns in the bf16
   // kernel, 64 in the fp32 one), dsp[(e M + m) dsp_ld + q] = sum over the block
-  // of dA * A with A = SiLU(H1) H3 recomputed from the saved H1, H3 (dA = g dY
-  // W2 for a gated dO, so the sum over all blocks is g times the gate's
-  // gradient).
+  // of dA * A with dA as above and A = SiLU(H1) H3 recomputed from the saved
+  // H1, H3 (so the sum over all blocks is g times the gate's gradient when the
+  // product is dY W2).
   float* dsp;
   int dsp_ld;
   // Variable rows per batch (token choice): batch e owns rows
@@ -197,6 +203,18 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // destinations of the DMA loads (M0) are formed with scalar arithmetic
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % WGM, wn = wave / WGM;
+  // SwiGLU: the row factors of this wave's rows (lane l holds row wm*WM + 64 t
+  // + l), read before the main loop so the epilogue finds them in registers
+  constexpr bool GATED = EPI == EPI_SWIGLU || EPI == EPI_SWIGLU_BWD;
+  constexpr int GR = GATED ? (WM + 63) / 64 : 1;
+  float gate_r[GR];
+  if constexpr (GATED) {
+#pragma unroll
+    for (int t = 0; t < GR; ++t) {
+      const int m = m0 + wm * WM + 64 * t + lane;
+      gate_r[t] = (p.gate && m < M) ? p.gate[(size_t)e * p.gate_bs + m] : 1.f;
+    }
+  }
   const bf16_t* Ab = reinterpret_cast<const bf16_t*>(p.A) + tc.a_off;
   const bf16_t* Bb = reinterpret_cast<const bf16_t*>(p.B) + (size_t)e * p.b_bs;
   const bf16_t* B2b = p.B2 ? reinterpret_cast<const bf16_t*>(p.B2) + (size_t)e * p.b_bs : nullptr;
@@ -639,6 +657,12 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
         const int c = lane + q * 64;
         const int m = mbase + c / CPR;
         const int n = n0 + wn * (EPI == EPI_SWIGLU ? HW : WN) + (c % CPR) * 8;
+        // the row factor, from the lane that holds it (every lane takes part)
+        float g = 1.f;
+        if constexpr (GATED) {
+          const int rr = (c < NCH ? c : NCH - 1) / CPR;   // row within the slice
+          g = __shfl(gate_r[(mi * 32) / 64], (mi * 32) % 64 + rr, 64);
+        }
         if (c >= NCH || m >= M || n >= p.N) continue;
         if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_ADD) {
           const bool second = m >= p.c_split;
@@ -666,7 +690,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
         } else if constexpr (EPI == EPI_SWIGLU) {
           float a[8];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) a[u] = silu_f(v[e][u]) * v3[e][u];
+          for (int u = 0; u < 8; ++u) a[u] = silu_f(v[e][u]) * v3[e][u] * g;
           Elem<bf16_t>::store8((bf16_t*)p.C + tc.c_off + (size_t)m * p.ldc + n, a);
           if (p.H1) {
             const size_t ho = tc.h_off + (size_t)m * p.ldh + n;
@@ -681,7 +705,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
             const uint32_t w1 = h1raw[mi & 1][q][u >> 1], w3 = h3raw[mi & 1][q][u >> 1];
             const float h1 = bf16_to_f32((u & 1) ? (w1 >> 16) : (w1 & 0xffffu));
             const float h3 = bf16_to_f32((u & 1) ? (w3 >> 16) : (w3 & 0xffffu));
-            const float da = v[e][u];
+            const float da = v[e][u] * g;
             const float sg = sigmoid_f(h1);
             const float s1 = h1 * sg;   // SiLU(h1)
             d3[u] = da * s1;
@@ -898,7 +922,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p, int a_kc, i
         *dst = (EPI == EPI_STORE_ADD) ? *dst + acc[i][jj] : acc[i][jj];
       } else if (EPI == EPI_SWIGLU) {
         const float h1 = acc[i][jj], h3 = acc3[i][jj];
-        ((float*)p.C)[c_off + (size_t)m * p.ldc + n] = silu_f(h1) * h3;
+        const float g = p.gate ? p.gate[(size_t)e * p.gate_bs + m] : 1.f;
+        ((float*)p.C)[c_off + (size_t)m * p.ldc + n] = silu_f(h1) * h3 * g;
         if (p.H1) {
           const size_t ho = h_off + (size_t)m * p.ldh + n;
           ((float*)p.H1)[ho] = h1;
@@ -907,7 +932,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p, int a_kc, i
       } else {
         const size_t ho = h_off + (size_t)m * p.ldh + n;
         const float h1 = ((const float*)p.H1)[ho], h3 = ((const float*)p.H3)[ho];
-        const float da = acc[i][jj];
+        const float da = acc[i][jj] * (p.gate ? p.gate[(size_t)e * p.gate_bs + m] : 1.f);
         const float sg = sigmoid_f(h1);
         const size_t off = c_off + (size_t)m * p.ldc + n;
         ((float*)p.C)[off] = da * h3 * sg * (1.0f + h1 * (1.0f - sg));
@@ -979,8 +1004,10 @@ int dsp_parts(int dtype, int h) { return dtype == DT_F32 ? (h + 63) / 64 : (h + 
 
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
-                           bool shared, void* W13T, const int32_t* rows, void* XeOut) {
+                           bool shared, void* W13T, const int32_t* rows, void* XeOut,
+                           const float* gate) {
   GemmParams p = base_params();
+  p.gate = gate; p.gate_bs = M;
   p.A = Xe; p.a_bs = (long)M * d; p.lda = d;
   if (rows) {   // Xe is X itself, row m of expert e is X[rows[e M + m]]
     p.a_bs = 0; p.a_rows = rows; p.a_rows_bs = M;
@@ -1030,10 +1057,16 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
-                          bool shared, const void* W2T, float* dsp) {
-  // dA[m, n] = sum_k dO[m, k] W2[k, n]  (k over d, n over h); epilogue -> dH1, dH3
+                          bool shared, const void* W2T, float* dsp, const int32_t* rows,
+                          void* dOut, const float* gate) {
+  // dA[m, n] = g_m sum_k dO[m, k] W2[k, n]  (k over d, n over h); epilogue -> dH1, dH3
   GemmParams p = base_params();
   p.A = dO; p.a_bs = (long)M * d; p.lda = d;
+  if (rows) {   // dO is dY itself, row m of expert e is dY[rows[e M + m]]
+    p.a_bs = 0; p.a_rows = rows; p.a_rows_bs = M;
+  }
+  p.AC = dOut; p.ac_bs = (long)M * d; p.ldac = d;
+  p.gate = gate; p.gate_bs = M;
   p.B = W2; p.b_bs = (long)d * h; p.ldb = h;
   p.M = M; p.N = h; p.K = d; p.kv_a = d; p.kv_b = d; p.batches = E;
   const size_t esz = dtype == DT_F32 ? 4 : 2;
@@ -1041,13 +1074,20 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
   p.H1 = (void*)H1; p.H3 = (void*)H3; p.h_bs = (long)M * h; p.ldh = h;
   p.dsp = dsp; p.dsp_ld = dsp_parts(dtype, h);
   if (M == 0) return hipSuccess;
-  if (dtype == DT_F32) return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
+  if (dtype == DT_F32) {
+    if (rows || dOut) return hipErrorInvalidValue;   // fp32 reads a gathered dO
+    return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
+  }
+  if (shared && (rows || dOut)) return hipErrorInvalidValue;
   if (W2T) {   // B[n, k] = W2T[n, k]: K-contiguous
     p.B = W2T; p.b_bs = (long)h * d; p.ldb = d;
     if (shared)
       return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
+    if (dOut)
+      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_DA, 2>(p, st);
     return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_DA>(p, st);
   }
+  if (dOut) return hipErrorInvalidValue;   // the copy-out comes with the K-contiguous B
   if (shared)
     return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_DA>(p, st);

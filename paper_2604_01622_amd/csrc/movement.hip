@@ -170,45 +170,10 @@ hipError_t run_combine(const T* Src, const float* S, const int32_t* slotT, const
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- backward gather
-// One wave per expert row (j, r), token i = sel[j, r]: dO[j, r] = S[i, j] dY[i].
-template <typename T>
-__global__ __launch_bounds__(256) void bwd_gather_kernel(const T* __restrict__ dY,
-                                                         const float* __restrict__ S,
-                                                         const int32_t* __restrict__ sel,
-                                                         T* __restrict__ dO, int N, int E, int K,
-                                                         int d) {
-  const int lane = threadIdx.x & 63;
-  const long r = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const long rows = (long)E * K;
-  if (r >= rows) return;
-  const int j = (int)(r / K);
-  const int i = sel[r];
-  if ((unsigned)i >= (unsigned)N) return;  // never for a valid selection
-  const float g = S[(size_t)i * E + j];
-  const T* y = dY + (size_t)i * d;
-  T* out = dO + (size_t)r * d;
-  const int nch = d >> 3;
-  for (int c0 = 0; c0 < nch; c0 += 128) {
-    // two 16-byte chunks per lane in flight before either is stored
-    float v0[8], v1[8];
-    const int c1 = c0 + lane, c2 = c0 + 64 + lane;
-    if (c1 < nch) Elem<T>::load8(y + c1 * 8, v0);
-    if (c2 < nch) Elem<T>::load8(y + c2 * 8, v1);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      v0[e] *= g;
-      v1[e] *= g;
-    }
-    if (c1 < nch) Elem<T>::store8(out + c1 * 8, v0);
-    if (c2 < nch) Elem<T>::store8(out + c2 * 8, v1);
-  }
-}
-
 // ---------------------------------------------------------------- router dZ
 // dZ[i, :] = S_i * (dS_i - <S_i, dS_i>) / tau = (u_i - S_i sum_j u_ij) / tau with
 // u_ij = S_ij dS_ij: on the selection the sum of the dA product's partials of
-// row (j, slot_ij) (they carry the gate, since dO = S_ij dY_i), 0 off it; dS
+// row (j, slot_ij) (they carry the gate: dA = S_ij dY_i W2), 0 off it; dS
 // itself is never formed.  Writes fp32 dZ [N, E] and, if dZb is given,
 // a bf16 copy [N, EP] whose columns E..EP-1 are zero.  A workgroup stages a
 // tile of `tok` (<= RZ_TOK) tokens through LDS so that every global access is
@@ -336,21 +301,6 @@ hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, 
                               E, K, d, st, K);
   return run_combine<bf16_t>((const bf16_t*)dXe, nullptr, slotT, (const bf16_t*)Xr, (bf16_t*)dX, N,
                              E, K, d, st, K);
-}
-
-hipError_t launch_bwd_gather(int dtype, const void* dY, const float* S,
-                             const int32_t* sel_token, void* dO, int N, int E, int K, int d,
-                             hipStream_t st) {
-  const long rows = (long)E * K;
-  if (rows == 0) return hipSuccess;
-  const long grid = (rows + 3) / 4;
-  if (dtype == DT_F32)
-    bwd_gather_kernel<float><<<dim3((unsigned)grid), 256, 0, st>>>(
-        (const float*)dY, S, sel_token, (float*)dO, N, E, K, d);
-  else
-    bwd_gather_kernel<bf16_t><<<dim3((unsigned)grid), 256, 0, st>>>(
-        (const bf16_t*)dY, S, sel_token, (bf16_t*)dO, N, E, K, d);
-  return hipGetLastError();
 }
 
 hipError_t launch_router_dz(const float* S, const float* dsp, int nparts, const int32_t* slotT,
