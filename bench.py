@@ -139,7 +139,7 @@ def stage_work(name, N, d, E, h, K, esz, EP, save_h, splits, hs=0):
         "gemm_w2": (2 * P * d * h, P * h * s + E * d * h * s + P * d * s),
         "combine": (0, E * N * 4 + P * d * s + N * d * s),
         "bwd_gather": (0, P * 4 + 2 * P * d * s),
-        "gemm_dA_swiglu_bwd": (2 * P * d * h, 2 * P * d * s + E * d * h * s + 4 * P * h * s
+        "gemm_dA_swiglu_bwd": (2 * P * d * h, P * d * s + E * d * h * s + 4 * P * h * s
                                + P * parts * 4 + 2 * P * 4),
         "gemm_dW2": (2 * P * d * h, P * d * s + P * h * s + E * d * h * s),
         "gemm_dXe": (4 * P * d * h, 2 * P * h * s + 2 * E * h * d * s + P * d * s),

@@ -102,7 +102,8 @@ typedef struct {
   size_t sel_gate;   /* fp32  [E, K]    its gate S[token, j]                    */
   size_t slot;       /* int32 [E, N]    [j, i]: row of token i in expert j's
                         buffer, or -1 if expert j did not select token i        */
-  size_t Xe;         /* dtype [E, K, d] gathered tokens                         */
+  size_t Xe;         /* fp32 [E, K, d] gathered tokens (bf16: none, = total;
+                        its products read the selected rows of X)               */
   size_t H1;         /* dtype [E, K, h] W1 projection                           */
   size_t H3;         /* dtype [E, K, h] W3 projection                           */
   size_t A;          /* dtype [E, K, h] gate * SiLU(H1) * H3                    */

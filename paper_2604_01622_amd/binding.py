@@ -328,12 +328,14 @@ def saved_views(saved: torch.Tensor, P: Problem) -> dict:
             "sel_token": view(lay["sel_token"], (E, K), torch.int32, 4),
             "sel_gate": view(lay["sel_gate"], (E, K), torch.float32, 4),
             "slot": view(lay["slot"], (E, N), torch.int32, 4),
-            "Xe": view(lay["Xe"], (E, K, d), dt, es), "H1": view(lay["H1"], (E, K, h), dt, es),
+            "H1": view(lay["H1"], (E, K, h), dt, es),
             "H3": view(lay["H3"], (E, K, h), dt, es), "A": view(lay["A"], (E, K, h), dt, es),
             "O": view(lay["O"], (E, K, d), dt, es),
             "Hs1": view(lay["Hs1"], (N, P.c.d_shared), dt, es),
             "Hs3": view(lay["Hs3"], (N, P.c.d_shared), dt, es),
             "As": view(lay["As"], (N, P.c.d_shared), dt, es)}
+    if dt == torch.float32:    # fp32 keeps the gathered rows; bf16 reads them from X
+        out["Xe"] = view(lay["Xe"], (E, K, d), dt, es)
     if dt == torch.bfloat16:   # the transposed weights the training forward writes
         hs = P.c.d_shared
         out["W2T"] = view(lay["W2T"], (E, h, d), dt, es)

@@ -140,9 +140,9 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
   s.sel = (int32_t*)c.take((size_t)P.E * P.K * 4);
   s.gate = (float*)c.take((size_t)P.E * P.K * 4);
   s.slot = (int32_t*)c.take((size_t)P.E * P.N * 4);
-  // bf16 inference reads the selected rows of X inside the W1/W3 product and
-  // needs no gathered copy
-  s.Xe = (with_h || P.dtype != EC_BF16) ? c.take((size_t)P.E * P.K * P.d * P.esz) : nullptr;
+  // bf16 reads the selected rows of X inside the products that use them (the
+  // forward's W1/W3, the backward's dW1/dW3) and needs no gathered copy
+  s.Xe = (P.dtype != EC_BF16) ? c.take((size_t)P.E * P.K * P.d * P.esz) : nullptr;
   s.H1 = with_h ? c.take((size_t)P.E * P.K * P.h * P.esz) : nullptr;
   s.H3 = with_h ? c.take((size_t)P.E * P.K * P.h * P.esz) : nullptr;
   s.A = c.take((size_t)P.E * P.K * P.h * P.esz);
@@ -160,7 +160,7 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
 }
 
 struct BwdWs {
-  void* dYe;      // [E, K, d] selected rows of dY; reused for dXe once dW2 is formed
+  void* dYe;      // [E, K, d] fp32: selected rows of dY; then dXe (both dtypes)
   float* dsp;     // [E, K, dsp_parts(h)] gate-gradient partials of the dA product
   void* dH;       // [E, K, 2h]
   float* dZ;      // [N, E]
@@ -565,15 +565,15 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
   // adds rows with weight 1).
   if (P.dtype == EC_BF16) {
     // the W1/W3 product reads the selected rows of X itself (the gather stage is
-    // empty); for the backward it also writes them out as Xe
+    // empty)
     EC_HIP(mark(3, stream));
     EC_HIP(ec::launch_gemm_w13(P.dtype, X, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
-                               false, s.W13T, s.sel, saved ? s.Xe : nullptr, s.gate));
+                               false, s.W13T, s.sel, s.gate));
   } else {
     EC_HIP(ec::launch_gather(P.dtype, X, s.sel, s.Xe, (long)P.E * M, P.d, P.N, stream));
     EC_HIP(mark(3, stream));
     EC_HIP(ec::launch_gemm_w13(P.dtype, s.Xe, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
-                               false, s.W13T, nullptr, nullptr, s.gate));
+                               false, s.W13T, nullptr, s.gate));
   }
   EC_HIP(mark(4, stream));
   EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream, false, s.W2T));
@@ -634,31 +634,29 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   const BwdWs w = carve_bwd(c, P);
   const int M = (int)P.K;
   const int E = P.E, d = P.d, h = P.h, N = P.N, hs = P.hs;
-  void* dYe = w.dYe;  // [E, K, d] the selected rows of dY (not gate-scaled)
+  void* dYe = w.dYe;  // [E, K, d] the selected rows of dY (not gate-scaled), fp32 only
   void* dXe = w.dYe;  // dYe is dead once dW2 is formed
   // The saved A carries the gate (A = g SiLU(H1) H3), so dW2 = dYe^T A; the
   // dA product scales its rows by g (dA = g dYe W2) and its epilogue also sums
   // dA * SiLU(H1) H3 per row: the gate's gradient times the gate.
   // bf16: dA and dXe = dH1 W1 + dH3 W3 read the transposed weights that the
-  // forward's products wrote into `saved`, and dA reads the selected rows of dY
-  // itself, writing them out as dYe for dW2 (the gather stage is empty).
+  // forward's products wrote into `saved`; dA and dW2 read the selected rows of
+  // dY, dW1/dW3 those of X, inside their operand loads (the gather stage is
+  // empty and no gathered copy exists).
   EC_HIP(mark(0, stream));
-  if (P.dtype == EC_BF16) {
-    EC_HIP(mark(1, stream));
-    EC_HIP(ec::launch_gemm_dA(P.dtype, dY, W2, s.H1, s.H3, w.dH, E, M, d, h, stream, false,
-                              s.W2T, w.dsp, s.sel, dYe, s.gate));
-  } else {
-    EC_HIP(ec::launch_gather(P.dtype, dY, s.sel, dYe, (long)E * M, d, N, stream));
-    EC_HIP(mark(1, stream));
-    EC_HIP(ec::launch_gemm_dA(P.dtype, dYe, W2, s.H1, s.H3, w.dH, E, M, d, h, stream, false,
-                              s.W2T, w.dsp, nullptr, nullptr, s.gate));
-  }
+  const bool bf = P.dtype == EC_BF16;
+  if (!bf) EC_HIP(ec::launch_gather(P.dtype, dY, s.sel, dYe, (long)E * M, d, N, stream));
+  EC_HIP(mark(1, stream));
+  EC_HIP(ec::launch_gemm_dA(P.dtype, bf ? dY : dYe, W2, s.H1, s.H3, w.dH, E, M, d, h, stream,
+                            false, s.W2T, w.dsp, bf ? s.sel : nullptr, s.gate));
   EC_HIP(mark(2, stream));
-  EC_HIP(ec::launch_gemm_dW2(P.dtype, dYe, s.A, dW2, E, M, d, h, stream));
+  EC_HIP(ec::launch_gemm_dW2(P.dtype, bf ? dY : dYe, s.A, dW2, E, M, d, h, stream,
+                             bf ? s.sel : nullptr));
   EC_HIP(mark(3, stream));
   EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream, false, s.W13T));
   EC_HIP(mark(4, stream));
-  EC_HIP(ec::launch_gemm_dW13(P.dtype, w.dH, s.Xe, dW1, dW3, E, M, d, h, stream));
+  EC_HIP(ec::launch_gemm_dW13(P.dtype, w.dH, bf ? X : s.Xe, dW1, dW3, E, M, d, h, stream,
+                              bf ? s.sel : nullptr));
   EC_HIP(mark(5, stream));
   EC_HIP(ec::launch_router_dz(s.S, w.dsp, ec::dsp_parts(P.dtype, h), s.slot, w.dZ, w.dZb, N, E, P.EP, M,
                               p->inv_temperature, stream));

@@ -69,15 +69,13 @@ int router_dwg_splits(int N, int E, int d);
 // W13T (bf16, may be null): also written, [E, d, 2h], row k = W1[:, k] then
 // W3[:, k] (the transposed weights the backward's dX product reads).
 // rows (bf16 routed experts, may be null): Xe is then X itself and row m of
-// expert e reads X[rows[e M + m]] (the gather happens in the operand load);
-// XeOut (may be null): the gathered rows are also written there, [E, M, d].
+// expert e reads X[rows[e M + m]] (the gather happens in the operand load).
 // gate (may be null): [E, M] fp32, row m of expert e is written as
 // A = gate[e M + m] SiLU(H1) H3 (H1, H3 themselves unscaled).
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
                            bool shared = false, void* W13T = nullptr,
-                           const int32_t* rows = nullptr, void* XeOut = nullptr,
-                           const float* gate = nullptr);
+                           const int32_t* rows = nullptr, const float* gate = nullptr);
 // O = A W2^T.  W2T (bf16, may be null): also written, [E, h, d] = W2 transposed
 // (what the backward's dA product reads).
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
@@ -88,14 +86,12 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
 // it); the product then reads K-contiguous weights.  dsp (may be null):
 // [E M, dsp_parts(dtype, h)] fp32, per row and column block the sum of dA * A
 // (A = SiLU(H1) H3), whose row sum is the gate's gradient times the gate when
-// dO holds the rows of dY.  rows (bf16 with W2T, may be null): dO is then dY
-// itself and row m of expert e reads dY[rows[e M + m]]; dOut (bf16 with W2T,
-// may be null): those gathered rows are also written there, [E, M, d].
+// dO holds the rows of dY.  rows (bf16, may be null): dO is then dY itself and
+// row m of expert e reads dY[rows[e M + m]].
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
                           bool shared = false, const void* W2T = nullptr, float* dsp = nullptr,
-                          const int32_t* rows = nullptr, void* dOut = nullptr,
-                          const float* gate = nullptr);
+                          const int32_t* rows = nullptr, const float* gate = nullptr);
 // gate-gradient partials per row of the dA product (blocks of 128 columns of
 // d_ff in bf16, 64 in fp32)
 int dsp_parts(int dtype, int h);
@@ -106,12 +102,15 @@ int dsp_parts(int dtype, int h);
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
                            int E, int M, int d, int h, hipStream_t st, bool shared = false,
                            const void* W13T = nullptr);
-// dW2 = dO^T A  ([E,d,h]).
+// dW2 = dO^T A  ([E,d,h]).  rows (bf16, may be null): dO is then dY itself and
+// row m of expert e reads dY[rows[e M + m]] (the gather happens in the loads).
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
-                           int d, int h, hipStream_t st);
-// dW1 = dH1^T Xe, dW3 = dH3^T Xe  ([E,h,d] each).
+                           int d, int h, hipStream_t st, const int32_t* rows = nullptr);
+// dW1 = dH1^T Xe, dW3 = dH3^T Xe  ([E,h,d] each).  rows (bf16, may be null): Xe
+// is then X itself and row m of expert e reads X[rows[e M + m]].
 hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1, void* dW3,
-                            int E, int M, int d, int h, hipStream_t st);
+                            int E, int M, int d, int h, hipStream_t st,
+                            const int32_t* rows = nullptr);
 
 // Token drop statistic: cnt[i] = #{j : slotT[j, i] >= 0} for i < N, then
 // dropped[g] = #{i in group g : cnt[i] == 0} for the tab.n groups of the table.

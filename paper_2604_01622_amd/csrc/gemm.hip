@@ -87,12 +87,13 @@ struct GemmParams {
   long bt_bs;
   int ldbt;
   int bt_split;
-  // bf16 K-contiguous A only (may be null): A copied out as its tiles pass through
-  // LDS, AC[e*ac_bs + m*ldac + k] = A(m, k) for m < M (with a_rows: the gathered
-  // rows).  Column block nt writes the k-steps kt with kt % NT == nt.
-  void* AC;
-  long ac_bs;
-  int ldac;
+  // bf16 K-major operands (used with the OPT_GA / OPT_GB instantiations): row k
+  // of batch e's A is row ka_rows[e*k_rows_bs + k] of A itself (kb_rows: of
+  // B), so the gather of the selected tokens happens in the operand load when
+  // the contraction runs over an expert's rows
+  const int32_t* ka_rows;
+  const int32_t* kb_rows;
+  long k_rows_bs;
   // SwiGLU forward and backward, uniform batches only (may be null): a factor
   // per output row, g = gate[e*gate_bs + m] for row m of batch e.  The forward
   // writes A = g SiLU(H1) H3 (H1, H3 unscaled); the backward takes dA = g (the
@@ -175,10 +176,12 @@ __device__ __forceinline__ int kc_swz(int row) {
 }
 __device__ __forceinline__ int km_swz(int k) { return (k & 3) << 2; }
 
-// COPY bit 1: write B transposed to p.BT; bit 2: copy A to p.AC (both bf16,
-// K-contiguous operands; see GemmParams).
+// Options of an instantiation (bf16; see GemmParams): OPT_BT writes the
+// K-contiguous B transposed to p.BT, OPT_GA / OPT_GB gather the rows of a
+// K-major A / B through p.ka_rows / p.kb_rows.
+enum { OPT_BT = 1, OPT_GA = 2, OPT_GB = 4 };
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32, int COPY>
+          bool OUT_F32, int OPT>
 __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoord& tc,
                                               char* smem) {
   constexpr int NT = 64 * WGM * WGN;
@@ -224,13 +227,46 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // K-contiguous: the row pointer of the chunk, offset by kt * KSTEP per step.
   // K-major: the chunk's address at k-step 0 (or the zero block for columns
   // past the operand), advanced by KSTEP rows after every issue; rows past the
-  // valid K read the zero block instead.
+  // valid K read the zero block instead.  K-major gathered (OPT_GA / OPT_GB):
+  // the chunk's column in row 0 of the operand (null past its width); the
+  // source rows of the next k-step's 64 rows are held one per lane (fetched
+  // one step ahead, the first two at set-up so that the prologue waits for no
+  // index) and each load takes its row's with a lane read.
+  constexpr bool GA = (OPT & OPT_GA) != 0 && !A_KC, GB = (OPT & OPT_GB) != 0 && !B_KC;
+  static_assert(((OPT & OPT_GA) == 0 || GA) && ((OPT & OPT_GB) == 0 || GB), "K-major gathers");
+  static_assert((!GA || OA::CPR == 32) && (!GB || OB::CPR == 32),
+                "a gathered load covers two k rows of 256 columns");
+  static_assert(!(GA || GB) || KSTEP == 64, "one source row per lane and k-step");
   const bf16_t* a_src[OA::LOADS];
   int a_row[OA::LOADS];
   long a_step[OA::LOADS];
   const bf16_t* b_src[OB::LOADS];
   int b_row[OB::LOADS];
   long b_step[OB::LOADS];
+  // source row of row k (< K) of a gathered operand; rows past kv re-read the
+  // last valid one (their loads take the zero block)
+  auto k_row = [&](const int32_t* rows, int k, int kv) -> int {
+    return rows[(size_t)e * p.k_rows_bs + (k < kv ? k : kv - 1)];
+  };
+  int a_kidx = 0, a_kidx1 = 0, b_kidx = 0, b_kidx1 = 0;
+  if constexpr (GA) {
+    if (p.kv_a > 0) {
+      a_kidx = k_row(p.ka_rows, lane, p.kv_a);
+      a_kidx1 = k_row(p.ka_rows, KSTEP + lane, p.kv_a);
+    }
+  }
+  if constexpr (GB) {
+    if (p.kv_b > 0) {
+      b_kidx = k_row(p.kb_rows, lane, p.kv_b);
+      b_kidx1 = k_row(p.kb_rows, KSTEP + lane, p.kv_b);
+    }
+  }
+  // the source row of k row 2 j + (lane >= 32) of the step (j uniform)
+  auto pick_row = [&](int kidx, int j) -> int {
+    const int lo = __builtin_amdgcn_readlane(kidx, 2 * j);
+    const int hi = __builtin_amdgcn_readlane(kidx, 2 * j + 1);
+    return lane < 32 ? lo : hi;
+  };
 #pragma unroll
   for (int q = 0; q < OA::LOADS; ++q) {
     const int id = (wave * OA::LOADS + q) * 64 + lane;
@@ -248,8 +284,12 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       const int row = id / OA::CPR, lc = (id % OA::CPR) ^ km_swz(row);
       const int col = m0 + lc * 8;   // first column of the chunk
       a_row[q] = row;                // k within the step
-      a_src[q] = col < M ? Ab + (size_t)row * p.lda + col : g_zero_block;
-      a_step[q] = col < M ? (long)KSTEP * p.lda : 0;
+      if constexpr (GA) {
+        a_src[q] = col < M ? reinterpret_cast<const bf16_t*>(p.A) + col : nullptr;
+      } else {
+        a_src[q] = col < M ? Ab + (size_t)row * p.lda + col : g_zero_block;
+        a_step[q] = col < M ? (long)KSTEP * p.lda : 0;
+      }
     }
   }
 #pragma unroll
@@ -272,17 +312,23 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       const int row = id / OB::CPR, lc = (id % OB::CPR) ^ km_swz(row);
       const int col = n0 + lc * 8;
       b_row[q] = row;
-      b_src[q] = col < p.N ? Bb + (size_t)row * p.ldb + col : g_zero_block;
-      b_step[q] = col < p.N ? (long)KSTEP * p.ldb : 0;
+      if constexpr (GB) {
+        b_src[q] = col < p.N ? reinterpret_cast<const bf16_t*>(p.B) + col : nullptr;
+      } else {
+        b_src[q] = col < p.N ? Bb + (size_t)row * p.ldb + col : g_zero_block;
+        b_step[q] = col < p.N ? (long)KSTEP * p.ldb : 0;
+      }
     }
   }
   // Issues k-step kt; the calls come with kt = 0, 1, 2, ... in order.
   // Loads [lo, hi) of k-step kt (A's loads first, then B's); each load of a
   // k-step is issued exactly once and the k-steps in order.
   // K-major rows past the valid K read the zero block; with full_step (a step
-  // known to lie below both kv) the per-load check is skipped.
-  auto issue_part = [&](int kt, int stage, int lo, int hi, auto full_step) {
+  // known to lie below both kv) the per-load check is skipped.  first: k-step
+  // 0 (its successor's source rows are already at hand).
+  auto issue_part = [&](int kt, int stage, int lo, int hi, auto full_step, auto first) {
     constexpr bool FULL = decltype(full_step)::value;
+    constexpr bool FIRST = decltype(first)::value;
     char* base = smem + stage * STAGE_BYTES;
 #pragma unroll
     for (int q = 0; q < OA::LOADS; ++q) {
@@ -290,11 +336,19 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       const bf16_t* g;
       if constexpr (A_KC) {
         g = a_src[q] + kt * KSTEP;
+      } else if constexpr (GA) {
+        const int k = kt * KSTEP + a_row[q];
+        const int src = pick_row(a_kidx, wave * OA::LOADS + q);
+        g = (a_src[q] && (FULL || k < p.kv_a)) ? a_src[q] + (size_t)src * p.lda : g_zero_block;
       } else {
         g = (FULL || kt * KSTEP + a_row[q] < p.kv_a) ? a_src[q] : g_zero_block;
         a_src[q] += a_step[q];
       }
       dma16(g, base + (wave * OA::LOADS + q) * 1024);
+    }
+    if constexpr (GA) {   // every A load of step kt has gone out: rows of step kt + 1
+      if (hi >= OA::LOADS)
+        a_kidx = FIRST ? a_kidx1 : k_row(p.ka_rows, (kt + 1) * KSTEP + lane, p.kv_a);
     }
 #pragma unroll
     for (int q = 0; q < OB::LOADS; ++q) {
@@ -302,15 +356,23 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       const bf16_t* g;
       if constexpr (B_KC) {
         g = b_src[q] + kt * KSTEP;
+      } else if constexpr (GB) {
+        const int k = kt * KSTEP + b_row[q];
+        const int src = pick_row(b_kidx, wave * OB::LOADS + q);
+        g = (b_src[q] && (FULL || k < p.kv_b)) ? b_src[q] + (size_t)src * p.ldb : g_zero_block;
       } else {
         g = (FULL || kt * KSTEP + b_row[q] < p.kv_b) ? b_src[q] : g_zero_block;
         b_src[q] += b_step[q];
       }
       dma16(g, base + OA::BYTES + (wave * OB::LOADS + q) * 1024);
     }
+    if constexpr (GB) {
+      if (hi >= OA::LOADS + OB::LOADS)
+        b_kidx = FIRST ? b_kidx1 : k_row(p.kb_rows, (kt + 1) * KSTEP + lane, p.kv_b);
+    }
   };
-  auto issue = [&](int kt, int stage) {
-    issue_part(kt, stage, 0, OA::LOADS + OB::LOADS, std::false_type{});
+  auto issue = [&](int kt, int stage, auto first) {
+    issue_part(kt, stage, 0, OA::LOADS + OB::LOADS, std::false_type{}, first);
   };
 
   auto b_lds_col = [&](int ni) -> int {
@@ -395,9 +457,10 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   };
   static_assert(3 * LOADS <= 63, "vmcnt range");
   const int KT = (p.K + KSTEP - 1) / KSTEP;
+  if (KT > 0) issue(0, 0, std::true_type{});
 #pragma unroll
-  for (int s2 = 0; s2 < STAGES; ++s2)
-    if (s2 < KT) issue(s2, s2);
+  for (int s2 = 1; s2 < STAGES; ++s2)
+    if (s2 < KT) issue(s2, s2, std::false_type{});
   if (KT > 0) {
     wait_younger(KT - 1 < STAGES - 1 ? KT - 1 : STAGES - 1);
     __builtin_amdgcn_s_barrier();
@@ -421,7 +484,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // reads (lane i gets k = kb + i of four rows each) and one 16-byte store of
   // eight consecutive rows per lane.
   auto write_bt = [&](int kt, int stage) {
-    if constexpr ((COPY & 1) && B_KC && !OUT_F32) {
+    if constexpr ((OPT & OPT_BT) && B_KC && !OUT_F32) {
       const char* sb = smem + stage * STAGE_BYTES + OA::BYTES;
       bf16_t* bt = reinterpret_cast<bf16_t*>(p.BT) + (size_t)e * p.bt_bs;
       constexpr int RB = BN / 32, KB = KSTEP / 16, WAVES = NT / 64;
@@ -456,25 +519,6 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     }
   };
 
-  // The A tile of k-step kt copied out row by row (16-byte chunks; rows past M
-  // are clamped duplicates and are not written).
-  auto write_ac = [&](int kt, int stage) {
-    if constexpr ((COPY & 2) && A_KC && !OUT_F32) {
-      const char* sa = smem + stage * STAGE_BYTES;
-      bf16_t* ac = reinterpret_cast<bf16_t*>(p.AC) + (size_t)e * p.ac_bs;
-      constexpr int CH = KSTEP / 8;
-      static_assert((BM * CH) % NT == 0, "whole chunks per thread");
-#pragma unroll
-      for (int i = 0; i < BM * CH / NT; ++i) {
-        const int id = i * NT + tid;
-        const int row = id / CH, c = id % CH;
-        const u32x4 v = *reinterpret_cast<const u32x4*>(sa + row * (KSTEP * 2) +
-                                                        ((c ^ kc_swz<KSTEP>(row)) << 4));
-        if (m0 + row < M)
-          *reinterpret_cast<u32x4*>(ac + (size_t)(m0 + row) * p.ldac + kt * KSTEP + c * 8) = v;
-      }
-    }
-  };
 
   // Fragment-read instructions per 16-wide k step (a K-major fragment takes
   // two).  Inside a stage the MFMAs on the current fragments alternate with
@@ -499,11 +543,8 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     constexpr bool RF = decltype(refill)::value;
     constexpr bool TAIL = SPLIT_DMA && decltype(tail_part)::value;
     const int stage = kt % STAGES;
-    if constexpr (COPY & 1) {
+    if constexpr (OPT & OPT_BT) {
       if (kt % tc.MT == mt) write_bt(kt, stage);
-    }
-    if constexpr (COPY & 2) {
-      if (kt % tc.NT == nt) write_ac(kt, stage);
     }
     // TAIL: the second part of the previous step's refill goes out in this
     // step's first 16-wide sub-step (it still has a whole step to land)
@@ -515,7 +556,8 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
         {
           const int q0 = DMA_HEAD + kk * TAIL_PER;
           const int q1 = q0 + TAIL_PER < LOADS ? q0 + TAIL_PER : LOADS;
-          issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, q0, q1, std::false_type{});
+          issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, q0, q1, std::false_type{},
+                     std::false_type{});
         }
         load_frags(cur ^ 1, stage, kk + 1);
 #pragma unroll
@@ -543,7 +585,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
         mfma_range(cur, HALF, NMF);
-        if constexpr (RF) issue_part(kt + STAGES, stage, 0, DMA_HEAD, full_refill);
+        if constexpr (RF) issue_part(kt + STAGES, stage, 0, DMA_HEAD, full_refill, std::false_type{});
         // after the final step this reads a stale stage, harmlessly
         load_frags(cur ^ 1, (kt + 1) % STAGES, 0);
 #pragma unroll
@@ -755,7 +797,7 @@ constexpr int dma_smem_bytes() {
 // One output tile per workgroup; consecutive tile ids (same expert) are kept
 // on one XCD so that its L2 serves their shared A rows and B columns.
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32, int TAG, int COPY>
+          bool OUT_F32, int TAG, int OPT>
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(1024)))
   char smem[dma_smem_bytes<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC>()];
@@ -807,22 +849,24 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
   tc.nt = in_grp / gm;
   tc.MT = MT;
   tc.NT = p.NT;
-  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, COPY>(p, tc, smem);
+  gemm_dma_tile<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, OPT>(p, tc, smem);
 }
 
-// COPY: the instantiation that also writes B transposed (bit 1, p.BT) and/or
-// copies A out (bit 2, p.AC); the pointers must be set exactly for those bits.
+// OPT: the options of the instantiation; the pointers of each option must be
+// set exactly when it is.
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
-          bool OUT_F32, int TAG, int COPY = 0>
+          bool OUT_F32, int TAG, int OPT = 0>
 hipError_t run_dma(GemmParams p, hipStream_t st) {
-  if (((COPY & 1) != 0) != (p.BT != nullptr) || ((COPY & 2) != 0) != (p.AC != nullptr))
+  if (((OPT & OPT_BT) != 0) != (p.BT != nullptr) ||
+      ((OPT & OPT_GA) != 0) != (p.ka_rows != nullptr) ||
+      ((OPT & OPT_GB) != 0) != (p.kb_rows != nullptr))
     return hipErrorInvalidValue;
   p.MT = (p.M + BM - 1) / BM;
   p.NT = (EPI == EPI_SWIGLU) ? (p.N + BN / 2 - 1) / (BN / 2) : (p.N + BN - 1) / BN;
   const long ntile = (long)p.batches * p.MT * p.NT;
   if (ntile == 0) return hipSuccess;
   const long grid = (ntile + 7) / 8 * 8;
-  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, COPY>
+  gemm_dma_kernel<BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, OPT>
       <<<dim3((unsigned)grid), 64 * WGM * WGN, 0, st>>>(p);
   return hipGetLastError();
 }
@@ -1004,15 +1048,13 @@ int dsp_parts(int dtype, int h) { return dtype == DT_F32 ? (h + 63) / 64 : (h + 
 
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
-                           bool shared, void* W13T, const int32_t* rows, void* XeOut,
-                           const float* gate) {
+                           bool shared, void* W13T, const int32_t* rows, const float* gate) {
   GemmParams p = base_params();
   p.gate = gate; p.gate_bs = M;
   p.A = Xe; p.a_bs = (long)M * d; p.lda = d;
   if (rows) {   // Xe is X itself, row m of expert e is X[rows[e M + m]]
     p.a_bs = 0; p.a_rows = rows; p.a_rows_bs = M;
   }
-  p.AC = XeOut; p.ac_bs = (long)M * d; p.ldac = d;
   p.B = W1; p.B2 = W3; p.b_bs = (long)h * d; p.ldb = d;
   p.M = M; p.N = h; p.K = d; p.kv_a = d; p.kv_b = d; p.batches = E;
   p.C = A; p.c_bs = (long)M * h; p.ldc = h;
@@ -1020,19 +1062,16 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
   p.BT = W13T; p.bt_bs = (long)d * 2 * h; p.ldbt = 2 * h; p.bt_split = h;   // [E, d, 2h]
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) {
-    if (rows || XeOut) return hipErrorInvalidValue;   // fp32 reads a gathered Xe
+    if (rows) return hipErrorInvalidValue;   // fp32 reads a gathered Xe
     return run_f32<EPI_SWIGLU>(p, 1, 1, st);
   }
   if (shared) {
-    if (rows || XeOut) return hipErrorInvalidValue;   // the shared experts read X as is
+    if (rows) return hipErrorInvalidValue;   // the shared experts read X as is
     if (W13T)
-      return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13, 1>(p, st);
+      return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13, OPT_BT>(p, st);
     return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13>(p, st);
   }
-  if (W13T && XeOut)
-    return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, 3>(p, st);
-  if (W13T) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, 1>(p, st);
-  if (XeOut) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, 2>(p, st);
+  if (W13T) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, OPT_BT>(p, st);
   return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
 }
 
@@ -1048,8 +1087,8 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
   if (W2T) {
     if (shared)
-      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2, 1>(p, st);
-    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2, 1>(p, st);
+      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2, OPT_BT>(p, st);
+    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2, OPT_BT>(p, st);
   }
   if (shared) return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
@@ -1058,14 +1097,13 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
                           bool shared, const void* W2T, float* dsp, const int32_t* rows,
-                          void* dOut, const float* gate) {
+                          const float* gate) {
   // dA[m, n] = g_m sum_k dO[m, k] W2[k, n]  (k over d, n over h); epilogue -> dH1, dH3
   GemmParams p = base_params();
   p.A = dO; p.a_bs = (long)M * d; p.lda = d;
   if (rows) {   // dO is dY itself, row m of expert e is dY[rows[e M + m]]
     p.a_bs = 0; p.a_rows = rows; p.a_rows_bs = M;
   }
-  p.AC = dOut; p.ac_bs = (long)M * d; p.ldac = d;
   p.gate = gate; p.gate_bs = M;
   p.B = W2; p.b_bs = (long)d * h; p.ldb = h;
   p.M = M; p.N = h; p.K = d; p.kv_a = d; p.kv_b = d; p.batches = E;
@@ -1075,19 +1113,16 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
   p.dsp = dsp; p.dsp_ld = dsp_parts(dtype, h);
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) {
-    if (rows || dOut) return hipErrorInvalidValue;   // fp32 reads a gathered dO
+    if (rows) return hipErrorInvalidValue;   // fp32 reads a gathered dO
     return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
   }
-  if (shared && (rows || dOut)) return hipErrorInvalidValue;
+  if (shared && rows) return hipErrorInvalidValue;
   if (W2T) {   // B[n, k] = W2T[n, k]: K-contiguous
     p.B = W2T; p.b_bs = (long)h * d; p.ldb = d;
     if (shared)
       return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
-    if (dOut)
-      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_DA, 2>(p, st);
     return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_DA>(p, st);
   }
-  if (dOut) return hipErrorInvalidValue;   // the copy-out comes with the K-contiguous B
   if (shared)
     return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_DA>(p, st);
@@ -1115,25 +1150,35 @@ hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void
 }
 
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,
-                           int d, int h, hipStream_t st) {
+                           int d, int h, hipStream_t st, const int32_t* rows) {
   // dW2[m, n] = sum_k dO[k, m] A[k, n]  (m over d, n over h, k over the M expert rows)
   GemmParams p = base_params();
   p.A = dO; p.a_bs = (long)M * d; p.lda = d;
   p.B = A; p.b_bs = (long)M * h; p.ldb = h;
   p.M = d; p.N = h; p.K = M; p.kv_a = M; p.kv_b = M; p.batches = E;
   p.C = dW2; p.c_bs = (long)d * h; p.ldc = h;
+  if (rows) {   // dO is dY itself, row k of expert e is dY[rows[e M + k]]
+    if (dtype == DT_F32) return hipErrorInvalidValue;
+    p.a_bs = 0; p.ka_rows = rows; p.k_rows_bs = M;
+    return run_dma<256, 256, 4, 2, 64, 2, false, false, EPI_STORE, false, G_DW2, OPT_GA>(p, st);
+  }
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 0, 0, st);
   return run_dma<256, 256, 4, 2, 64, 2, false, false, EPI_STORE, false, G_DW2>(p, st);
 }
 
 hipError_t launch_gemm_dW13(int dtype, const void* dH, const void* Xe, void* dW1, void* dW3,
-                            int E, int M, int d, int h, hipStream_t st) {
+                            int E, int M, int d, int h, hipStream_t st, const int32_t* rows) {
   // [dW1; dW3][m, n] = sum_k dH[k, m] Xe[k, n]  (m over 2h, n over d)
   GemmParams p = base_params();
   p.A = dH; p.a_bs = (long)M * 2 * h; p.lda = 2 * h;
   p.B = Xe; p.b_bs = (long)M * d; p.ldb = d;
   p.M = 2 * h; p.N = d; p.K = M; p.kv_a = M; p.kv_b = M; p.batches = E;
   p.C = dW1; p.C2 = dW3; p.c_split = h; p.c_bs = (long)h * d; p.ldc = d;
+  if (rows) {   // Xe is X itself, row k of expert e is X[rows[e M + k]]
+    if (dtype == DT_F32) return hipErrorInvalidValue;
+    p.b_bs = 0; p.kb_rows = rows; p.k_rows_bs = M;
+    return run_dma<256, 256, 4, 2, 64, 2, false, false, EPI_STORE, false, G_DW13, OPT_GB>(p, st);
+  }
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 0, 0, st);
   return run_dma<256, 256, 4, 2, 64, 2, false, false, EPI_STORE, false, G_DW13>(p, st);
 }

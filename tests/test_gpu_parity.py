@@ -374,8 +374,8 @@ def test_full_train_bf16():
 ])
 def test_saved_copies_from_the_forward(groups, d, h, cf):
     """The training forward's copies of W2^T, [W1; W3]^T and the shared experts'
-    transposed weights, and of the gathered rows Xe = X[sel], all written from the
-    GEMMs' LDS tiles, are exact."""
+    transposed weights, all written from the GEMMs' LDS tiles, are exact (bf16
+    saves no gathered Xe: the products that need it read the rows of X)."""
     wl = synth.small("wt", groups, d, 8, h, seed=43, capacity_factor=cf, d_shared=128)
     print(f"[case] transposed weights groups={groups} d={d} h={h} cf={cf}", flush=True)
     inp = synth.draw(wl)
@@ -384,8 +384,7 @@ def test_saved_copies_from_the_forward(groups, d, h, cf):
     tr = lambda a: np.ascontiguousarray(np.swapaxes(a, -1, -2))
     assert np.array_equal(host(v["W2T"]), tr(inp.W2))
     assert np.array_equal(host(v["W13T"]), np.concatenate([tr(inp.W1), tr(inp.W3)], axis=2))
-    sel = v["sel_token"].cpu().numpy()
-    assert np.array_equal(host(v["Xe"]), inp.X[sel])
+    assert "Xe" not in v
     Ws1, Ws3, Ws2 = inp.shared
     assert np.array_equal(host(v["Ws2T"]), tr(Ws2))
     assert np.array_equal(host(v["Ws13T"]), np.concatenate([tr(Ws1), tr(Ws3)], axis=1))
