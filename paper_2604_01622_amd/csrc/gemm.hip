@@ -150,7 +150,7 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 __device__ __attribute__((aligned(16))) bf16_t g_zero_block[4096];  // stays zero
 
-__device__ __forceinline__ v4i16 ds_read_tr16(const char* p) {
+__device__ __forceinline__ v4i16 ds_read_tr16(const char* __restrict__ p) {
 #if defined(__HIP_DEVICE_COMPILE__)
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
 #else
