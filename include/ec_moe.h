@@ -111,12 +111,6 @@ typedef struct {
   size_t Hs1;        /* dtype [N, hs]   shared experts' W1 projection           */
   size_t Hs3;        /* dtype [N, hs]   shared experts' W3 projection           */
   size_t As;         /* dtype [N, hs]   shared experts' SiLU(Hs1) * Hs3         */
-  /* bf16 only (offsets equal `total` for fp32): the weights transposed, written
-   * by the forward and read K-contiguous by the backward's dA and dX products. */
-  size_t W2T;        /* bf16 [E, h, d]  W2 transposed                           */
-  size_t W13T;       /* bf16 [E, d, 2h] row k = W1[:, k] then W3[:, k]          */
-  size_t Ws2T;       /* bf16 [hs, d]    Ws2 transposed                          */
-  size_t Ws13T;      /* bf16 [d, 2 hs]  row k = Ws1[:, k] then Ws3[:, k]        */
   size_t total;      /* bytes of the whole buffer                               */
 } ec_saved_layout;
 
@@ -177,9 +171,7 @@ int ec_token_coverage(const ec_problem *p, const int32_t *slot,
  *   Ws1, Ws3 [hs, d] dtype;  Ws2 [d, hs] dtype (NULL when d_shared = 0);
  *   Y [N, d] dtype out.
  * saved: NULL for inference, else ec_saved_layout.total bytes that receive the
- * activations the backward needs (for bf16 also the transposed expert weights,
- * written by the W1/W3 and W2 products as their tiles pass through on-chip
- * memory).  ws: ec_workspace_size(p, 1) bytes.                                 */
+ * activations the backward needs.  ws: ec_workspace_size(p, 1) bytes.         */
 int ec_moe_forward(const ec_problem *p, const void *X, const void *Wg,
                    const void *W1, const void *W3, const void *W2,
                    const void *Ws1, const void *Ws3, const void *Ws2, void *Y,

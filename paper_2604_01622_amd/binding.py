@@ -42,8 +42,7 @@ class _Problem(ctypes.Structure):
 
 class _SavedLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in ("S", "sel_token", "sel_gate", "slot", "Xe", "H1",
-                                               "H3", "A", "O", "Hs1", "Hs3", "As", "W2T", "W13T",
-                                               "Ws2T", "Ws13T", "total")]
+                                               "H3", "A", "O", "Hs1", "Hs3", "As", "total")]
 
 
 _lib = None
@@ -312,9 +311,8 @@ def backward(X, Wg, W1, W3, W2, dY, saved, group_offsets, capacity, inv_temperat
 
 
 def saved_views(saved: torch.Tensor, P: Problem) -> dict:
-    """Typed views into a saved-activation buffer (S, sel_token, sel_gate, slot, Xe, H1, H3,
-    A (gate-scaled), O (gate-weighted), the shared experts' activations, and for bf16 the
-    transposed weights)."""
+    """Typed views into a saved-activation buffer (S, sel_token, sel_gate, slot, Xe (fp32
+    only), H1, H3, A (gate-scaled), O (gate-weighted) and the shared experts' activations)."""
     lay = P.saved_layout()
     N, d, E, h, K = P.c.n_tokens, P.c.d_model, P.c.n_experts, P.c.d_ff, P.K
     dt = P.dtype
@@ -336,13 +334,6 @@ def saved_views(saved: torch.Tensor, P: Problem) -> dict:
             "As": view(lay["As"], (N, P.c.d_shared), dt, es)}
     if dt == torch.float32:    # fp32 keeps the gathered rows; bf16 reads them from X
         out["Xe"] = view(lay["Xe"], (E, K, d), dt, es)
-    if dt == torch.bfloat16:   # the transposed weights the training forward writes
-        hs = P.c.d_shared
-        out["W2T"] = view(lay["W2T"], (E, h, d), dt, es)
-        out["W13T"] = view(lay["W13T"], (E, d, 2 * h), dt, es)
-        if hs:
-            out["Ws2T"] = view(lay["Ws2T"], (hs, d), dt, es)
-            out["Ws13T"] = view(lay["Ws13T"], (d, 2 * hs), dt, es)
     return out
 
 

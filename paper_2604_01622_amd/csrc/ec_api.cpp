@@ -125,13 +125,6 @@ struct Saved {
   void* Hs1;      // shared experts, [N, hs] each (null when there are none)
   void* Hs3;
   void* As;
-  // bf16 training only: the weights transposed, written by the forward's
-  // products as their tiles pass through LDS, read K-contiguous by the
-  // backward's dA and dX products (null otherwise)
-  void* W2T;      // [E, h, d]
-  void* W13T;     // [E, d, 2h]: row k = W1[:, k], then W3[:, k]
-  void* Ws2T;     // [hs, d]
-  void* Ws13T;    // [d, 2 hs]
 };
 
 Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
@@ -151,11 +144,6 @@ Saved carve_saved(Carve& c, const Plan& P, bool with_h) {
   s.Hs1 = (with_h && sh) ? c.take(sh) : nullptr;
   s.Hs3 = (with_h && sh) ? c.take(sh) : nullptr;
   s.As = sh ? c.take(sh) : nullptr;
-  const bool wt = with_h && P.dtype == EC_BF16;
-  s.W2T = wt ? c.take((size_t)P.E * P.h * P.d * 2) : nullptr;
-  s.W13T = wt ? c.take((size_t)P.E * P.d * 2 * P.h * 2) : nullptr;
-  s.Ws2T = (wt && P.hs) ? c.take((size_t)P.hs * P.d * 2) : nullptr;
-  s.Ws13T = (wt && P.hs) ? c.take((size_t)P.d * 2 * P.hs * 2) : nullptr;
   return s;
 }
 
@@ -431,10 +419,6 @@ int ec_saved_layout_of(const ec_problem* p, ec_saved_layout* out) {
   out->Hs1 = off(s.Hs1);
   out->Hs3 = off(s.Hs3);
   out->As = off(s.As);
-  out->W2T = off(s.W2T);
-  out->W13T = off(s.W13T);
-  out->Ws2T = off(s.Ws2T);
-  out->Ws13T = off(s.Ws13T);
   out->total = m.used;
   return EC_OK;
 }
@@ -568,23 +552,23 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
     // empty)
     EC_HIP(mark(3, stream));
     EC_HIP(ec::launch_gemm_w13(P.dtype, X, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
-                               false, s.W13T, s.sel, s.gate));
+                               false, s.sel, s.gate));
   } else {
     EC_HIP(ec::launch_gather(P.dtype, X, s.sel, s.Xe, (long)P.E * M, P.d, P.N, stream));
     EC_HIP(mark(3, stream));
     EC_HIP(ec::launch_gemm_w13(P.dtype, s.Xe, W1, W3, s.A, s.H1, s.H3, P.E, M, P.d, P.h, stream,
-                               false, s.W13T, nullptr, s.gate));
+                               false, nullptr, s.gate));
   }
   EC_HIP(mark(4, stream));
-  EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream, false, s.W2T));
+  EC_HIP(ec::launch_gemm_w2(P.dtype, s.A, W2, s.O, P.E, M, P.d, P.h, stream, false));
   EC_HIP(mark(5, stream));
   if (P.hs) {
     // shared experts on every token; their output goes to Y and the combine adds
     // the routed sum to it
     EC_HIP(ec::launch_gemm_w13(P.dtype, X, Ws1, Ws3, s.As, s.Hs1, s.Hs3, 1, P.N, P.d, P.hs,
-                               stream, true, s.Ws13T));
+                               stream, true));
     EC_HIP(mark(6, stream));
-    EC_HIP(ec::launch_gemm_w2(P.dtype, s.As, Ws2, Y, 1, P.N, P.d, P.hs, stream, true, s.Ws2T));
+    EC_HIP(ec::launch_gemm_w2(P.dtype, s.As, Ws2, Y, 1, P.N, P.d, P.hs, stream, true));
   } else {
     EC_HIP(mark(6, stream));
   }
@@ -639,21 +623,20 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   // The saved A carries the gate (A = g SiLU(H1) H3), so dW2 = dYe^T A; the
   // dA product scales its rows by g (dA = g dYe W2) and its epilogue also sums
   // dA * SiLU(H1) H3 per row: the gate's gradient times the gate.
-  // bf16: dA and dXe = dH1 W1 + dH3 W3 read the transposed weights that the
-  // forward's products wrote into `saved`; dA and dW2 read the selected rows of
-  // dY, dW1/dW3 those of X, inside their operand loads (the gather stage is
-  // empty and no gathered copy exists).
+  // bf16: dA and dXe = dH1 W1 + dH3 W3 read the weights K-major; dA and dW2
+  // read the selected rows of dY, dW1/dW3 those of X, inside their operand
+  // loads (the gather stage is empty and no gathered copy exists).
   EC_HIP(mark(0, stream));
   const bool bf = P.dtype == EC_BF16;
   if (!bf) EC_HIP(ec::launch_gather(P.dtype, dY, s.sel, dYe, (long)E * M, d, N, stream));
   EC_HIP(mark(1, stream));
   EC_HIP(ec::launch_gemm_dA(P.dtype, bf ? dY : dYe, W2, s.H1, s.H3, w.dH, E, M, d, h, stream,
-                            false, s.W2T, w.dsp, bf ? s.sel : nullptr, s.gate));
+                            false, w.dsp, bf ? s.sel : nullptr, s.gate));
   EC_HIP(mark(2, stream));
   EC_HIP(ec::launch_gemm_dW2(P.dtype, bf ? dY : dYe, s.A, dW2, E, M, d, h, stream,
                              bf ? s.sel : nullptr));
   EC_HIP(mark(3, stream));
-  EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream, false, s.W13T));
+  EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dH, W1, W3, dXe, E, M, d, h, stream, false));
   EC_HIP(mark(4, stream));
   EC_HIP(ec::launch_gemm_dW13(P.dtype, w.dH, bf ? X : s.Xe, dW1, dW3, E, M, d, h, stream,
                               bf ? s.sel : nullptr));
@@ -666,13 +649,11 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
   EC_HIP(mark(7, stream));
   if (hs && N > 0) {
     // shared experts: their output gradient is dY itself (no gate)
-    EC_HIP(ec::launch_gemm_dA(P.dtype, dY, Ws2, s.Hs1, s.Hs3, w.dHs, 1, N, d, hs, stream, true,
-                              s.Ws2T));
+    EC_HIP(ec::launch_gemm_dA(P.dtype, dY, Ws2, s.Hs1, s.Hs3, w.dHs, 1, N, d, hs, stream, true));
     EC_HIP(mark(8, stream));
     EC_HIP(ec::launch_shared_dW2(P.dtype, dY, s.As, dWs2, N, d, hs, w.spart, w.s_splits2, stream));
     EC_HIP(mark(9, stream));
-    EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dHs, Ws1, Ws3, dX, 1, N, d, hs, stream, true,
-                               s.Ws13T));
+    EC_HIP(ec::launch_gemm_dXe(P.dtype, w.dHs, Ws1, Ws3, dX, 1, N, d, hs, stream, true));
     EC_HIP(mark(10, stream));
     EC_HIP(ec::launch_shared_dW13(P.dtype, w.dHs, X, dWs1, dWs3, N, d, hs, w.spart,
                                   w.s_splits13, stream));

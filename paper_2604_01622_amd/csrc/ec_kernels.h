@@ -66,42 +66,36 @@ int router_dwg_splits(int N, int E, int d);
 
 // H = Xe W1^T, Xe W3^T -> A = SiLU(H1) * H3 (and H1, H3 if non-null).
 // `shared`: the same product for the shared experts (own kernel symbol).
-// W13T (bf16, may be null): also written, [E, d, 2h], row k = W1[:, k] then
-// W3[:, k] (the transposed weights the backward's dX product reads).
 // rows (bf16 routed experts, may be null): Xe is then X itself and row m of
 // expert e reads X[rows[e M + m]] (the gather happens in the operand load).
 // gate (may be null): [E, M] fp32, row m of expert e is written as
 // A = gate[e M + m] SiLU(H1) H3 (H1, H3 themselves unscaled).
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
-                           bool shared = false, void* W13T = nullptr,
-                           const int32_t* rows = nullptr, const float* gate = nullptr);
-// O = A W2^T.  W2T (bf16, may be null): also written, [E, h, d] = W2 transposed
-// (what the backward's dA product reads).
+                           bool shared = false, const int32_t* rows = nullptr,
+                           const float* gate = nullptr);
+// O = A W2^T.
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
-                          int h, hipStream_t st, bool shared = false, void* W2T = nullptr);
+                          int h, hipStream_t st, bool shared = false);
 // dA = g dO W2 and the SwiGLU backward: dH[:, 0:h] = dH1, dH[:, h:2h] = dH3
-// ([E,M,2h]), g = gate[e M + m] per row (1 when gate is null).
-// W2T (bf16, may be null): W2 transposed, [E, h, d] (as launch_gemm_w2 writes
-// it); the product then reads K-contiguous weights.  dsp (may be null):
+// ([E,M,2h]), g = gate[e M + m] per row (1 when gate is null); W2 is read
+// K-major.  dsp (may be null):
 // [E M, dsp_parts(dtype, h)] fp32, per row and column block the sum of dA * A
 // (A = SiLU(H1) H3), whose row sum is the gate's gradient times the gate when
 // dO holds the rows of dY.  rows (bf16, may be null): dO is then dY itself and
 // row m of expert e reads dY[rows[e M + m]].
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
-                          bool shared = false, const void* W2T = nullptr, float* dsp = nullptr,
-                          const int32_t* rows = nullptr, const float* gate = nullptr);
+                          bool shared = false, float* dsp = nullptr, const int32_t* rows = nullptr,
+                          const float* gate = nullptr);
 // gate-gradient partials per row of the dA product (blocks of 128 columns of
 // d_ff in bf16, 64 in fp32)
 int dsp_parts(int dtype, int h);
 // dXe = dH1 W1 + dH3 W3  ([E,M,d]).
 // shared: dXe += dH1 W1 + dH3 W3 (the shared experts' term added to dX).
-// W13T (required for bf16): [E, d, 2h], row n = column n of W1 then of W3, so
-// that the product reads K-contiguous weights.
+// The weights are read K-major (bf16: h a multiple of 64).
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
-                           int E, int M, int d, int h, hipStream_t st, bool shared = false,
-                           const void* W13T = nullptr);
+                           int E, int M, int d, int h, hipStream_t st, bool shared = false);
 // dW2 = dO^T A  ([E,d,h]).  rows (bf16, may be null): dO is then dY itself and
 // row m of expert e reads dY[rows[e M + m]] (the gather happens in the loads).
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,

@@ -11,8 +11,8 @@
 // global memory by global_load_lds_dwordx4 (no VGPR staging).  K-contiguous
 // operands sit in LDS as 128-byte rows with XOR-swizzled 16-byte chunks
 // (conflict-free fragment reads); K-major operands (the weight gradients'
-// token-row contractions) stay K-major in LDS and are read with the
-// transposing ds_read_b64_tr_b16.  The MFMAs of each k-step alternate with the
+// token-row contractions, and the weights in the dA and dX products) stay
+// K-major in LDS and are read with the transposing ds_read_b64_tr_b16.  The MFMAs of each k-step alternate with the
 // next step's fragment reads and, once the barrier has freed a stage, with its
 // refill's DMA (for K-contiguous products half of it then, half in the next
 // step's first sub-step), so LDS latency hides behind MFMAs in flight.  The
@@ -21,11 +21,10 @@
 // coalesced stores.  Tiles are numbered so that consecutive ones share an
 // expert and stay on one XCD.
 //
-// The W1/W3 product gathers its A rows (the selected tokens) in the operand
-// load.  In the training forward the W1/W3 and W2 products also copy tiles
-// out of LDS as they pass: the gathered rows (for the dW1/dW3 product) and the
-// weights transposed (so that the backward's dX and dA products read them
-// K-contiguous).
+// The products that read the selected tokens' rows (of X, or of the output
+// gradient dY) gather them in the operand load: the W1/W3 and dA products per
+// row of their K-contiguous A, the dW2 and dW1/dW3 products per k row of their
+// K-major operand, so no gathered copy is ever written.
 //
 // fp32: a plain LDS-tiled FMA kernel with the same operand conventions.
 #include <type_traits>
@@ -58,8 +57,9 @@ struct GemmParams {
   long a_rows_bs;
   // B operand, element (n, k) of batch e:
   //   K-contiguous:  B[e*b_bs + n*ldb + k]  (SwiGLU: rows of W1 and W3 side by side)
-  //   N-contiguous:  B[e*b_bs + k*ldb + n]; the fp32 kernel reads rows k >= k_split
-  //                  from B2 instead (B2[e*b_bs + (k-k_split)*ldb + n])
+  //   N-contiguous:  B[e*b_bs + k*ldb + n]; rows k >= k_split come from B2
+  //                  instead (B2[e*b_bs + (k-k_split)*ldb + n]; the bf16 kernel
+  //                  needs k_split to be a multiple of its k-step)
   const void* B;
   const void* B2;
   long b_bs;
@@ -79,14 +79,6 @@ struct GemmParams {
   void* H3;
   long h_bs;
   int ldh;
-  // bf16 with K-contiguous B only (may be null): B transposed, written while its
-  // tiles pass through LDS, BT[e*bt_bs + k*ldbt + n] = B(n, k) (SwiGLU: W3's
-  // rows go to columns bt_split + n).  Row block mt writes the k-steps kt with
-  // kt % MT == mt of its column block, so each element is written once.
-  void* BT;
-  long bt_bs;
-  int ldbt;
-  int bt_split;
   // bf16 K-major operands (used with the OPT_GA / OPT_GB instantiations): row k
   // of batch e's A is row ka_rows[e*k_rows_bs + k] of A itself (kb_rows: of
   // B), so the gather of the selected tokens happens in the operand load when
@@ -137,9 +129,9 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) {
 constexpr int vmcnt_imm(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
 
 // Each operand is K-contiguous (stored [rows][K]) or K-major (stored
-// [K][rows], the backward's transposed products).  A K-major tile is kept K-major in LDS (64 rows of k, its
-// columns contiguous, 16-byte chunks XOR-swizzled by k) and read with the
-// transposing ds_read_b64_tr_b16: in each 16-lane group, lane j addresses the
+// [K][rows]: the backward's transposed products).  A K-major tile is kept
+// K-major in LDS (64 rows of k, its columns contiguous, 16-byte chunks
+// XOR-swizzled by k) and read with the transposing ds_read_b64_tr_b16: in each 16-lane group, lane j addresses the
 // 4 consecutive columns 4*(j%4).. of row kbase + j/4, and lane i receives
 // column i of rows kbase..kbase+3 -- two such reads make one MFMA fragment.
 // Rows past the valid K (ragged tail) and columns past the operand's width are
@@ -176,10 +168,9 @@ __device__ __forceinline__ int kc_swz(int row) {
 }
 __device__ __forceinline__ int km_swz(int k) { return (k & 3) << 2; }
 
-// Options of an instantiation (bf16; see GemmParams): OPT_BT writes the
-// K-contiguous B transposed to p.BT, OPT_GA / OPT_GB gather the rows of a
-// K-major A / B through p.ka_rows / p.kb_rows.
-enum { OPT_BT = 1, OPT_GA = 2, OPT_GB = 4 };
+// Options of an instantiation (bf16; see GemmParams): OPT_GA / OPT_GB gather
+// the rows of a K-major A / B through p.ka_rows / p.kb_rows.
+enum { OPT_GA = 1, OPT_GB = 2 };
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
           bool OUT_F32, int OPT>
 __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoord& tc,
@@ -228,12 +219,15 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // K-major: the chunk's address at k-step 0 (or the zero block for columns
   // past the operand), advanced by KSTEP rows after every issue; rows past the
   // valid K read the zero block instead.  K-major gathered (OPT_GA / OPT_GB):
-  // the chunk's column in row 0 of the operand (null past its width); the
-  // source rows of the next k-step's 64 rows are held one per lane (fetched
-  // one step ahead, the first two at set-up so that the prologue waits for no
-  // index) and each load takes its row's with a lane read.
+  // the chunk's column in row 0 of the operand (clamped into the row: columns
+  // past the width produce outputs that are not stored); the source rows of
+  // the next k-step's 64 rows are held one per lane (fetched one step ahead,
+  // the first two at set-up so that the prologue waits for no index) and each
+  // load takes its row's with a lane read.  Rows past the valid K re-read a
+  // valid row: the other operand, never gathered, reads zeros there.
   constexpr bool GA = (OPT & OPT_GA) != 0 && !A_KC, GB = (OPT & OPT_GB) != 0 && !B_KC;
   static_assert(((OPT & OPT_GA) == 0 || GA) && ((OPT & OPT_GB) == 0 || GB), "K-major gathers");
+  static_assert(!(GA && GB), "one gathered operand: the other zero-fills the ragged K");
   static_assert((!GA || OA::CPR == 32) && (!GB || OB::CPR == 32),
                 "a gathered load covers two k rows of 256 columns");
   static_assert(!(GA || GB) || KSTEP == 64, "one source row per lane and k-step");
@@ -285,7 +279,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       const int col = m0 + lc * 8;   // first column of the chunk
       a_row[q] = row;                // k within the step
       if constexpr (GA) {
-        a_src[q] = col < M ? reinterpret_cast<const bf16_t*>(p.A) + col : nullptr;
+        a_src[q] = reinterpret_cast<const bf16_t*>(p.A) + (col < M ? col : M - 8);
       } else {
         a_src[q] = col < M ? Ab + (size_t)row * p.lda + col : g_zero_block;
         a_step[q] = col < M ? (long)KSTEP * p.lda : 0;
@@ -313,13 +307,18 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       const int col = n0 + lc * 8;
       b_row[q] = row;
       if constexpr (GB) {
-        b_src[q] = col < p.N ? reinterpret_cast<const bf16_t*>(p.B) + col : nullptr;
+        b_src[q] = reinterpret_cast<const bf16_t*>(p.B) + (col < p.N ? col : p.N - 8);
       } else {
         b_src[q] = col < p.N ? Bb + (size_t)row * p.ldb + col : g_zero_block;
         b_step[q] = col < p.N ? (long)KSTEP * p.ldb : 0;
       }
     }
   }
+  // K-major B split at k_split: from row k_split of B to row 0 of B2
+  const long b_jump =
+      (!B_KC && B2b) ? (long)(((intptr_t)B2b - (intptr_t)(Bb + (size_t)p.k_split * p.ldb)) /
+                              (intptr_t)sizeof(bf16_t))
+                     : 0;
   // Issues k-step kt; the calls come with kt = 0, 1, 2, ... in order.
   // Loads [lo, hi) of k-step kt (A's loads first, then B's); each load of a
   // k-step is issued exactly once and the k-steps in order.
@@ -337,9 +336,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       if constexpr (A_KC) {
         g = a_src[q] + kt * KSTEP;
       } else if constexpr (GA) {
-        const int k = kt * KSTEP + a_row[q];
-        const int src = pick_row(a_kidx, wave * OA::LOADS + q);
-        g = (a_src[q] && (FULL || k < p.kv_a)) ? a_src[q] + (size_t)src * p.lda : g_zero_block;
+        g = a_src[q] + (size_t)pick_row(a_kidx, wave * OA::LOADS + q) * p.lda;
       } else {
         g = (FULL || kt * KSTEP + a_row[q] < p.kv_a) ? a_src[q] : g_zero_block;
         a_src[q] += a_step[q];
@@ -357,12 +354,12 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       if constexpr (B_KC) {
         g = b_src[q] + kt * KSTEP;
       } else if constexpr (GB) {
-        const int k = kt * KSTEP + b_row[q];
-        const int src = pick_row(b_kidx, wave * OB::LOADS + q);
-        g = (b_src[q] && (FULL || k < p.kv_b)) ? b_src[q] + (size_t)src * p.ldb : g_zero_block;
+        g = b_src[q] + (size_t)pick_row(b_kidx, wave * OB::LOADS + q) * p.ldb;
       } else {
         g = (FULL || kt * KSTEP + b_row[q] < p.kv_b) ? b_src[q] : g_zero_block;
-        b_src[q] += b_step[q];
+        // the next step's row; at k_split it continues in row 0 of B2
+        const bool jump = (kt + 1) * KSTEP == p.k_split && b_step[q] != 0;
+        b_src[q] += b_step[q] + (jump ? b_jump : 0);
       }
       dma16(g, base + OA::BYTES + (wave * OB::LOADS + q) * 1024);
     }
@@ -479,45 +476,6 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
                                                               acc[mi][ni], 0, 0, 0);
     }
   };
-  // The B tile of k-step kt (BN rows of KSTEP k, K-contiguous in LDS) written
-  // out transposed: each wave moves blocks of 32 rows x 16 k, two transposing
-  // reads (lane i gets k = kb + i of four rows each) and one 16-byte store of
-  // eight consecutive rows per lane.
-  auto write_bt = [&](int kt, int stage) {
-    if constexpr ((OPT & OPT_BT) && B_KC && !OUT_F32) {
-      const char* sb = smem + stage * STAGE_BYTES + OA::BYTES;
-      bf16_t* bt = reinterpret_cast<bf16_t*>(p.BT) + (size_t)e * p.bt_bs;
-      constexpr int RB = BN / 32, KB = KSTEP / 16, WAVES = NT / 64;
-      static_assert((RB * KB) % WAVES == 0, "whole blocks per wave");
-#pragma unroll
-      for (int i = 0; i < RB * KB / WAVES; ++i) {
-        const int b = wave * (RB * KB / WAVES) + i;
-        const int rb = (b % RB) * 32, kb = (b / RB) * 16;
-        v4i16 v[2];
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const int n = rb + 8 * g16 + 4 * hf + (j16 >> 2);
-          const int kc = kb + 4 * (j16 & 3);
-          v[hf] = ds_read_tr16(sb + n * (KSTEP * 2) + (((kc >> 3) ^ kc_swz<KSTEP>(n)) << 4) +
-                               (kc & 7) * 2);
-        }
-        const int r0 = rb + 8 * g16;   // first of this lane's eight rows
-        int col;
-        bool ok;
-        if constexpr (EPI == EPI_SWIGLU) {
-          const int nn = n0 + r0 % (BN / 2);
-          col = (r0 < BN / 2 ? 0 : p.bt_split) + nn;
-          ok = nn < p.N;
-        } else {
-          col = n0 + r0;
-          ok = col < p.N;
-        }
-        if (ok)
-          *reinterpret_cast<u32x4*>(bt + (size_t)(kt * KSTEP + kb + j16) * p.ldbt + col) =
-              __builtin_bit_cast(u32x4, v);
-      }
-    }
-  };
 
 
   // Fragment-read instructions per 16-wide k step (a K-major fragment takes
@@ -543,9 +501,6 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     constexpr bool RF = decltype(refill)::value;
     constexpr bool TAIL = SPLIT_DMA && decltype(tail_part)::value;
     const int stage = kt % STAGES;
-    if constexpr (OPT & OPT_BT) {
-      if (kt % tc.MT == mt) write_bt(kt, stage);
-    }
     // TAIL: the second part of the previous step's refill goes out in this
     // step's first 16-wide sub-step (it still has a whole step to land)
 #pragma unroll
@@ -857,8 +812,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(GemmParams 
 template <int BM, int BN, int WGM, int WGN, int KSTEP, int STAGES, bool A_KC, bool B_KC, int EPI,
           bool OUT_F32, int TAG, int OPT = 0>
 hipError_t run_dma(GemmParams p, hipStream_t st) {
-  if (((OPT & OPT_BT) != 0) != (p.BT != nullptr) ||
-      ((OPT & OPT_GA) != 0) != (p.ka_rows != nullptr) ||
+  if (((OPT & OPT_GA) != 0) != (p.ka_rows != nullptr) ||
       ((OPT & OPT_GB) != 0) != (p.kb_rows != nullptr))
     return hipErrorInvalidValue;
   p.MT = (p.M + BM - 1) / BM;
@@ -1048,7 +1002,7 @@ int dsp_parts(int dtype, int h) { return dtype == DT_F32 ? (h + 63) / 64 : (h + 
 
 hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void* W3, void* A,
                            void* H1, void* H3, int E, int M, int d, int h, hipStream_t st,
-                           bool shared, void* W13T, const int32_t* rows, const float* gate) {
+                           bool shared, const int32_t* rows, const float* gate) {
   GemmParams p = base_params();
   p.gate = gate; p.gate_bs = M;
   p.A = Xe; p.a_bs = (long)M * d; p.lda = d;
@@ -1059,7 +1013,6 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
   p.M = M; p.N = h; p.K = d; p.kv_a = d; p.kv_b = d; p.batches = E;
   p.C = A; p.c_bs = (long)M * h; p.ldc = h;
   p.H1 = H1; p.H3 = H3; p.h_bs = (long)M * h; p.ldh = h;
-  p.BT = W13T; p.bt_bs = (long)d * 2 * h; p.ldbt = 2 * h; p.bt_split = h;   // [E, d, 2h]
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) {
     if (rows) return hipErrorInvalidValue;   // fp32 reads a gathered Xe
@@ -1067,37 +1020,27 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
   }
   if (shared) {
     if (rows) return hipErrorInvalidValue;   // the shared experts read X as is
-    if (W13T)
-      return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13, OPT_BT>(p, st);
     return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13>(p, st);
   }
-  if (W13T) return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13, OPT_BT>(p, st);
   return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
 }
 
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
-                          int h, hipStream_t st, bool shared, void* W2T) {
+                          int h, hipStream_t st, bool shared) {
   GemmParams p = base_params();
   p.A = A; p.a_bs = (long)M * h; p.lda = h;
   p.B = W2; p.b_bs = (long)d * h; p.ldb = h;
   p.M = M; p.N = d; p.K = h; p.kv_a = h; p.kv_b = h; p.batches = E;
   p.C = O; p.c_bs = (long)M * d; p.ldc = d;
-  p.BT = W2T; p.bt_bs = (long)h * d; p.ldbt = d;   // [E, h, d]
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
-  if (W2T) {
-    if (shared)
-      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2, OPT_BT>(p, st);
-    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2, OPT_BT>(p, st);
-  }
   if (shared) return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
 }
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
                           const void* H3, void* dH, int E, int M, int d, int h, hipStream_t st,
-                          bool shared, const void* W2T, float* dsp, const int32_t* rows,
-                          const float* gate) {
+                          bool shared, float* dsp, const int32_t* rows, const float* gate) {
   // dA[m, n] = g_m sum_k dO[m, k] W2[k, n]  (k over d, n over h); epilogue -> dH1, dH3
   GemmParams p = base_params();
   p.A = dO; p.a_bs = (long)M * d; p.lda = d;
@@ -1117,20 +1060,14 @@ hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void*
     return run_f32<EPI_SWIGLU_BWD>(p, 1, 0, st);
   }
   if (shared && rows) return hipErrorInvalidValue;
-  if (W2T) {   // B[n, k] = W2T[n, k]: K-contiguous
-    p.B = W2T; p.b_bs = (long)h * d; p.ldb = d;
-    if (shared)
-      return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
-    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_SWIGLU_BWD, false, G_DA>(p, st);
-  }
+  // B = W2 K-major: B(n, k) = W2[k, n]
   if (shared)
     return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_SH_DA>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_SWIGLU_BWD, false, G_DA>(p, st);
 }
 
 hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void* W3, void* dXe,
-                           int E, int M, int d, int h, hipStream_t st, bool shared,
-                           const void* W13T) {
+                           int E, int M, int d, int h, hipStream_t st, bool shared) {
   // dXe[m, n] = sum_k dH[m, k] W13[k, n], k < h from W1, k >= h from W3
   GemmParams p = base_params();
   p.A = dH; p.a_bs = (long)M * 2 * h; p.lda = 2 * h;
@@ -1140,13 +1077,12 @@ hipError_t launch_gemm_dXe(int dtype, const void* dH, const void* W1, const void
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return shared ? run_f32<EPI_STORE_ADD>(p, 1, 0, st)
                                      : run_f32<EPI_STORE>(p, 1, 0, st);
-  // bf16 reads the transposed weights, B[n, k] = W13T[n, k] (K-contiguous)
-  if (!W13T) return hipErrorInvalidValue;
-  p.B = W13T; p.B2 = nullptr; p.b_bs = (long)d * 2 * h; p.ldb = 2 * h; p.k_split = 1 << 30;
-  // the shared experts' input gradient is added to dX
+  // bf16: B K-major, rows k >= h from W3 (h is a multiple of the k-step); the
+  // shared experts' input gradient is added to dX
+  if (h % 64 != 0) return hipErrorInvalidValue;
   if (shared)
-    return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
-  return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_DXE>(p, st);
+    return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE_ADD, false, G_SH_DXE>(p, st);
+  return run_dma<256, 256, 4, 2, 64, 2, true, false, EPI_STORE, false, G_DXE>(p, st);
 }
 
 hipError_t launch_gemm_dW2(int dtype, const void* dO, const void* A, void* dW2, int E, int M,

@@ -135,12 +135,7 @@ def test_workspace_and_saved_layout():
     assert ls["Hs3"] - ls["Hs1"] >= N * 192 * 2 and ls["As"] - ls["Hs3"] >= N * 192 * 2
     assert ls["total"] - ls["As"] >= N * 192 * 2
     assert Ps.workspace_size(1) > P.workspace_size(1) and Ps.workspace_size(2) > P.workspace_size(2)
-    # bf16: the transposed expert weights follow the activations; fp32 has none
-    assert lay["W13T"] - lay["W2T"] >= E * h * d * 2 and lay["total"] - lay["W13T"] >= E * d * 2 * h * 2
-    assert ls["Ws2T"] - ls["W13T"] >= E * d * 2 * h * 2 and ls["Ws13T"] - ls["Ws2T"] >= 192 * d * 2
-    assert ls["total"] - ls["Ws13T"] >= d * 2 * 192 * 2
     lf = _problem(dtype=torch.float32).saved_layout()
-    assert lf["W2T"] == lf["W13T"] == lf["Ws2T"] == lf["Ws13T"] == lf["total"]
     assert lf["H1"] - lf["Xe"] >= E * K * d * 4 and lf["Xe"] - lf["slot"] >= E * N * 4
 
 

@@ -365,29 +365,23 @@ def test_full_train_bf16():
     assert all(v <= 2e-2 for v in errs.values()), errs
 
 
-# ------------------------------------------------------------------ transposed weights
+# ------------------------------------------------------------------ K-major operands
 
 @pytest.mark.parametrize("groups,d,h,cf", [
-    ([300], 192, 320, 4.0),        # one row block writes every k-step; ragged column blocks
+    ([300], 192, 320, 4.0),        # ragged column blocks; the W1 | W3 split inside a tile
     ([900, 650], 64, 192, 8.0),    # more row blocks than k-steps
     ([2048], 256, 128, 12.0),      # twelve row blocks share four k-steps
 ])
-def test_saved_copies_from_the_forward(groups, d, h, cf):
-    """The training forward's copies of W2^T, [W1; W3]^T and the shared experts'
-    transposed weights, all written from the GEMMs' LDS tiles, are exact (bf16
-    saves no gathered Xe: the products that need it read the rows of X)."""
-    wl = synth.small("wt", groups, d, 8, h, seed=43, capacity_factor=cf, d_shared=128)
-    print(f"[case] transposed weights groups={groups} d={d} h={h} cf={cf}", flush=True)
-    inp = synth.draw(wl)
-    caps = caps_for(wl, inp)
-    v = run_layer(inp, caps, wl.inv_temperatures[0])["views"]
-    tr = lambda a: np.ascontiguousarray(np.swapaxes(a, -1, -2))
-    assert np.array_equal(host(v["W2T"]), tr(inp.W2))
-    assert np.array_equal(host(v["W13T"]), np.concatenate([tr(inp.W1), tr(inp.W3)], axis=2))
-    assert "Xe" not in v
-    Ws1, Ws3, Ws2 = inp.shared
-    assert np.array_equal(host(v["Ws2T"]), tr(Ws2))
-    assert np.array_equal(host(v["Ws13T"]), np.concatenate([tr(Ws1), tr(Ws3)], axis=1))
+def test_kmajor_weights_and_gathered_rows(groups, d, h, cf):
+    """The backward reads the expert weights K-major (dA: W2, dX: W1 then W3
+    along one contraction) and its weight-gradient products gather the rows of
+    X and dY per k row; the training forward saves no gathered or transposed
+    copies (bf16)."""
+    wl = synth.small("km", groups, d, 8, h, seed=43, capacity_factor=cf, d_shared=128,
+                     backward=True)
+    print(f"[case] K-major groups={groups} d={d} h={h} cf={cf}", flush=True)
+    out = full_case(wl)
+    assert "Xe" not in out["views"]
 
 
 # ------------------------------------------------------------------ shared experts
