@@ -490,8 +490,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
   // A stage's refill is issued in two parts: DMA_HEAD loads after the barrier
   // that frees the stage, the rest in the next step's first sub-step (two
   // stages only: the wait at every step end is then for all outstanding loads).
-  // K-contiguous operands only (the K-major products measured slower with it).
-  constexpr bool SPLIT_DMA = STAGES == 2 && KK > 1 && A_KC && B_KC;
+  constexpr bool SPLIT_DMA = STAGES == 2 && KK > 1;
   // (measured: half after the barrier and half in one sub-step beats a quarter
   // then three sub-steps, none after the barrier, or two tail sub-steps)
   constexpr int DMA_HEAD = SPLIT_DMA ? LOADS / 2 : LOADS;
@@ -511,7 +510,7 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
         {
           const int q0 = DMA_HEAD + kk * TAIL_PER;
           const int q1 = q0 + TAIL_PER < LOADS ? q0 + TAIL_PER : LOADS;
-          issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, q0, q1, std::false_type{},
+          issue_part(kt - 1 + STAGES, (kt - 1) % STAGES, q0, q1, full_refill,
                      std::false_type{});
         }
         load_frags(cur ^ 1, stage, kk + 1);
@@ -560,19 +559,22 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
     using T_ = std::true_type;
     using F_ = std::false_type;
     int kt = 0;
+    // refills of the steps below KT - 1 skip the K-major row check when
+    // every such step lies below both kv (the usual case: only the last step
+    // is ragged); with a split refill, so does the second half of such a
+    // refill in the next step
+    const bool full_ok = p.kv_a >= (KT - 1) * KSTEP && p.kv_b >= (KT - 1) * KSTEP;
+    const int n_full = full_ok ? KT - STAGES - 1 : 0;
     if constexpr (SPLIT_DMA) {
       if (KT > STAGES) {
         kstep(0, T_{}, F_{}, F_{});
-        for (kt = 1; kt + STAGES < KT; ++kt) kstep(kt, T_{}, T_{}, F_{});
+        if constexpr (!A_KC || !B_KC)
+          for (kt = 1; kt < n_full; ++kt) kstep(kt, T_{}, T_{}, T_{});
+        for (kt = kt > 1 ? kt : 1; kt + STAGES < KT; ++kt) kstep(kt, T_{}, T_{}, F_{});
         kstep(kt, F_{}, T_{}, F_{});
         ++kt;
       }
     } else {
-      // refills of the steps below KT - 1 skip the K-major row check when
-      // every such step lies below both kv (the usual case: only the last
-      // step is ragged)
-      const bool full_ok = p.kv_a >= (KT - 1) * KSTEP && p.kv_b >= (KT - 1) * KSTEP;
-      const int n_full = full_ok ? KT - STAGES - 1 : 0;
       for (; kt < n_full; ++kt) kstep(kt, T_{}, F_{}, T_{});
       for (; kt + STAGES < KT; ++kt) kstep(kt, T_{}, F_{}, F_{});
     }
