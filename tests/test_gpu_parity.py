@@ -365,6 +365,31 @@ def test_full_train_bf16():
     assert all(v <= 2e-2 for v in errs.values()), errs
 
 
+# ------------------------------------------------------------------ saved activations
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_saved_activations_carry_the_gate(dtype):
+    """The saved buffer holds what the header documents: sel_gate is S at the
+    selection (an exact copy), A = gate * SiLU(H1) * H3 and O = A W2^T, checked
+    against the saved H1, H3 and A themselves (so only the epilogue's arithmetic
+    and the product are under test)."""
+    wl = synth.small(f"gate_{dtype}", [300, 200], 128, 8, 192, dtype=dtype, seed=5,
+                     capacity_factor=3.0)
+    print(f"[case] saved activations {dtype}", flush=True)
+    inp = synth.draw(wl)
+    caps = caps_for(wl, inp)
+    v = run_layer(inp, caps, wl.inv_temperatures[0])["views"]
+    S, sel = v["S"].cpu().numpy(), v["sel_token"].cpu().numpy()
+    g = v["sel_gate"].cpu().numpy()
+    assert np.array_equal(g, S[sel, np.arange(wl.n_experts)[:, None]])
+    H1, H3, A = (ref.widen(host(v[n])) for n in ("H1", "H3", "A"))
+    A_exp = g[..., None].astype(np.float64) * (H1 / (1.0 + np.exp(-H1))) * H3
+    tol = out_tol(wl.dtype)
+    assert rel_l2(A, A_exp) <= tol, rel_l2(A, A_exp)
+    O_exp = np.matmul(A, np.swapaxes(ref.widen(inp.W2), 1, 2))
+    assert rel_l2(host(v["O"]), O_exp) <= tol, rel_l2(host(v["O"]), O_exp)
+
+
 # ------------------------------------------------------------------ K-major operands
 
 @pytest.mark.parametrize("groups,d,h,cf", [
