@@ -609,8 +609,11 @@ __device__ __forceinline__ void gemm_dma_tile(const GemmParams& p, const TileCoo
       const int c = lane + q * 64;
       const int m = mb + c / CPR, n = n0 + wn * WN + (c % CPR) * 8;
       const size_t ho = (m < M && n < p.N) ? tc.h_off + (size_t)m * p.ldh + n : 0;
-      h1raw[mi & 1][q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H1 + ho);
-      h3raw[mi & 1][q] = *reinterpret_cast<const u32x4*>((const bf16_t*)p.H3 + ho);
+      // read once: streaming loads
+      h1raw[mi & 1][q] =
+          __builtin_nontemporal_load(reinterpret_cast<const u32x4*>((const bf16_t*)p.H1 + ho));
+      h3raw[mi & 1][q] =
+          __builtin_nontemporal_load(reinterpret_cast<const u32x4*>((const bf16_t*)p.H3 + ho));
     }
   };
   if constexpr (EPI == EPI_SWIGLU_BWD) {
