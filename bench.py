@@ -8,7 +8,7 @@ Default workload: 8 sequences x 2048 tokens, d = 2048, 64 experts of hidden
 storage, forward + backward.  Prints ONE JSON line on stdout.
 
     python bench.py [--steps K] [--warmup W]
-                    [--workload train|train_shared|static|timestep|fine|tiny]
+                    [--workload train|train_shared|static|timestep|fine|decode|tiny]
 """
 from __future__ import annotations
 
@@ -120,6 +120,12 @@ def _rocm_version():
     return None
 
 
+def WORKLOADS(synth):
+    return {"train": synth.TRAIN_BF16, "train_shared": synth.TRAIN_SHARED_BF16,
+            "static": synth.STATIC_BF16, "timestep": synth.TIMESTEP_BF16,
+            "fine": synth.FINE_BF16, "decode": synth.DECODE_BF16, "tiny": synth.TINY_F32}
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -200,9 +206,7 @@ def run_tc(a):
     import paper_2604_01622_amd as ec
     from paper_2604_01622_amd import binding, synth
 
-    wl = {"train": synth.TRAIN_BF16, "train_shared": synth.TRAIN_SHARED_BF16,
-          "static": synth.STATIC_BF16, "timestep": synth.TIMESTEP_BF16,
-          "fine": synth.FINE_BF16, "tiny": synth.TINY_F32}[a.workload]
+    wl = WORKLOADS(synth)[a.workload]
     torch.cuda.set_device(0)
     log(f"[bench] drawing {wl.name}")
     inp = synth.draw(wl, with_dy=False)
@@ -328,7 +332,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="train",
-                    choices=["train", "train_shared", "static", "timestep", "fine", "tiny"])
+                    choices=["train", "train_shared", "static", "timestep", "fine", "decode",
+                             "tiny"])
     ap.add_argument("--routing", default="ec", choices=["ec", "tc"],
                     help="tc: the token-choice comparison policy (forward), beside expert choice "
                          "with the same number of token-expert pairs")
@@ -373,9 +378,7 @@ def main():
     import paper_2604_01622_amd as ec
     from paper_2604_01622_amd import binding, synth
 
-    wl = {"train": synth.TRAIN_BF16, "train_shared": synth.TRAIN_SHARED_BF16,
-          "static": synth.STATIC_BF16, "timestep": synth.TIMESTEP_BF16,
-          "fine": synth.FINE_BF16, "tiny": synth.TINY_F32}[a.workload]
+    wl = WORKLOADS(synth)[a.workload]
     backward = a.workload in ("train", "train_shared")
     inv_tau = wl.inv_temperatures[0]
     torch.cuda.set_device(0)
@@ -462,6 +465,12 @@ def main():
             st["gbs"] = round(by / (t * 1e-3) / 1e9, 1)
             st["hbm_frac"] = round(by / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
         stages[n] = st
+    # routing as one stage: the router GEMM + softmax and the column top-k together
+    r_ms = stage_ms["router"] + stage_ms["topk"]
+    r_by = sum(stage_work(n, N, d, E, h, K, esz, EP, backward, splits, hs)[1]
+               for n in ("router", "topk"))
+    route = {"ms": round(r_ms, 4), "bytes": r_by, "gbs": round(r_by / (r_ms * 1e-3) / 1e9, 1),
+             "hbm_frac": round(r_by / (r_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
     dom = max(stage_ms, key=stage_ms.get)
     fl, by = stage_work(dom, N, d, E, h, K, esz, EP, backward, splits, hs)
     t_dom = stage_ms[dom] * 1e-3
@@ -493,7 +502,7 @@ def main():
                       "tokens": N, "groups": wl.n_groups, "d_model": d, "experts": E,
                       "d_ff": h, "shared_hidden": hs, "k_per_group": [int(x) for x in caps],
                       "K_tot": K},
-           "stages": stages, "roofline": roof,
+           "stages": stages, "route": route, "roofline": roof,
            "grouped_gemm": {"tflops": round(gemm_fl / (gemm_ms * 1e-3) / 1e12, 1),
                             "mfma_frac": round(gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
 

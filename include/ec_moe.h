@@ -20,9 +20,11 @@
  *    dW1, dW3, dW2.  S, gates and dWg are always fp32; accumulation is fp32.
  *  - The caller owns every buffer (inputs, outputs, the saved activations and
  *    the workspace).  The library allocates no device memory and keeps no
- *    pointer after returning; its only mutable state is per calling thread
- *    (the last error and the optional stage-timing events), so calls from
- *    different threads are independent.
+ *    pointer to a caller's device buffer after returning.  Its only mutable
+ *    state is per calling thread: the last error, and the host array of
+ *    stage-timing events that ec_set_stage_events registers, which the library
+ *    keeps (and records into on later calls) until ec_set_stage_events is
+ *    called again on that thread; calls from different threads are independent.
  *  - Work is enqueued on `stream` and the call returns without waiting for it.
  *    Capacities and group offsets are HOST arrays so that planning needs no
  *    device synchronisation.
@@ -123,9 +125,19 @@ const char *ec_last_error(void);
 /* K_tot = sum_g k_g after validating the problem; -1 on an invalid problem.  */
 int64_t ec_total_capacity(const ec_problem *p);
 
-/* Workspace bytes needed by ec_route (mode 0), ec_moe_forward (mode 1) or
- * ec_moe_backward (mode 2).  0 on an invalid problem (see ec_last_error).    */
+/* Workspace bytes needed by
+ *   mode 0: ec_route;
+ *   mode 1: ec_moe_forward without a saved buffer (inference: the workspace
+ *           then also holds the routing and expert activations);
+ *   mode 2: ec_moe_backward;
+ *   mode 3: ec_moe_forward with a saved buffer (training: the activations go
+ *           to the saved buffer, so the workspace is much smaller).
+ * 0 on an invalid problem or mode (see ec_last_error).                       */
 size_t ec_workspace_size(const ec_problem *p, int mode);
+
+/* Bytes of the saved buffer that ec_moe_forward fills for ec_moe_backward
+ * (= ec_saved_layout.total).  0 on an invalid problem.                       */
+size_t ec_saved_size(const ec_problem *p);
 
 /* Layout of the saved buffer; returns an ec_status.                          */
 int ec_saved_layout_of(const ec_problem *p, ec_saved_layout *out /* HOST */);
@@ -170,8 +182,9 @@ int ec_token_coverage(const ec_problem *p, const int32_t *slot,
  *   W1, W3 [E, h, d] dtype;  W2 [E, d, h] dtype;
  *   Ws1, Ws3 [hs, d] dtype;  Ws2 [d, hs] dtype (NULL when d_shared = 0);
  *   Y [N, d] dtype out.
- * saved: NULL for inference, else ec_saved_layout.total bytes that receive the
- * activations the backward needs.  ws: ec_workspace_size(p, 1) bytes.         */
+ * saved: NULL for inference, else ec_saved_size(p) bytes that receive the
+ * activations the backward needs.  ws: ec_workspace_size(p, 1) bytes without a
+ * saved buffer, ec_workspace_size(p, 3) with one.                              */
 int ec_moe_forward(const ec_problem *p, const void *X, const void *Wg,
                    const void *W1, const void *W3, const void *W2,
                    const void *Ws1, const void *Ws3, const void *Ws2, void *Y,

@@ -217,13 +217,15 @@ def swiglu_ffn_ref(x, W1j, W3j, W2j):
 
 
 def forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 1.0,
-                sel_token=None, shared=None) -> dict:
+                sel_token=None, shared=None, on_expert=None) -> dict:
     """Layer output y_i = sum over experts j that selected i of g_ij FFN_j(x_i),
     with g_ij = S_ij; y_i = 0 when no expert selected token i.  With shared
     experts (Ws1, Ws3, Ws2), their FFN of x_i is added to every y_i.
 
     If sel_token is given it replaces the selection (used to evaluate the layer on
-    the selection another implementation made from its own score matrix)."""
+    the selection another implementation made from its own score matrix).
+    on_expert(j, O_j), if given, receives each expert's gate-weighted outputs
+    O_j[r] = g_{sel[j, r], j} FFN_j(x_{sel[j, r]}) as they are computed."""
     Xf, W1f, W3f, W2f = widen(X), widen(W1), widen(W3), widen(W2)
     S = router_ref(X, Wg, inv_tau)
     sel = select_ref(S, group_offsets, capacity) if sel_token is None else np.asarray(sel_token)
@@ -233,8 +235,10 @@ def forward_ref(X, Wg, W1, W3, W2, group_offsets, capacity, inv_tau: float = 1.0
     for j in range(E):
         rows = sel[j]
         gate[j] = S[rows, j]
-        o = swiglu_ffn_ref(Xf[rows], W1f[j], W3f[j], W2f[j])
-        Y[rows] += gate[j][:, None] * o            # rows are distinct within one expert
+        o = gate[j][:, None] * swiglu_ffn_ref(Xf[rows], W1f[j], W3f[j], W2f[j])
+        Y[rows] += o                               # rows are distinct within one expert
+        if on_expert is not None:
+            on_expert(j, o)
     if shared is not None:
         Y += shared_ffn_ref(Xf, shared)
     return {"S": S, "sel_token": sel, "gate": gate, "Y": Y}
@@ -396,9 +400,11 @@ def shared_grads_units_ref(X, shared, dY, units):
 # ---------------------------------------------------------------------------
 
 def backward_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau: float = 1.0,
-                 sel_token=None, shared=None) -> dict:
+                 sel_token=None, shared=None, on_expert=None) -> dict:
     """Gradients of sum(Y * dY) w.r.t. X, Wg, W1, W3, W2 (and the shared experts'
-    Ws1, Ws3, Ws2 when given: their FFN adds its own dX term).
+    Ws1, Ws3, Ws2 when given: their FFN adds its own dX term).  The forward
+    output Y comes along (the same terms), and on_expert(j, O_j) as in
+    forward_ref.
 
     Chain, per selected pair (i, j) with x = x_i:
       O = W2_j A, A = SiLU(H1) * H3, H1 = W1_j x, H3 = W3_j x, y_i += S_ij O
@@ -419,6 +425,7 @@ def backward_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau: float 
     dW1 = np.zeros_like(W1f)
     dW3 = np.zeros_like(W3f)
     dW2 = np.zeros_like(W2f)
+    Y = np.zeros_like(Xf)
     for j in range(E):
         rows = sel[j]
         x = Xf[rows]
@@ -428,6 +435,9 @@ def backward_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau: float 
         a = h1 * sg * h3
         o = a @ W2f[j].T
         g = S[rows, j]
+        Y[rows] += g[:, None] * o
+        if on_expert is not None:
+            on_expert(j, g[:, None] * o)
         dy = dYf[rows]
         dS[rows, j] = np.sum(dy * o, axis=1)
         do = g[:, None] * dy
@@ -442,10 +452,11 @@ def backward_ref(X, Wg, W1, W3, W2, dY, group_offsets, capacity, inv_tau: float 
     dWg = dZ.T @ Xf
     dX += dZ @ Wgf
     out = {"dX": dX, "dWg": dWg, "dW1": dW1, "dW3": dW3, "dW2": dW2, "dS": dS,
-           "S": S, "sel_token": sel}
+           "S": S, "sel_token": sel, "Y": Y}
     if shared is not None:
         dXs, out["dWs1"], out["dWs3"], out["dWs2"] = shared_backward_ref(Xf, shared, dYf)
         out["dX"] = dX + dXs
+        out["Y"] = Y + shared_ffn_ref(Xf, shared)
     return out
 
 

@@ -21,7 +21,7 @@ EC_F32, EC_BF16 = 0, 1
 SCHEDULERS = {"linear": 0, "linear_rev": 1, "cosine": 2, "cosine_rev": 3, "gaussian": 4,
               "gaussian_rev": 5}
 EXPORTS = ("ec_status_string", "ec_last_error", "ec_total_capacity", "ec_workspace_size",
-           "ec_saved_layout_of", "ec_capacity", "ec_route", "ec_token_coverage", "ec_moe_forward",
+           "ec_saved_size", "ec_saved_layout_of", "ec_capacity", "ec_route", "ec_token_coverage", "ec_moe_forward",
            "ec_moe_backward", "ec_tc_capacity", "ec_tc_workspace_size", "ec_tc_route",
            "ec_tc_forward", "ec_set_stage_events")
 
@@ -66,6 +66,8 @@ def lib() -> ctypes.CDLL:
         L.ec_total_capacity.argtypes = [pp]
         L.ec_workspace_size.restype = sz
         L.ec_workspace_size.argtypes = [pp, ctypes.c_int]
+        L.ec_saved_size.restype = sz
+        L.ec_saved_size.argtypes = [pp]
         L.ec_saved_layout_of.restype = ctypes.c_int
         L.ec_saved_layout_of.argtypes = [pp, ctypes.POINTER(_SavedLayout)]
         L.ec_capacity.restype = ctypes.c_int
@@ -150,6 +152,12 @@ class Problem:
             msg = lib().ec_last_error().decode()
             if msg:
                 raise ECError(1, msg)
+        return int(n)
+
+    def saved_size(self) -> int:
+        n = lib().ec_saved_size(self.ref)
+        if n == 0:
+            raise ECError(2, lib().ec_last_error().decode())
         return int(n)
 
     def saved_layout(self) -> dict:
@@ -281,8 +289,8 @@ def forward(X, Wg, W1, W3, W2, group_offsets, capacity, inv_temperature=1.0, sav
     P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature, shared)
     dev = X.device
     Y = torch.empty_like(X)
-    saved = _empty(P.saved_layout()["total"], dev) if save else None
-    ws = _empty(P.workspace_size(1), dev)
+    saved = _empty(P.saved_size(), dev) if save else None
+    ws = _empty(P.workspace_size(3 if save else 1), dev)
     _check(lib().ec_moe_forward(P.ref, _ptr(X), _ptr(Wg), _ptr(W1), _ptr(W3), _ptr(W2),
                                 *_shared_ptrs(shared), _ptr(Y), _ptr(saved),
                                 0 if saved is None else saved.numel(), _ptr(ws), ws.numel(),
@@ -348,8 +356,8 @@ class Layer:
         self.P = Problem.of(X, Wg, W1.shape[1], group_offsets, capacity, inv_temperature, shared)
         dev = X.device
         self.Y = torch.empty_like(X)
-        self.saved = _empty(self.P.saved_layout()["total"], dev) if training else None
-        self.ws_f = _empty(self.P.workspace_size(1), dev)
+        self.saved = _empty(self.P.saved_size(), dev) if training else None
+        self.ws_f = _empty(self.P.workspace_size(3 if training else 1), dev)
         if training:
             self.ws_b = _empty(self.P.workspace_size(2), dev)
             self.dX = torch.empty_like(X)

@@ -189,10 +189,12 @@ size_t route_ws(const Plan& P, bool need_slot) {
   return c.used;
 }
 
-size_t forward_ws(const Plan& P) {
+// have_saved: the caller passes a saved buffer, which then holds the
+// activations; otherwise the workspace holds them (without H1, H3).
+size_t forward_ws(const Plan& P, bool have_saved) {
   Carve c(nullptr);
   c.take((size_t)P.E * P.N * 4);  // ST
-  carve_saved(c, P, false);       // activations when no saved buffer is given
+  if (!have_saved) carve_saved(c, P, false);
   return c.used;
 }
 
@@ -392,10 +394,17 @@ size_t ec_workspace_size(const ec_problem* p, int mode) {
   if (validate(p, &P) != EC_OK) return 0;
   switch (mode) {
     case 0: return route_ws(P, true);
-    case 1: return forward_ws(P);
+    case 1: return forward_ws(P, false);
     case 2: return backward_ws(P);
+    case 3: return forward_ws(P, true);
     default: fail(EC_ERR_ARG, "unknown workspace mode %d", mode); return 0;
   }
+}
+
+size_t ec_saved_size(const ec_problem* p) {
+  Plan P;
+  if (validate(p, &P) != EC_OK) return 0;
+  return saved_bytes(P);
 }
 
 int ec_saved_layout_of(const ec_problem* p, ec_saved_layout* out) {
@@ -527,7 +536,7 @@ int ec_moe_forward(const ec_problem* p, const void* X, const void* Wg, const voi
   if (saved && saved_bytes_in < saved_bytes(P))
     return fail(EC_ERR_WORKSPACE, "saved buffer %zu bytes < %zu required", saved_bytes_in,
                 saved_bytes(P));
-  const size_t need = forward_ws(P);
+  const size_t need = forward_ws(P, saved != nullptr);
   EC_TRY(check_ptr(ws, "workspace"));
   if (ws_bytes < need)
     return fail(EC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);

@@ -81,9 +81,10 @@ template <> struct Elem<bf16_t> {
     uint4 a;
     a.x = pack_bf16x2(v[0], v[1]); a.y = pack_bf16x2(v[2], v[3]);
     a.z = pack_bf16x2(v[4], v[5]); a.w = pack_bf16x2(v[6], v[7]);
-    // a streaming (non-temporal) store: no kernel here re-reads what it writes,
-    // and the hint keeps the written lines from displacing operands in the
-    // caches (measured: combines -8-9%, the dA product -2%)
+    // a streaming (non-temporal) store: no kernel re-reads its own output within
+    // the same launch (later launches do: W2 and dW2 read A, dA reads H1/H3, the
+    // combine reads O), and the hint keeps the written lines from displacing the
+    // launch's operands in the caches (measured: combines -8-9%, dA -2%)
     __builtin_nontemporal_store(u32x4{a.x, a.y, a.z, a.w}, reinterpret_cast<u32x4*>(p));
   }
   static __device__ __forceinline__ float load1(const bf16_t* p) { return bf16_to_f32(*p); }

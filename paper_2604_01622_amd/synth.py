@@ -155,13 +155,19 @@ FINE_BF16 = Workload("fine_bf16_4x4096_d2048_E128_h768_c8", (4096,) * 4, 2048, 1
 TRAIN_BF16 = dataclasses.replace(TIMESTEP_BF16, name="train_bf16_8x2048_d2048_E64_h1024_c12-8t",
                                  backward=True, dy_seed=4)
 
+# single-sample decoding (Section 5.2): one sequence of 2048 tokens, every expert
+# choosing from that one pool, capacity c(t) = 12 - 8t at the sample's mask ratio
+# (at most k_max = 2048 * 12 / 64 = 384 tokens per expert), forward only
+DECODE_BF16 = Workload("decode_bf16_1x2048_d2048_E64_h1024_c12-8t", (2048,), 2048, 64, 1024,
+                       "bf16", seed=5, c_min=4.0, c_max=12.0)
+
 # the training workload with the 8B-A1B block's 2 shared experts (each of the
 # routed experts' width) added to every token
 TRAIN_SHARED_BF16 = dataclasses.replace(
     TRAIN_BF16, name="train_shared_bf16_8x2048_d2048_E64_h1024_s2x1024_c12-8t", d_shared=2048)
 
 WORKLOADS = {w.name: w for w in (TINY_F32, STATIC_BF16, TIMESTEP_BF16, FINE_BF16, TRAIN_BF16,
-                                 TRAIN_SHARED_BF16)}
+                                 TRAIN_SHARED_BF16, DECODE_BF16)}
 
 
 def small(name: str, group_lengths: Sequence[int], d: int, E: int, h: int, dtype: str = "bf16",

@@ -126,8 +126,9 @@ def test_workspace_and_saved_layout():
     assert lay["H1"] - lay["slot"] >= E * N * 4
     assert lay["Xe"] == lay["total"]     # bf16 gathers the selected rows inside the products
     assert lay["total"] - lay["O"] >= E * K * d * 2
-    for mode in (0, 1, 2):
+    for mode in (0, 1, 2, 3):
         assert P.workspace_size(mode) > 0
+    assert P.saved_size() == lay["total"]
     assert lay["Hs1"] == lay["Hs3"] == lay["As"] == lay["total"]    # no shared experts
     Ps = _problem(d_shared=192)
     ls = Ps.saved_layout()
@@ -175,3 +176,34 @@ def test_tc_validation():
     st = L.ec_tc_forward(P.ref, 2, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, FAKE, None,
                          FAKE, 64, None)
     assert st == EC_ERR_WORKSPACE
+
+
+def test_forward_workspace_with_saved_buffer():
+    """With a saved buffer the forward's activations live there, so its workspace
+    (mode 3) holds only the transposed scores; without one (mode 1) the
+    workspace also carries S, the selection, the slot map, A and O."""
+    L = ec.lib()
+    N, E, K, d, h = 256, 8, 30, 128, 64
+    P = _problem()
+    w1, w3 = P.workspace_size(1), P.workspace_size(3)
+    assert w3 == -(-E * N * 4 // 256) * 256                # ST only
+    assert w1 - w3 >= N * E * 4 + 2 * E * K * 4 + E * N * 4 + E * K * (h + d) * 2
+    # the benchmark's training shapes: about 0.88 GB smaller
+    big = binding.Problem(16384, 2048, 64, 1024, [0] + [2048 * (g + 1) for g in range(8)],
+                          [278, 182, 362, 269, 350, 139, 338, 289], 1.0, torch.bfloat16)
+    assert big.workspace_size(1) - big.workspace_size(3) > 0.85e9
+    NS = (None, None, None)
+    sv = P.saved_size()
+    # with a saved buffer, a mode-3 workspace is enough; one byte less is rejected
+    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, *NS, FAKE, FAKE, sv, FAKE, w3 - 1,
+                          None)
+    assert st == EC_ERR_WORKSPACE
+    # without a saved buffer, the mode-3 size is too small
+    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, *NS, FAKE, None, 0, FAKE, w3, None)
+    assert st == EC_ERR_WORKSPACE
+    assert "workspace" in L.ec_last_error().decode()
+    # a saved buffer one byte short is rejected before the workspace is looked at
+    st = L.ec_moe_forward(P.ref, FAKE, FAKE, FAKE, FAKE, FAKE, *NS, FAKE, FAKE, sv - 1, FAKE, w1,
+                          None)
+    assert st == EC_ERR_WORKSPACE and "saved" in L.ec_last_error().decode()
+    assert L.ec_saved_size(_problem(capacity=[101, 20]).ref) == 0

@@ -510,6 +510,53 @@ def test_tc_restricted_and_override_forms_equal_full():
     assert not full["kept"].all()                          # the caps drop pairs here
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_tc_dropped_pair_gates(seed):
+    """Token choice with drops and k >= 2, built without the oracle's selection
+    code: a token's experts by rank (torch's stable sort of the negated scores),
+    gates normalised over all k chosen experts before any drop, and pair (i, j)
+    kept iff fewer than cap_g earlier tokens of i's group chose j.  A dropped
+    pair's weight is lost; the other pairs keep their pre-drop gates.  Expected
+    output from torch's SwiGLU.  Renormalising over the kept pairs (the other
+    reading) must give a different output on these cases."""
+    rng = np.random.default_rng(900 + seed)
+    lens, E, k = [13, 9], 5, 3
+    inp = _tiny_inputs(lens, 8, E, 12, seed=900 + seed)
+    off = inp.wl.group_offsets
+    cap = [7, 5]
+    S = torch.softmax(torch.from_numpy(ref.widen(inp.X)) @ torch.from_numpy(ref.widen(inp.Wg)).T,
+                      dim=1)
+    order = torch.sort(-S, dim=1, stable=True).indices[:, :k]     # ties: lower expert index
+    picked = torch.gather(S, 1, order)
+    gate = picked / picked.sum(dim=1, keepdim=True)
+    N = sum(lens)
+    kept = torch.zeros((N, k), dtype=torch.bool)
+    for g in range(len(lens)):
+        for i in range(int(off[g]), int(off[g + 1])):
+            for r in range(k):
+                j = int(order[i, r])
+                earlier = int((order[int(off[g]):i] == j).any(dim=1).sum())
+                kept[i, r] = earlier < cap[g]
+    partial = kept.any(dim=1) & (~kept).any(dim=1)        # some pairs kept, some dropped
+    assert int(partial.sum()) >= 2
+    x = torch.from_numpy(ref.widen(inp.X))
+    W = [torch.from_numpy(ref.widen(w)) for w in (inp.W1, inp.W3, inp.W2)]
+    want = torch.zeros_like(x)
+    renorm = torch.zeros_like(x)
+    for i in range(N):
+        kg = gate[i] * kept[i]
+        for r in range(k):
+            if kept[i, r]:
+                j = int(order[i, r])
+                f = _torch_swiglu_t(x[i:i + 1], W[0][j], W[1][j], W[2][j])[0]
+                want[i] += gate[i, r] * f
+                renorm[i] += kg[r] / kg.sum() * f     # kg.sum() > 0: pair r is kept
+    got = ref.tc_forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, cap)
+    assert np.array_equal(got["kept"], kept.numpy())
+    assert np.max(np.abs(got["Y"] - want.numpy())) < 1e-12
+    assert np.max(np.abs(renorm.numpy() - want.numpy())) > 1e-3
+
+
 def test_tc_capacity_rule():
     assert list(ref.tc_capacity_ref([2048, 100], 64, 8, 1.0)) == [256, 13]   # ceil(8 L / 64)
     assert list(ref.tc_capacity_ref([2048], 64, 8, 1.25)) == [320]
@@ -592,3 +639,17 @@ def test_restricted_forms_equal_full_definitions():
         assert np.max(np.abs(g2 - full["dW2"][j])) < 1e-12
     dWg = ref.router_grad_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, sel, inv_tau)
     assert np.max(np.abs(dWg - full["dWg"])) < 1e-12
+    # the backward's Y and the per-expert outputs: the forward's terms, and their
+    # sum over the experts that chose a token is that token's output
+    assert np.max(np.abs(full["Y"] - Y)) < 1e-12
+    for fn in (lambda cb: ref.forward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, off, k, inv_tau,
+                                          on_expert=cb),
+               lambda cb: ref.backward_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, off, k,
+                                           inv_tau, on_expert=cb)):
+        acc, seen = np.zeros_like(Y), []
+        def cb(j, o):
+            seen.append(j)
+            assert o.shape == (int(np.sum(k)), 16)
+            np.add.at(acc, sel[j], o)
+        fn(cb)
+        assert seen == list(range(5)) and np.max(np.abs(acc - Y)) < 1e-12
