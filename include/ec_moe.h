@@ -164,6 +164,24 @@ int ec_route(const ec_problem *p, const void *X, const void *Wg, float *S,
              int32_t *sel_token, float *sel_gate, int32_t *slot,
              void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Routing for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, outputs and errors as ec_route, without the workspace: its
+ * scratch (the transposed scores, E N 4 bytes, and the slot map, another
+ * E N 4 bytes, when slot is NULL) lives in a static device array of
+ * EC_ROUTE_NOALLOC_MAX_BYTES that the library holds on every GPU it runs on
+ * until the process ends; the call allocates nothing and enqueues no memset.
+ * A problem needing more scratch than that returns EC_ERR_WORKSPACE before
+ * anything is enqueued.  Every call on one GPU shares that GPU's array: calls
+ * that overlap on one GPU (on different streams, or from different threads
+ * without ordering) race and give undefined results; calls ordered on one
+ * stream are safe.  The first call on a device looks up the array's address
+ * (hipGetSymbolAddress) with that device current.                           */
+#define EC_ROUTE_NOALLOC_MAX_BYTES ((size_t)16 << 20)
+int ec_route_noalloc(const ec_problem *p, const void *X, const void *Wg, float *S,
+                     int32_t *sel_token, float *sel_gate, int32_t *slot,
+                     hipStream_t stream);
+
 /* Token drop statistic (Appendix D: the fraction of tokens that no routed
  * expert chose, whose layer output is therefore zero).  Reads a slot map as
  * written by ec_route or kept in the saved buffer:

@@ -13,6 +13,7 @@ from .binding import (  # noqa: F401
     forward,
     lib,
     route,
+    route_noalloc,
     saved_views,
     token_coverage,
     tc_capacity,
@@ -22,5 +23,5 @@ from .binding import (  # noqa: F401
     TcLayer,
 )
 
-__all__ = ["ECError", "Problem", "Layer", "TcLayer", "route", "forward", "backward", "capacity",
+__all__ = ["ECError", "Problem", "Layer", "TcLayer", "route", "route_noalloc", "forward", "backward", "capacity",
            "saved_views", "token_coverage", "tc_capacity", "tc_route", "tc_forward", "lib"]

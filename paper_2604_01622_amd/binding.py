@@ -21,7 +21,7 @@ EC_F32, EC_BF16 = 0, 1
 SCHEDULERS = {"linear": 0, "linear_rev": 1, "cosine": 2, "cosine_rev": 3, "gaussian": 4,
               "gaussian_rev": 5}
 EXPORTS = ("ec_status_string", "ec_last_error", "ec_total_capacity", "ec_workspace_size",
-           "ec_saved_size", "ec_saved_layout_of", "ec_capacity", "ec_route", "ec_token_coverage", "ec_moe_forward",
+           "ec_saved_size", "ec_saved_layout_of", "ec_capacity", "ec_route", "ec_route_noalloc", "ec_token_coverage", "ec_moe_forward",
            "ec_moe_backward", "ec_tc_capacity", "ec_tc_workspace_size", "ec_tc_route",
            "ec_tc_forward", "ec_set_stage_events")
 
@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
                                   ctypes.c_double, ctypes.c_int, i32p]
         L.ec_route.restype = ctypes.c_int
         L.ec_route.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.ec_route_noalloc.restype = ctypes.c_int
+        L.ec_route_noalloc.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp]
         L.ec_token_coverage.restype = ctypes.c_int
         L.ec_token_coverage.argtypes = [pp, vp, vp, vp, vp]
         L.ec_moe_forward.restype = ctypes.c_int
@@ -208,6 +210,23 @@ def route(X: torch.Tensor, Wg: torch.Tensor, group_offsets, capacity, inv_temper
     _check(lib().ec_route(P.ref, _ptr(X), _ptr(Wg), _ptr(S), _ptr(sel) if K else None,
                           _ptr(gate) if K else None, _ptr(slot), _ptr(ws), ws.numel(),
                           _stream()))
+    return S, sel, gate, slot
+
+
+def route_noalloc(X: torch.Tensor, Wg: torch.Tensor, group_offsets, capacity,
+                  inv_temperature=1.0, d_ff: int = 64, with_slot: bool = True):
+    """Router + column top-k with the library's static scratch instead of a
+    workspace (ec_route_noalloc).  Returns S, sel_token, sel_gate and slot (None
+    when with_slot is False: the slot map then lives in the scratch)."""
+    P = Problem.of(X, Wg, d_ff, group_offsets, capacity, inv_temperature)
+    N, E, K = X.shape[0], Wg.shape[0], P.K
+    dev = X.device
+    S = torch.empty((N, E), dtype=torch.float32, device=dev)
+    sel = torch.empty((E, K), dtype=torch.int32, device=dev)
+    gate = torch.empty((E, K), dtype=torch.float32, device=dev)
+    slot = torch.empty((E, N), dtype=torch.int32, device=dev) if with_slot else None
+    _check(lib().ec_route_noalloc(P.ref, _ptr(X), _ptr(Wg), _ptr(S), _ptr(sel) if K else None,
+                                  _ptr(gate) if K else None, _ptr(slot), _stream()))
     return S, sel, gate, slot
 
 

@@ -10,6 +10,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "ec_kernels.h"
@@ -355,6 +356,35 @@ int enqueue_tc_route(const ec_problem* p, const Plan& P, int top_k, const void* 
   return EC_OK;
 }
 
+// ---- routing without allocation ---------------------------------------------
+// ec_route_noalloc's workspace: a library-owned device array, one copy per GPU,
+// kept until the process ends.  In host code `scratch` names a host-side stand-in;
+// the device address comes from hipGetSymbolAddress, taken once per device on the
+// entry point's first call there (with that device current) and kept per device.
+constexpr size_t kScratchBytes = EC_ROUTE_NOALLOC_MAX_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array.
+int scratch_of_current_device(void** out) {
+  int dev = -1;
+  EC_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(EC_ERR_HIP, "device index %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    EC_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) return fail(EC_ERR_HIP, "hipGetSymbolAddress returned a null address");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return EC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -488,6 +518,34 @@ int ec_route(const ec_problem* p, const void* X, const void* Wg, float* S, int32
   if (ws_bytes < need)
     return fail(EC_ERR_WORKSPACE, "workspace %zu bytes < %zu required", ws_bytes, need);
   if (P.N == 0) return EC_OK;
+  Carve c(ws);
+  float* ST = (float*)c.take((size_t)P.E * P.N * 4);
+  int32_t* sl = slot ? slot : (int32_t*)c.take((size_t)P.E * P.N * 4);
+  return enqueue_route(p, P, X, Wg, S, ST, sel_token, sel_gate, sl, stream);
+}
+
+int ec_route_noalloc(const ec_problem* p, const void* X, const void* Wg, float* S,
+                     int32_t* sel_token, float* sel_gate, int32_t* slot, hipStream_t stream) {
+  Plan P;
+  EC_TRY(validate(p, &P));
+  EC_TRY(check_ptr(X, "X"));
+  EC_TRY(check_ptr(Wg, "Wg"));
+  EC_TRY(check_ptr(S, "S"));
+  EC_TRY(check_ptr(sel_token, "sel_token", P.K == 0));
+  EC_TRY(check_ptr(sel_gate, "sel_gate", true));
+  EC_TRY(check_ptr(slot, "slot", true));
+  const size_t need = route_ws(P, slot == nullptr);
+  if (need > kScratchBytes)
+    return fail(EC_ERR_WORKSPACE,
+                "ec_route_noalloc: the problem needs %zu bytes of scratch (E N 4 for the "
+                "transposed scores, twice that without a slot buffer); its static array "
+                "holds %zu",
+                need, kScratchBytes);
+  if (P.N == 0) return EC_OK;
+  void* ws = nullptr;
+  EC_TRY(scratch_of_current_device(&ws));
+  // nothing in the scratch must start at zero: the router writes every score of
+  // ST and the top-k writes every entry of the slot map (the groups cover all N)
   Carve c(ws);
   float* ST = (float*)c.take((size_t)P.E * P.N * 4);
   int32_t* sl = slot ? slot : (int32_t*)c.take((size_t)P.E * P.N * 4);

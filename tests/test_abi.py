@@ -207,3 +207,23 @@ def test_forward_workspace_with_saved_buffer():
                           None)
     assert st == EC_ERR_WORKSPACE and "saved" in L.ec_last_error().decode()
     assert L.ec_saved_size(_problem(capacity=[101, 20]).ref) == 0
+
+
+def test_route_noalloc_rejects_problems_beyond_its_scratch():
+    """Validation happens on the host before any HIP call: a problem whose
+    transposed scores (E N 4 bytes, twice that without a slot buffer) exceed the
+    static scratch is refused with EC_ERR_WORKSPACE."""
+    L = ec.lib()
+    limit = 16 << 20
+    # E N 4 = 16 MiB: fits with a slot buffer, not without one
+    P = binding.Problem(32768, 64, 128, 64, [0, 32768], [256], 1.0, torch.bfloat16)
+    st = L.ec_route_noalloc(P.ref, FAKE, FAKE, FAKE, FAKE, None, None, None)
+    assert st == EC_ERR_WORKSPACE and str(limit) in L.ec_last_error().decode()
+    P2 = binding.Problem(32769, 64, 128, 64, [0, 32769], [256], 1.0, torch.bfloat16)
+    st = L.ec_route_noalloc(P2.ref, FAKE, FAKE, FAKE, FAKE, None, FAKE, None)
+    assert st == EC_ERR_WORKSPACE
+    # the usual argument checks come first
+    assert L.ec_route_noalloc(_problem(capacity=[101, 20]).ref, FAKE, FAKE, FAKE, FAKE, None,
+                              None, None) == EC_ERR_CAPACITY
+    assert L.ec_route_noalloc(_problem().ref, MISALIGNED, FAKE, FAKE, FAKE, None, None,
+                              None) == EC_ERR_ALIGN
