@@ -116,6 +116,59 @@ __device__ __forceinline__ float row16_sum(float t) {
   return dpp_add(dpp_add(dpp_add(dpp_add(t, 0), 1), 2), 3);
 }
 
+// DPP move of a 32-bit value within rows of 16 lanes; lanes whose source is
+// outside the row read 0 (bound_ctrl).  Controls used here: quad_perm
+// [1,0,3,2] = 0xB1 and [2,3,0,1] = 0x4E, row_shl:n = 0x100 + n, row_ror:n = 0x120 + n.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __builtin_bit_cast(float, dpp_u32<CTRL>(__builtin_bit_cast(uint32_t, v)));
+}
+
+// Maximum over the 16 lanes of a DPP row; every lane of the row ends with it.
+__device__ __forceinline__ float row16_max(float t) {
+  t = fmaxf(t, dpp_f32<0xB1>(t));
+  t = fmaxf(t, dpp_f32<0x4E>(t));
+  t = fmaxf(t, dpp_f32<0x124>(t));
+  return fmaxf(t, dpp_f32<0x128>(t));
+}
+
+// Minimum and maximum of an unsigned value over the whole wave (uniform results).
+__device__ __forceinline__ void wave_minmax_u32(uint32_t mn, uint32_t mx, uint32_t* out_mn,
+                                                uint32_t* out_mx) {
+  uint32_t a, b;
+  a = dpp_u32<0xB1>(mn); mn = a < mn ? a : mn;  b = dpp_u32<0xB1>(mx); mx = b > mx ? b : mx;
+  a = dpp_u32<0x4E>(mn); mn = a < mn ? a : mn;  b = dpp_u32<0x4E>(mx); mx = b > mx ? b : mx;
+  a = dpp_u32<0x124>(mn); mn = a < mn ? a : mn; b = dpp_u32<0x124>(mx); mx = b > mx ? b : mx;
+  a = dpp_u32<0x128>(mn); mn = a < mn ? a : mn; b = dpp_u32<0x128>(mx); mx = b > mx ? b : mx;
+  uint32_t rmn = __builtin_amdgcn_readlane(mn, 0), rmx = __builtin_amdgcn_readlane(mx, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const uint32_t c = __builtin_amdgcn_readlane(mn, r), d = __builtin_amdgcn_readlane(mx, r);
+    rmn = c < rmn ? c : rmn;
+    rmx = d > rmx ? d : rmx;
+  }
+  *out_mn = rmn;
+  *out_mx = rmx;
+}
+
+// Exclusive suffix sum over the wave's lanes: the sum of v over lanes > lane.
+__device__ __forceinline__ uint32_t wave_excl_suffix_u32(uint32_t v) {
+  uint32_t x = v;                       // inclusive suffix within the row of 16
+  x += dpp_u32<0x101>(x);
+  x += dpp_u32<0x102>(x);
+  x += dpp_u32<0x104>(x);
+  x += dpp_u32<0x108>(x);
+  const uint32_t t1 = __builtin_amdgcn_readlane(x, 16), t2 = __builtin_amdgcn_readlane(x, 32),
+                 t3 = __builtin_amdgcn_readlane(x, 48);
+  const int row = (threadIdx.x & 63) >> 4;
+  const uint32_t later = row == 0 ? t1 + t2 + t3 : (row == 1 ? t2 + t3 : (row == 2 ? t3 : 0u));
+  return x - v + later;
+}
+
 // Order-preserving map from fp32 to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t f32_order_key(float f) {
   uint32_t u = __float_as_uint(f);

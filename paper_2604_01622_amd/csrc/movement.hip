@@ -179,7 +179,14 @@ hipError_t run_combine(const T* Src, const float* S, const int32_t* slotT, const
 // tile of `tok` (<= RZ_TOK) tokens through LDS so that every global access is
 // coalesced; the tile keeps the dynamic LDS under 64 KiB for any E <= 256.
 constexpr int RZ_TOK = 32;
+constexpr int RZ_B = 8;       // (expert, token) entries per thread per batch
 
+// NP > 0: rows of exactly NP partials (NP a multiple of 4: 16-byte aligned rows),
+// read as float4 vectors; NP = 0: any count, read one by one.  Either way each
+// batch first loads the slots of its RZ_B entries, then every partial they
+// select, so the loads are in flight together; the partials of a row are then
+// added in a fixed order (0, 1, ...).
+template <int NP>
 __global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict__ S,
                                                         const float* __restrict__ dsp,
                                                         int nparts,
@@ -195,21 +202,75 @@ __global__ __launch_bounds__(256) void router_dz_kernel(const float* __restrict_
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i0 = blockIdx.x * tok;
   const int nt = N - i0 < tok ? N - i0 : tok;
-  for (int c = tid; c < nt * E; c += 256) {            // S tile: contiguous rows
-    const int t = c / E, j = c % E;
-    sS[t * LD + j] = S[(size_t)i0 * E + c];
+  // S tile (contiguous rows), RZ_B loads per thread in flight together
+  for (int c0 = 0; c0 < nt * E; c0 += 256 * RZ_B) {
+    float v[RZ_B];
+#pragma unroll
+    for (int b = 0; b < RZ_B; ++b) {
+      const int c = c0 + b * 256 + tid;
+      v[b] = S[(size_t)i0 * E + (c < nt * E ? c : nt * E - 1)];
+    }
+#pragma unroll
+    for (int b = 0; b < RZ_B; ++b) {
+      const int c = c0 + b * 256 + tid;
+      if (c < nt * E) sS[(c / E) * LD + c % E] = v[b];
+    }
   }
-  for (int c = tid; c < E * tok; c += 256) {           // slot tile: tok tokens per expert
-    const int j = c / tok, t = c % tok;
-    float u = 0.f;
-    if (t < nt) {
-      const int r = slotT[(size_t)j * N + i0 + t];
-      if (r >= 0 && r < K) {
-        const float* pp = dsp + ((size_t)j * K + r) * nparts;
-        for (int q = 0; q < nparts; ++q) u += pp[q];   // fixed order
+  const int total = E * tok;                            // slot tile: tok tokens per expert
+  for (int c0 = 0; c0 < total; c0 += 256 * RZ_B) {
+    int row[RZ_B];
+    bool sel[RZ_B];
+#pragma unroll
+    for (int b = 0; b < RZ_B; ++b) {
+      const int c = c0 + b * 256 + tid;
+      const int j = c / tok, t = c % tok;
+      const bool in = c < total && t < nt;
+      const int r = slotT[(size_t)(in ? j : 0) * N + i0 + (in ? t : 0)];   // always in range
+      sel[b] = in && K > 0 && r >= 0 && r < K;
+      row[b] = sel[b] ? j * K + r : 0;
+    }
+    float u[RZ_B];
+    if constexpr (NP > 0) {
+      // unconditional loads (an entry off the selection reads row 0, a valid row
+      // whenever K > 0) so that none waits behind a branch; K = 0 is uniform
+      float4 v[RZ_B][NP / 4];
+      if (K > 0) {
+#pragma unroll
+        for (int b = 0; b < RZ_B; ++b)
+#pragma unroll
+          for (int w = 0; w < NP / 4; ++w)
+            v[b][w] = *reinterpret_cast<const float4*>(dsp + (size_t)row[b] * NP + 4 * w);
+      }
+#pragma unroll
+      for (int b = 0; b < RZ_B; ++b)
+#pragma unroll
+        for (int w = 0; w < NP / 4; ++w)
+          if (!sel[b]) v[b][w] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int b = 0; b < RZ_B; ++b) {
+        float x = 0.f;
+#pragma unroll
+        for (int w = 0; w < NP / 4; ++w) {
+          x += v[b][w].x; x += v[b][w].y; x += v[b][w].z; x += v[b][w].w;
+        }
+        u[b] = x;
+      }
+    } else {
+#pragma unroll
+      for (int b = 0; b < RZ_B; ++b) {
+        float x = 0.f;
+        if (sel[b]) {
+          const float* pp = dsp + (size_t)row[b] * nparts;
+          for (int q = 0; q < nparts; ++q) x += pp[q];
+        }
+        u[b] = x;
       }
     }
-    sU[t * LD + j] = u;
+#pragma unroll
+    for (int b = 0; b < RZ_B; ++b) {
+      const int c = c0 + b * 256 + tid;
+      if (c < total) sU[(c % tok) * LD + c / tok] = u[b];
+    }
   }
   __syncthreads();
   for (int t = wave; t < nt; t += 4) {                 // <S_t, dS_t> = sum_j u_tj, a wave per token
@@ -309,8 +370,24 @@ hipError_t launch_router_dz(const float* S, const float* dsp, int nparts, const 
   if (N == 0) return hipSuccess;
   const int tok = E > 128 ? RZ_TOK / 2 : RZ_TOK;
   const size_t lds = (size_t)2 * tok * (E + 1) * sizeof(float);
-  router_dz_kernel<<<(N + tok - 1) / tok, 256, lds, st>>>(S, dsp, nparts, slotT, dZ, dZb, N, E,
-                                                           EP, K, inv_tau, tok);
+  const int grid = (N + tok - 1) / tok;
+  switch (nparts) {
+    case 4:
+      router_dz_kernel<4><<<grid, 256, lds, st>>>(S, dsp, nparts, slotT, dZ, dZb, N, E, EP, K,
+                                                  inv_tau, tok);
+      break;
+    case 8:
+      router_dz_kernel<8><<<grid, 256, lds, st>>>(S, dsp, nparts, slotT, dZ, dZb, N, E, EP, K,
+                                                  inv_tau, tok);
+      break;
+    case 16:
+      router_dz_kernel<16><<<grid, 256, lds, st>>>(S, dsp, nparts, slotT, dZ, dZb, N, E, EP, K,
+                                                   inv_tau, tok);
+      break;
+    default:
+      router_dz_kernel<0><<<grid, 256, lds, st>>>(S, dsp, nparts, slotT, dZ, dZb, N, E, EP, K,
+                                                  inv_tau, tok);
+  }
   return hipGetLastError();
 }
 

@@ -18,39 +18,41 @@ namespace ec {
 
 namespace {
 
-constexpr int RT_ROWS = 64;   // tokens per workgroup
 constexpr int RT_KC = 64;     // K chunk
 constexpr int RT_LDK = RT_KC + 8;  // padded LDS row (bf16 elements)
+constexpr int RT_PX = 4;      // X chunks in flight per wave
 
-// K splits per workgroup: the 64 tokens' 4 wave-rows of 16 tokens are each
-// repeated KS times over disjoint K ranges, so that KS * 4 waves stream X
-// concurrently (more loads in flight per CU); fewer splits for many experts
-// keep the router-matrix LDS tiles within 160 KiB.
+// A workgroup takes TG wave-rows of 16 tokens (TG = 4, or 1 when the tokens
+// would not fill every CU with 4-row workgroups), each repeated KS times over
+// disjoint K ranges, so that KS * TG waves stream X concurrently (more loads in
+// flight per CU); fewer splits for many experts keep the router-matrix LDS
+// tiles within 160 KiB.
 template <int ET> struct RouterCfg { static constexpr int KS = ET <= 4 ? 4 : (ET <= 8 ? 2 : 1); };
 
-template <int ET>
+template <int ET, int TG>
 constexpr int router_lds_bytes() {
   constexpr int KS = RouterCfg<ET>::KS;
   constexpr int w = KS * 2 * ET * 16 * RT_LDK * 2;     // router tiles
-  constexpr int r = KS > 1 ? KS * 4 * 64 * ET * 4 * 4 : 0;   // split partial sums
+  constexpr int r = KS > 1 ? KS * TG * 64 * ET * 4 * 4 : 0;   // split partial sums
   return w > r ? w : r;
 }
 
-template <int ET>
-__global__ __launch_bounds__(256 * RouterCfg<ET>::KS) void router_softmax_bf16_kernel(
+template <int ET, int TG>
+__global__ __launch_bounds__(64 * TG * RouterCfg<ET>::KS) void router_softmax_bf16_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wg, float* __restrict__ S,
     float* __restrict__ ST, int N, int d, int E, float inv_tau) {
   constexpr int EP = ET * 16;
   constexpr int KS = RouterCfg<ET>::KS;
-  constexpr int NT = 256 * KS;
-  __shared__ __attribute__((aligned(16))) char smem[router_lds_bytes<ET>()];
+  constexpr int NT = 64 * TG * KS;
+  constexpr int RT_ROWS = 16 * TG;               // tokens per workgroup
+  __shared__ __attribute__((aligned(16))) char smem[router_lds_bytes<ET, TG>()];
   __shared__ float sT[EP][RT_ROWS + 1];
   bf16_t* sW = reinterpret_cast<bf16_t*>(smem);   // [KS][2][EP * RT_LDK]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int tg = wave & 3, ks = wave >> 2;       // token group, K split
+  const int tg = wave % TG, ks = wave / TG;     // token group, K split
   const int row0 = blockIdx.x * RT_ROWS;
   const int myrow = row0 + tg * 16 + (lane & 15);
   const int xrow = myrow < N ? myrow : N - 1;
@@ -95,33 +97,46 @@ __global__ __launch_bounds__(256 * RouterCfg<ET>::KS) void router_softmax_bf16_k
 #pragma unroll
   for (int t = 0; t < ET; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // X: a ring of RT_PX chunks per wave in registers, so RT_PX chunks of the
+  // wave's rows are in flight; the ring index is static (the loop is unrolled by
+  // RT_PX).  Router tiles: chunk i+1 goes to LDS at the start of iteration i
+  // (its loads were issued an iteration earlier) and chunk i+2 is loaded.
+  // X is the critical path: its ring is requested at once (the first router
+  // tile just before it, so that its LDS store waits only for that tile's loads).
   uint4 wreg[WPT];
   load_w(0, wreg);
-  uint4 xa0, xa1;
-  load_x(0, xa0, xa1);
+  uint4 xr[RT_PX][2];
+#pragma unroll
+  for (int u = 0; u < RT_PX; ++u) load_x(u, xr[u][0], xr[u][1]);
   store_w(0, wreg);
+  load_w(1, wreg);
   __syncthreads();
 
-  for (int i = 0; i < cps; ++i) {
-    const int buf = i & 1;
-    const bool live = chunk_of(ks, i) >= 0;
-    const uint4 z = make_uint4(0, 0, 0, 0);
-    const bf16x8 a0 = __builtin_bit_cast(bf16x8, live ? xa0 : z);
-    const bf16x8 a1 = __builtin_bit_cast(bf16x8, live ? xa1 : z);
-    const int inext = i + 1 < cps ? i + 1 : i;
-    load_w(inext, wreg);
-    load_x(inext, xa0, xa1);
-    const bf16_t* sWb = &sW[(ks * 2 + buf) * EP * RT_LDK];
+  for (int i0 = 0; i0 < cps; i0 += RT_PX) {
 #pragma unroll
-    for (int t = 0; t < ET; ++t) {
-      const bf16_t* wp = &sWb[(t * 16 + (lane & 15)) * RT_LDK + (lane >> 4) * 16];
-      const bf16x8 b0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(wp));
-      const bf16x8 b1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(wp + 8));
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc[t], 0, 0, 0);
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc[t], 0, 0, 0);
+    for (int u = 0; u < RT_PX; ++u) {
+      const int i = i0 + u;
+      if (i < cps) {                             // uniform over the workgroup
+        const int buf = i & 1;
+        if (i + 1 < cps) store_w(buf ^ 1, wreg); // chunk i+1; buffer last read in iteration i-1
+        load_w(i + 2 < cps ? i + 2 : i, wreg);
+        const bool live = chunk_of(ks, i) >= 0;
+        const uint4 z = make_uint4(0, 0, 0, 0);
+        const bf16x8 a0 = __builtin_bit_cast(bf16x8, live ? xr[u][0] : z);
+        const bf16x8 a1 = __builtin_bit_cast(bf16x8, live ? xr[u][1] : z);
+        load_x(i + RT_PX < cps ? i + RT_PX : i, xr[u][0], xr[u][1]);
+        const bf16_t* sWb = &sW[(ks * 2 + buf) * EP * RT_LDK];
+#pragma unroll
+        for (int t = 0; t < ET; ++t) {
+          const bf16_t* wp = &sWb[(t * 16 + (lane & 15)) * RT_LDK + (lane >> 4) * 16];
+          const bf16x8 b0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(wp));
+          const bf16x8 b1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(wp + 8));
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc[t], 0, 0, 0);
+        }
+        __syncthreads();
+      }
     }
-    store_w(buf ^ 1, wreg);
-    __syncthreads();
   }
 
   // sum the K splits of each token group (fixed order), in the lane layout of the
@@ -130,14 +145,14 @@ __global__ __launch_bounds__(256 * RouterCfg<ET>::KS) void router_softmax_bf16_k
     float* red = reinterpret_cast<float*>(smem);   // [KS][4 groups][64 lanes][ET][4]
 #pragma unroll
     for (int t = 0; t < ET; ++t)
-      *reinterpret_cast<f32x4*>(&red[(((ks * 4 + tg) * 64 + lane) * ET + t) * 4]) = acc[t];
+      *reinterpret_cast<f32x4*>(&red[(((ks * TG + tg) * 64 + lane) * ET + t) * 4]) = acc[t];
     __syncthreads();
     if (ks == 0) {
 #pragma unroll
       for (int t = 0; t < ET; ++t) {
         f32x4 v = acc[t];
         for (int q = 1; q < KS; ++q)
-          v += *reinterpret_cast<const f32x4*>(&red[(((q * 4 + tg) * 64 + lane) * ET + t) * 4]);
+          v += *reinterpret_cast<const f32x4*>(&red[(((q * TG + tg) * 64 + lane) * ET + t) * 4]);
         acc[t] = v;
       }
     }
@@ -157,16 +172,14 @@ __global__ __launch_bounds__(256 * RouterCfg<ET>::KS) void router_softmax_bf16_k
         v[t] = ok ? acc[t][i] * inv_tau : -INFINITY;
         m = fmaxf(m, v[t]);
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+      m = row16_max(m);          // the token's 16 lanes form one DPP row
       float s = 0.f;
 #pragma unroll
       for (int t = 0; t < ET; ++t) {
         v[t] = (t * 16 + col < E) ? expf(v[t] - m) : 0.f;
         s += v[t];
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o, 64);
+      s = row16_sum(s);
 #pragma unroll
       for (int t = 0; t < ET; ++t) {
         const int e = t * 16 + col;
@@ -251,6 +264,16 @@ __global__ __launch_bounds__(256) void router_softmax_f32_kernel(
   }
 }
 
+
+template <int ET, int TG>
+hipError_t run_router(const bf16_t* x, const bf16_t* w, float* S, float* ST, int N, int d, int E,
+                      float inv_tau, hipStream_t st) {
+  const int grid = (N + 16 * TG - 1) / (16 * TG);
+  router_softmax_bf16_kernel<ET, TG><<<grid, 64 * TG * RouterCfg<ET>::KS, 0, st>>>(x, w, S, ST, N,
+                                                                                 d, E, inv_tau);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_router_softmax(int dtype, const void* X, const void* Wg, float* S, float* ST,
@@ -262,25 +285,21 @@ hipError_t launch_router_softmax(int dtype, const void* X, const void* Wg, float
                                                     d, E, inv_tau);
     return hipGetLastError();
   }
-  const int grid = (N + RT_ROWS - 1) / RT_ROWS;
   const bf16_t* x = (const bf16_t*)X;
   const bf16_t* w = (const bf16_t*)Wg;
-  if (E <= 16)
-    router_softmax_bf16_kernel<1><<<grid, 256 * RouterCfg<1>::KS, 0, st>>>(x, w, S, ST, N, d, E,
-                                                                          inv_tau);
-  else if (E <= 32)
-    router_softmax_bf16_kernel<2><<<grid, 256 * RouterCfg<2>::KS, 0, st>>>(x, w, S, ST, N, d, E,
-                                                                          inv_tau);
-  else if (E <= 64)
-    router_softmax_bf16_kernel<4><<<grid, 256 * RouterCfg<4>::KS, 0, st>>>(x, w, S, ST, N, d, E,
-                                                                          inv_tau);
-  else if (E <= 128)
-    router_softmax_bf16_kernel<8><<<grid, 256 * RouterCfg<8>::KS, 0, st>>>(x, w, S, ST, N, d, E,
-                                                                          inv_tau);
-  else
-    router_softmax_bf16_kernel<16><<<grid, 256 * RouterCfg<16>::KS, 0, st>>>(x, w, S, ST, N, d, E,
-                                                                          inv_tau);
-  return hipGetLastError();
+  // 64-token workgroups when they fill every CU (256), else 16-token ones
+  if (N >= 256 * 64) {
+    if (E <= 16) return run_router<1, 4>(x, w, S, ST, N, d, E, inv_tau, st);
+    if (E <= 32) return run_router<2, 4>(x, w, S, ST, N, d, E, inv_tau, st);
+    if (E <= 64) return run_router<4, 4>(x, w, S, ST, N, d, E, inv_tau, st);
+    if (E <= 128) return run_router<8, 4>(x, w, S, ST, N, d, E, inv_tau, st);
+    return run_router<16, 4>(x, w, S, ST, N, d, E, inv_tau, st);
+  }
+  if (E <= 16) return run_router<1, 1>(x, w, S, ST, N, d, E, inv_tau, st);
+  if (E <= 32) return run_router<2, 1>(x, w, S, ST, N, d, E, inv_tau, st);
+  if (E <= 64) return run_router<4, 1>(x, w, S, ST, N, d, E, inv_tau, st);
+  if (E <= 128) return run_router<8, 1>(x, w, S, ST, N, d, E, inv_tau, st);
+  return run_router<16, 1>(x, w, S, ST, N, d, E, inv_tau, st);
 }
 
 }  // namespace ec

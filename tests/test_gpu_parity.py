@@ -176,6 +176,17 @@ def test_maximum_widths(dtype, d, h):
     full_case(wl)
 
 
+@pytest.mark.parametrize("dtype,h", [("bf16", 512), ("bf16", 1024), ("bf16", 2048), ("f32", 256),
+                                     ("f32", 1024), ("bf16", 768)])
+def test_gate_gradient_partials(dtype, h):
+    # the router backward sums each selected pair's gate-gradient partials (one per
+    # 128 hidden units in bf16, 64 in fp32): 4, 8 and 16 per row read as vectors,
+    # 6 through the general path
+    wl = synth.small(f"dsp_{dtype}_{h}", [300, 157], 128, 16, h, dtype=dtype, seed=24,
+                     capacity_factor=3.0, backward=True)
+    full_case(wl)
+
+
 def test_zero_capacity_everywhere():
     wl = synth.small("k0", [100, 50], 64, 8, 64, seed=14, capacity_factor=0.0, backward=True)
     out = full_case(wl)
@@ -206,6 +217,28 @@ def test_long_group_route_only():
     wl = synth.small("long", [20000, 777], 64, 4, 64, seed=18, capacity_factor=1.5)
     inp = synth.draw(wl)
     caps = caps_for(wl, inp)
+    check_route(inp, caps, 1.0)
+
+
+@pytest.mark.parametrize("lens", [[500, 17], [2048, 1999, 64], [4096, 3000, 2049],
+                                  [9000, 100], [13000, 5]])
+@pytest.mark.parametrize("ties", [False, True])
+def test_topk_every_path(lens, ties):
+    """Every selection path: one wave per column with 8, 32 or 64 keys per lane
+    (columns up to 512, 2048, 4096 tokens), then one workgroup per column with the
+    keys cached in LDS (up to 12288) or re-read; normal scores and scores with
+    whole runs of bitwise-equal values; capacities from 0 to the whole group."""
+    wl = synth.small("paths", lens, 64, 8, 64, seed=23, capacity_factor=1.0)
+    inp = synth.draw(wl)
+    if ties:
+        rng = np.random.default_rng(23)
+        protos = rng.integers(-1, 2, size=(6, 64)).astype(np.float32)
+        inp.X[:] = synth.f32_to_bf16_bits(protos[rng.integers(0, 6, size=wl.n_tokens)])
+    rng = np.random.default_rng(24)
+    caps = np.array([[0, 1, L // 3, L - 1, L][int(rng.integers(0, 5))] if L > 1 else L
+                     for L in lens], dtype=np.int32)
+    caps[0] = lens[0] // 8
+    print(f"[case] top-k paths lens={lens} ties={ties} caps={caps.tolist()}", flush=True)
     check_route(inp, caps, 1.0)
 
 
