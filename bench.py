@@ -40,16 +40,22 @@ GEMM_TAGS = {"gemm_w13_swiglu": 1, "gemm_w2": 2, "gemm_dA_swiglu_bwd": 3, "gemm_
              "gemm_dW2": 5, "gemm_dW13": 6, "router_dx": 7, "router_dwg": 8,
              "shared_w13_swiglu": 9, "shared_w2": 10, "shared_dA_swiglu_bwd": 11, "shared_dX": 12,
              "shared_dW2": 13, "shared_dW13": 14}
-KERNEL_SOURCES = ["paper_2604_01622_amd/csrc/gemm.hip", "paper_2604_01622_amd/csrc/ec_common.h"]
+CSRC = "paper_2604_01622_amd/csrc/"
+# the sources each stage's kernels are built from (a record of counters stays valid
+# while their code is unchanged)
+STAGE_SOURCES = {"router": ["router.hip"], "topk": ["topk.hip"],
+                 "combine": ["movement.hip"], "bwd_combine": ["movement.hip"],
+                 "router_dz": ["movement.hip"], "router_dwg_reduce": ["gemm.hip"]}
+SIMD_NUM = 256 * 4   # MI355X: 256 CUs of 4 SIMDs
 CALIB_BYTES = 1 << 30   # plain elementwise copy used to scale the byte counters
 FLUSH_BYTES = 512 << 20  # cold-cache steps: twice the 256 MiB last-level (MALL) cache
 
 
-def sources_hash():
-    """Hash of the GEMM sources' code (comments and whitespace removed), so that the
-    stored traffic counters stay valid across comment-only edits."""
+def sources_hash(stage="gemm"):
+    """Hash of the code of a stage's sources and the shared header (comments and
+    whitespace removed), so that stored counters stay valid across comment-only edits."""
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in [CSRC + x for x in STAGE_SOURCES.get(stage, ["gemm.hip"])] + [CSRC + "ec_common.h"]:
         with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
             src = fh.read()
         src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
@@ -59,10 +65,19 @@ def sources_hash():
 
 
 def stage_of_kernel(name):
-    """Stage of a gemm_dma_kernel instantiation from its stage-tag template argument
-    (the eleventh: BM, BN, WGM, WGN, KSTEP, STAGES, A_KC, B_KC, EPI, OUT_F32, TAG, OPT)."""
+    """Stage of a kernel from its name: a gemm_dma_kernel instantiation by its
+    stage-tag template argument (the eleventh: BM, BN, WGM, WGN, KSTEP, STAGES, A_KC,
+    B_KC, EPI, OUT_F32, TAG, OPT), the other kernels by their names."""
     m = re.search(r"gemm_dma_kernel<([^>]*)>", name)
     if not m:
+        for key, st in (("router_softmax", "router"), ("topk_col_kernel", "topk"),
+                        ("topk_kernel", "topk"), ("router_dz_kernel", "router_dz"),
+                        ("splitk_reduce_kernel", "router_dwg_reduce")):
+            if key in name:
+                return st
+        c = re.search(r"combine_kernel<[^>]*,\s*(true|false)>", name)
+        if c:
+            return "bwd_combine" if c.group(1) == "true" else "combine"
         return None
     args = [a.strip() for a in m.group(1).split(",")]
     if len(args) < 11 or not args[10].isdigit():
@@ -72,13 +87,51 @@ def stage_of_kernel(name):
 
 
 def pmc_per_dispatch(db, counter):
-    """{kernel name: [value per dispatch]} for one counter of a rocprofv3 --pmc database."""
+    """{kernel name: [value per dispatch]} for one counter of a rocprofv3 --pmc database:
+    the sum over the counter's instances, except GRBM counters (one per XCD), whose
+    maximum is the dispatch's value (as in rocprof's derived metrics)."""
     c = sqlite3.connect(db)
     out = {}
+    agg = "max" if counter.startswith("GRBM") else "sum"
     for name, did, v in c.execute(
-            "select name, dispatch_id, sum(counter_value) from pmc_events where counter_name = ? "
+            f"select name, dispatch_id, {agg}(counter_value) from pmc_events where counter_name = ? "
             "group by name, dispatch_id order by dispatch_id", (counter,)):
         out.setdefault(name, []).append(v)
+    return out
+
+
+def counters_from(dbs, workload):
+    """Per-stage medians of the counters in rocprofv3 --pmc databases (each run with
+    --kernel-trace, so that the durations under counting come along), with the MFMA
+    utilisation SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs) and the clock
+    GRBM_GUI_ACTIVE / duration."""
+    import statistics as stat
+    per = {}
+    for db in dbs:
+        c = sqlite3.connect(db)
+        names = [r[0] for r in c.execute("select distinct counter_name from pmc_events")]
+        for cn in names:
+            for name, vals in pmc_per_dispatch(db, cn).items():
+                st = stage_of_kernel(name)
+                if st:
+                    per.setdefault(st, {}).setdefault(cn, []).extend(vals)
+        try:
+            for name, dur in c.execute("select name, duration from kernels"):
+                st = stage_of_kernel(name)
+                if st:
+                    per.setdefault(st, {}).setdefault("duration_ns", []).append(dur)
+        except sqlite3.OperationalError:
+            pass
+    out = {}
+    for st, d in per.items():
+        rec = {k: stat.median(v) for k, v in d.items()}
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in rec and rec.get("GRBM_GUI_ACTIVE"):
+            rec["mfma_busy_frac"] = rec["SQ_VALU_MFMA_BUSY_CYCLES"] / (rec["GRBM_GUI_ACTIVE"] * SIMD_NUM)
+        if rec.get("GRBM_GUI_ACTIVE") and rec.get("duration_ns"):
+            rec["clock_ghz"] = rec["GRBM_GUI_ACTIVE"] / rec["duration_ns"]
+        rec["sources_sha256_16"] = sources_hash(st)
+        rec["workload"] = workload
+        out[st] = rec
     return out
 
 
@@ -104,7 +157,7 @@ def traffic_from(fetch_db, write_db, workload):
         wb = sum(write[name]) / len(write[name]) * 1024.0 * f_write
         recs[st] = {"stage": st, "kernel": name, "fetch_bytes": fb, "write_bytes": wb,
                     "traffic_bytes": fb + wb, "fetch_scale": f_fetch, "write_scale": f_write,
-                    "dispatches": len(vals), "sources_sha256_16": sources_hash(),
+                    "dispatches": len(vals), "sources_sha256_16": sources_hash(st),
                     "workload": workload}
     return recs
 
@@ -237,16 +290,20 @@ def run_tc(a):
         for _ in range(a.warmup):
             fn()
         torch.cuda.synchronize()
-        evs = [binding.StageEvents(len(binding.FORWARD_STAGES)) for _ in range(a.steps)]
+        # uninstrumented steps for the time, then instrumented ones for the stages
         s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s0.record()
+        for _ in range(a.steps):
+            fn()
+        s1.record()
+        torch.cuda.synchronize()
+        ms = s0.elapsed_time(s1) / a.steps
+        evs = [binding.StageEvents(len(binding.FORWARD_STAGES)) for _ in range(a.steps)]
         for i in range(a.steps):
             evs[i].arm()
             fn()
         binding.StageEvents.disarm()
-        s1.record()
         torch.cuda.synchronize()
-        ms = s0.elapsed_time(s1) / a.steps
         st = {n: float(np.mean(col)) for n, col in
               zip(binding.FORWARD_STAGES, zip(*[e.durations_ms() for e in evs]))}
         return ms, st
@@ -355,7 +412,20 @@ def main():
                          "shapes, as a reference for the grouped GEMM figures")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
                     help="write profiles/traffic_<stage>.json from two --pmc runs and exit")
+    ap.add_argument("--counters-from", nargs="+", metavar="PMC_DB",
+                    help="write profiles/counters_<workload>.json (per-stage medians, MFMA "
+                         "utilisation, clock) from --pmc --kernel-trace runs and exit")
     a = ap.parse_args()
+    if a.counters_from:
+        recs = counters_from(a.counters_from, a.workload)
+        with open(os.path.join(ROOT, "profiles", f"counters_{a.workload}.json"), "w") as f:
+            json.dump(recs, f, indent=1, sort_keys=True)
+        for st, r in sorted(recs.items()):
+            mf = r.get("mfma_busy_frac")
+            print(f"{st:22s} mfma_busy {'-' if mf is None else f'{100 * mf:5.1f}%'} clock "
+                  f"{r.get('clock_ghz', float('nan')):.2f} GHz  duration "
+                  f"{r.get('duration_ns', float('nan')) / 1e3:8.1f} us")
+        return
     if a.routing == "tc" and not a.traffic_from:
         if a.gpus != 1:
             print("bench.py runs on exactly one GPU", file=sys.stderr)
@@ -423,12 +493,25 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    fwd_ev = [binding.StageEvents(len(binding.FORWARD_STAGES)) for _ in range(a.steps)]
-    bwd_ev = [binding.StageEvents(len(binding.BACKWARD_STAGES)) for _ in range(a.steps)]
+    # The timed steps run uninstrumented: each stage event the library records is
+    # a command of its own on the stream (several microseconds apiece), so the
+    # per-stage durations come from a second pass of the same number of steps.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     log(f"[bench] timing {a.steps} steps")
     torch.cuda.synchronize()
     start.record()
+    for _ in range(a.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / a.steps
+    value = N / (ms * 1e-3)
+
+    fwd_ev = [binding.StageEvents(len(binding.FORWARD_STAGES)) for _ in range(a.steps)]
+    bwd_ev = [binding.StageEvents(len(binding.BACKWARD_STAGES)) for _ in range(a.steps)]
+    log(f"[bench] {a.steps} steps with stage events")
+    s_start, s_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s_start.record()
     for i in range(a.steps):
         fwd_ev[i].arm()
         layer.forward()
@@ -436,10 +519,9 @@ def main():
             bwd_ev[i].arm()
             layer.backward(dY)
     binding.StageEvents.disarm()
-    end.record()
+    s_end.record()
     torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / a.steps
-    value = N / (ms * 1e-3)
+    ms_instrumented = s_start.elapsed_time(s_end) / a.steps
 
     stage_ms = {}
     for n, col in zip(binding.FORWARD_STAGES, zip(*[e.durations_ms() for e in fwd_ev])):
@@ -479,7 +561,7 @@ def main():
     if os.path.exists(tf):
         with open(tf) as f:
             rec = json.load(f)
-        if rec.get("sources_sha256_16") == sources_hash() and rec.get("workload") == a.workload:
+        if rec.get("sources_sha256_16") == sources_hash(dom) and rec.get("workload") == a.workload:
             traffic = round(rec["traffic_bytes"])
     if dom in GEMM_STAGES:
         peak = PEAK_BF16_TFLOPS if esz == 2 else PEAK_F32_TFLOPS
@@ -502,7 +584,8 @@ def main():
                       "tokens": N, "groups": wl.n_groups, "d_model": d, "experts": E,
                       "d_ff": h, "shared_hidden": hs, "k_per_group": [int(x) for x in caps],
                       "K_tot": K},
-           "stages": stages, "route": route, "roofline": roof,
+           "stages": stages, "route": route, "ms_per_step_with_stage_events": round(ms_instrumented, 4),
+           "roofline": roof,
            "grouped_gemm": {"tflops": round(gemm_fl / (gemm_ms * 1e-3) / 1e12, 1),
                             "mfma_frac": round(gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
 

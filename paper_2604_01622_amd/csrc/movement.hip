@@ -82,7 +82,9 @@ __device__ __forceinline__ int token_expert_list(const int32_t* sslot, const flo
 // loads per lane in flight) with no branch between the loads and their FMAs:
 // entries past the token's last expert read the zero row with gate 0, and lanes
 // past the row's end read its last chunk and store nothing.
-template <typename T, int MAXE>
+// BWD: the backward combine of dXe (its own kernel symbol, so that traces and
+// counters tell the two stages apart).
+template <typename T, int MAXE, bool BWD>
 __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
                                                       const float* __restrict__ S,
                                                       const int32_t* __restrict__ slotT,
@@ -157,16 +159,16 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ Src,
   }
 }
 
-template <typename T>
+template <typename T, bool BWD>
 hipError_t run_combine(const T* Src, const float* S, const int32_t* slotT, const T* Xr, T* Y,
                        int N, int E, int K, int d, hipStream_t st, long kstride) {
   const int grid = (N + CB_TOK - 1) / CB_TOK;
   if (E <= 64)
-    combine_kernel<T, 64><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
+    combine_kernel<T, 64, BWD><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
   else if (E <= 128)
-    combine_kernel<T, 128><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
+    combine_kernel<T, 128, BWD><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
   else
-    combine_kernel<T, 256><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
+    combine_kernel<T, 256, BWD><<<grid, 256, 0, st>>>(Src, S, slotT, Xr, Y, N, E, K, d, kstride);
   return hipGetLastError();
 }
 
@@ -348,20 +350,20 @@ hipError_t launch_combine(int dtype, const void* O, const float* S, const int32_
   if (N == 0) return hipSuccess;
   if (kstride < 0) kstride = K;
   if (dtype == DT_F32)
-    return run_combine<float>((const float*)O, S, slotT, (const float*)Xr, (float*)Y, N, E, K, d,
-                              st, kstride);
-  return run_combine<bf16_t>((const bf16_t*)O, S, slotT, (const bf16_t*)Xr, (bf16_t*)Y, N, E, K,
-                             d, st, kstride);
+    return run_combine<float, false>((const float*)O, S, slotT, (const float*)Xr, (float*)Y, N, E,
+                                     K, d, st, kstride);
+  return run_combine<bf16_t, false>((const bf16_t*)O, S, slotT, (const bf16_t*)Xr, (bf16_t*)Y, N,
+                                    E, K, d, st, kstride);
 }
 
 hipError_t launch_bwd_combine(int dtype, const void* dXe, const int32_t* slotT, const void* Xr,
                               void* dX, int N, int E, int K, int d, hipStream_t st) {
   if (N == 0) return hipSuccess;
   if (dtype == DT_F32)
-    return run_combine<float>((const float*)dXe, nullptr, slotT, (const float*)Xr, (float*)dX, N,
-                              E, K, d, st, K);
-  return run_combine<bf16_t>((const bf16_t*)dXe, nullptr, slotT, (const bf16_t*)Xr, (bf16_t*)dX, N,
-                             E, K, d, st, K);
+    return run_combine<float, true>((const float*)dXe, nullptr, slotT, (const float*)Xr,
+                                    (float*)dX, N, E, K, d, st, K);
+  return run_combine<bf16_t, true>((const bf16_t*)dXe, nullptr, slotT, (const bf16_t*)Xr,
+                                   (bf16_t*)dX, N, E, K, d, st, K);
 }
 
 hipError_t launch_router_dz(const float* S, const float* dsp, int nparts, const int32_t* slotT,
