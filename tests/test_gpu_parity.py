@@ -187,6 +187,17 @@ def test_gate_gradient_partials(dtype, h):
     full_case(wl)
 
 
+@pytest.mark.parametrize("k", [100, 128, 257, 384, 385, 612])
+def test_expert_buffer_row_counts(k):
+    # expert buffers of k rows around the 256-row tile boundaries: one partial
+    # block (100, 128), full blocks and a ragged last one (257, 384, 385, 612)
+    wl = synth.small(f"rows{k}", [1024], 256, 4, 256, seed=25, capacity_factor=k / 256,
+                     backward=True)
+    inp = synth.draw(wl, with_dy=True)
+    assert int(np.sum(caps_for(wl, inp))) == k
+    full_case(wl, inp=inp)
+
+
 def test_zero_capacity_everywhere():
     wl = synth.small("k0", [100, 50], 64, 8, 64, seed=14, capacity_factor=0.0, backward=True)
     out = full_case(wl)
