@@ -386,8 +386,8 @@ def vendor_gemm(E, M, d, h, warmup, steps, backward):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="train",
                     choices=["train", "train_shared", "static", "timestep", "fine", "decode",
                              "tiny"])
@@ -523,18 +523,18 @@ def main():
     torch.cuda.synchronize()
     ms_instrumented = s_start.elapsed_time(s_end) / a.steps
 
-    stage_ms = {}
+    stage_ms, stage_med = {}, {}
     for n, col in zip(binding.FORWARD_STAGES, zip(*[e.durations_ms() for e in fwd_ev])):
-        stage_ms[n] = float(np.mean(col))
+        stage_ms[n], stage_med[n] = float(np.mean(col)), float(np.median(col))
     if backward:
         for n, col in zip(binding.BACKWARD_STAGES, zip(*[e.durations_ms() for e in bwd_ev])):
-            stage_ms[n] = float(np.mean(col))
+            stage_ms[n], stage_med[n] = float(np.mean(col)), float(np.median(col))
     if not hs:   # the shared-expert stages are empty
         stage_ms = {n: t for n, t in stage_ms.items() if not n.startswith("shared_")}
     stages = {}
     for n, t in stage_ms.items():
         fl, by = stage_work(n, N, d, E, h, K, esz, EP, backward, splits, hs)
-        st = {"ms": round(t, 4)}
+        st = {"ms": round(t, 4), "ms_median": round(stage_med[n], 4)}
         if t < 0.010:   # an empty stage (bf16: the gather happens inside the W1/W3 product)
             stages[n] = st
             continue

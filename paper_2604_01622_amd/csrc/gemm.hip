@@ -845,6 +845,17 @@ hipError_t run_dma_var(GemmParams p, long max_rows, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Row blocks of 192 for the forward expert products when they pad the expert
+// buffers enough less than blocks of 256 (one 2048-token sequence at c(t) =
+// 12 - 8t has 373 rows per expert: 384 computed instead of 512).  A 192-row
+// tile (96 x 64 per wave) does three quarters of the work in 0.875 of the time
+// (W1/W3 on that sequence), so a computed row costs 7/6 as much.  Both keep an
+// expert's row blocks side by side on one XCD, so its weights are fetched once.
+bool short_rows(int M) {
+  const long r256 = (M + 255) / 256 * 256L, r192 = (M + 191) / 192 * 192L;
+  return r192 * 7 < r256 * 6;
+}
+
 // ------------------------------------------------------------------ fp32 FMA
 
 constexpr int FT = 64;   // tile
@@ -1027,6 +1038,7 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
     if (rows) return hipErrorInvalidValue;   // the shared experts read X as is
     return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13>(p, st);
   }
+  if (short_rows(M)) return run_dma<192, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
   return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
 }
 
@@ -1040,6 +1052,7 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
   if (shared) return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2>(p, st);
+  if (short_rows(M)) return run_dma<192, 256, 2, 4, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
   return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
 }
 
