@@ -6,7 +6,8 @@
 // bf16: one pipelined kernel (gemm_dma_kernel) for every product of the
 // forward and backward.  v_mfma_f32_32x32x16_bf16 with fp32 accumulation; a
 // 256 x 256 output tile per workgroup of 8 waves (2 per SIMD, 64 x 128 or
-// 128 x 64 each);
+// 128 x 64 each; the forward products take 192-row tiles of 96 x 64 per wave
+// when those pad short expert buffers less);
 // K advances 64 at a time through a 2-stage LDS ring filled straight from
 // global memory by global_load_lds_dwordx4 (no VGPR staging).  K-contiguous
 // operands sit in LDS as 128-byte rows with XOR-swizzled 16-byte chunks
