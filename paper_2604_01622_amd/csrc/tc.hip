@@ -15,59 +15,65 @@ namespace {
 
 constexpr int TC_TOK = 64;   // tokens per workgroup of the row top-k
 
-// Row top-k of S [N, E] (E <= 256).  One wave per token: lane l holds experts
-// l, l + 64, l + 128, l + 192; k rounds of a wave-wide arg-max (larger score,
-// then lower index).  G[i, j] = S_ij / (sum of the chosen scores) for chosen j,
-// 0 elsewhere; flagT[j, i] = 1 if token i chose expert j, else 0 (transposed
-// through LDS so that every expert row is written contiguously).
+// Row top-k of S [N, E] (E <= 256).  Sixteen lanes per token (four tokens per
+// wave at a time): lane r of a token's group holds experts r, r + 16, ...,
+// r + 16 (NQ - 1); k rounds of an arg-max (larger score, then lower index) over
+// the group, the lanes exchanging candidates within their 16-lane DPP row.
+// G[i, j] = S_ij / (sum of the chosen scores) for chosen j, 0 elsewhere;
+// flagT[j, i] = 1 if token i chose expert j, else 0 (transposed through LDS so
+// that every expert row is written contiguously).
+template <int NQ>
 __global__ __launch_bounds__(256) void tc_topk_kernel(const float* __restrict__ S, int N, int E,
                                                       int k, float* __restrict__ G,
                                                       int32_t* __restrict__ flagT) {
   __shared__ uint8_t sflag[TC_TOK][256];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, r = tid & 15, grp = tid >> 4;   // 16 groups of 16 lanes
   const int i0 = blockIdx.x * TC_TOK;
-  for (int t = wave; t < TC_TOK; t += 4) {
+  for (int t = grp; t < TC_TOK; t += 16) {
     const int i = i0 + t;
-    if (i >= N) break;
-    float v[4];
-    bool taken[4];
+    if (i >= N) break;                              // uniform over the group
+    float v[NQ];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int j = lane + 64 * q;
+    for (int q = 0; q < NQ; ++q) {
+      const int j = r + 16 * q;
       v[q] = (j < E) ? S[(size_t)i * E + j] : -INFINITY;
-      taken[q] = false;
     }
+    uint32_t taken = 0u;                            // bit q: expert r + 16 q chosen
     float sum = 0.f;
-    for (int r = 0; r < k; ++r) {
+    for (int c = 0; c < k; ++c) {
       float bv = -INFINITY;
       int bj = 0x7fffffff;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int j = lane + 64 * q;
-        if (j < E && !taken[q] && (v[q] > bv || (v[q] == bv && j < bj))) {
+      for (int q = 0; q < NQ; ++q) {
+        const int j = r + 16 * q;
+        if (j < E && !((taken >> q) & 1u) && (v[q] > bv || (v[q] == bv && j < bj))) {
           bv = v[q];
           bj = j;
         }
       }
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const float ov = __shfl_xor(bv, m);
-        const int oj = __shfl_xor(bj, m);
+      // all-reduce over the 16-lane row by DPP: rotations by 8 and 4, then the
+      // quad exchanges (the comparison is commutative and associative)
+      auto better = [&](float ov, int oj) {
         if (ov > bv || (ov == bv && oj < bj)) {
           bv = ov;
           bj = oj;
         }
-      }
-      if ((bj & 63) == lane) taken[bj >> 6] = true;
+      };
+      better(dpp_f32<0x128>(bv), (int)dpp_u32<0x128>((uint32_t)bj));
+      better(dpp_f32<0x124>(bv), (int)dpp_u32<0x124>((uint32_t)bj));
+      better(dpp_f32<0x4E>(bv), (int)dpp_u32<0x4E>((uint32_t)bj));
+      better(dpp_f32<0xB1>(bv), (int)dpp_u32<0xB1>((uint32_t)bj));
+      if ((bj & 15) == r) taken |= 1u << (bj >> 4);
       sum += bv;
     }
     const float inv = 1.0f / sum;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int j = lane + 64 * q;
+    for (int q = 0; q < NQ; ++q) {
+      const int j = r + 16 * q;
       if (j < E) {
-        G[(size_t)i * E + j] = taken[q] ? v[q] * inv : 0.f;
-        sflag[t][j] = taken[q] ? 1 : 0;
+        const bool ch = (taken >> q) & 1u;
+        G[(size_t)i * E + j] = ch ? v[q] * inv : 0.f;
+        sflag[t][j] = ch ? 1 : 0;
       }
     }
   }
@@ -196,7 +202,11 @@ __global__ __launch_bounds__(256) void tc_place_kernel(int32_t* __restrict__ slo
 hipError_t launch_tc_topk(const float* S, int N, int E, int k, float* G, int32_t* flagT,
                           hipStream_t st) {
   if (N == 0) return hipSuccess;
-  tc_topk_kernel<<<(N + TC_TOK - 1) / TC_TOK, 256, 0, st>>>(S, N, E, k, G, flagT);
+  const int grid = (N + TC_TOK - 1) / TC_TOK;
+  if (E <= 64)
+    tc_topk_kernel<4><<<grid, 256, 0, st>>>(S, N, E, k, G, flagT);
+  else
+    tc_topk_kernel<16><<<grid, 256, 0, st>>>(S, N, E, k, G, flagT);
   return hipGetLastError();
 }
 

@@ -598,6 +598,21 @@ def test_tc_skewed_router_with_empty_experts():
             assert np.any(np.diff(rows) == 0)
 
 
+@pytest.mark.parametrize("E,top_k,zero_router", [(65, 3, False), (200, 7, False), (256, 256, False),
+                                                 (64, 8, True), (130, 5, True)])
+def test_tc_expert_counts_and_ties(E, top_k, zero_router):
+    # the row top-k keeps a token's scores in 16 lanes (4 or 16 experts a lane);
+    # a zero router makes every score equal, so each token takes the lowest
+    # expert indices
+    wl = synth.small(f"tcE{E}", [200, 77], 64, E, 64, seed=54, capacity_factor=1.0)
+    inp = synth.draw(wl)
+    if zero_router:
+        inp.Wg[:] = 0
+    rows, kept = check_tc(inp, ec.tc_capacity(wl.group_lengths, E, top_k, 1.0), top_k)
+    if zero_router:
+        assert np.all(np.diff(rows)[top_k:] == 0)
+
+
 def test_full_tc_timestep_bf16():
     wl = synth.TIMESTEP_BF16
     print(f"[case] token choice on {wl.name}", flush=True)
