@@ -13,10 +13,12 @@ namespace ec {
 
 namespace {
 
-constexpr int TC_TOK = 64;   // tokens per workgroup of the row top-k
+constexpr int TC_TOK = 16;   // tokens per workgroup of the row top-k (one per 16-lane group)
 
 // Row top-k of S [N, E] (E <= 256).  Sixteen lanes per token (four tokens per
-// wave at a time): lane r of a token's group holds experts r, r + 16, ...,
+// wave, sixteen per workgroup, so that several waves per SIMD hide the
+// latency of the selection's dependent steps): lane r of a token's group holds
+// experts r, r + 16, ...,
 // r + 16 (NQ - 1); k rounds of an arg-max (larger score, then lower index) over
 // the group, the lanes exchanging candidates within their 16-lane DPP row.
 // G[i, j] = S_ij / (sum of the chosen scores) for chosen j, 0 elsewhere;
@@ -29,15 +31,24 @@ __global__ __launch_bounds__(256) void tc_topk_kernel(const float* __restrict__ 
   __shared__ uint8_t sflag[TC_TOK][256];
   const int tid = threadIdx.x, r = tid & 15, grp = tid >> 4;   // 16 groups of 16 lanes
   const int i0 = blockIdx.x * TC_TOK;
-  for (int t = grp; t < TC_TOK; t += 16) {
-    const int i = i0 + t;
-    if (i >= N) break;                              // uniform over the group
-    float v[NQ];
+  constexpr int TPG = TC_TOK / 16;                 // tokens per lane group
+  // every token's scores are loaded before the first selection
+  float v[TPG][NQ];
+#pragma unroll
+  for (int u = 0; u < TPG; ++u) {
+    const int i = i0 + grp + 16 * u;
+    const int ii = i < N ? i : N - 1;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const int j = r + 16 * q;
-      v[q] = (j < E) ? S[(size_t)i * E + j] : -INFINITY;
+      v[u][q] = (j < E) ? S[(size_t)ii * E + j] : -INFINITY;
     }
+  }
+#pragma unroll
+  for (int u = 0; u < TPG; ++u) {
+    const int t = grp + 16 * u;
+    const int i = i0 + t;
+    if (i >= N) break;                              // uniform over the group
     uint32_t taken = 0u;                            // bit q: expert r + 16 q chosen
     float sum = 0.f;
     for (int c = 0; c < k; ++c) {
@@ -46,8 +57,8 @@ __global__ __launch_bounds__(256) void tc_topk_kernel(const float* __restrict__ 
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         const int j = r + 16 * q;
-        if (j < E && !((taken >> q) & 1u) && (v[q] > bv || (v[q] == bv && j < bj))) {
-          bv = v[q];
+        if (j < E && !((taken >> q) & 1u) && (v[u][q] > bv || (v[u][q] == bv && j < bj))) {
+          bv = v[u][q];
           bj = j;
         }
       }
@@ -72,7 +83,7 @@ __global__ __launch_bounds__(256) void tc_topk_kernel(const float* __restrict__ 
       const int j = r + 16 * q;
       if (j < E) {
         const bool ch = (taken >> q) & 1u;
-        G[(size_t)i * E + j] = ch ? v[q] * inv : 0.f;
+        G[(size_t)i * E + j] = ch ? v[u][q] * inv : 0.f;
         sflag[t][j] = ch ? 1 : 0;
       }
     }
