@@ -428,7 +428,8 @@ def main():
         return
     if a.routing == "tc" and not a.traffic_from:
         if a.gpus != 1:
-            print("bench.py runs on exactly one GPU", file=sys.stderr)
+            print(f"bench.py runs on exactly one GPU; --gpus {a.gpus} is not supported",
+                  file=sys.stderr)
             sys.exit(2)
         return run_tc(a)
     if a.traffic_from:
@@ -441,7 +442,7 @@ def main():
         return
     if a.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {a.gpus} is not supported (the layer's "
-              "multi-GPU sharding is a design, not part of this build)", file=sys.stderr)
+              "multi-GPU sharding is described, not implemented)", file=sys.stderr)
         sys.exit(2)
 
     import torch
