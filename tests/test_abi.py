@@ -227,3 +227,15 @@ def test_route_noalloc_rejects_problems_beyond_its_scratch():
                               None, None) == EC_ERR_CAPACITY
     assert L.ec_route_noalloc(_problem().ref, MISALIGNED, FAKE, FAKE, FAKE, None, None,
                               None) == EC_ERR_ALIGN
+
+
+def test_product_path_fails_loudly_without_the_library(monkeypatch, tmp_path):
+    # no CPU fallback: every entry point needs the built HIP library
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "libecmoe.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        binding.capacity([2048], 64, c=8.0)
+    X = torch.zeros((16, 64), dtype=torch.bfloat16)
+    Wg = torch.zeros((4, 64), dtype=torch.bfloat16)
+    with pytest.raises(RuntimeError, match="missing"):
+        binding.route(X, Wg, [0, 16], [4], 1.0)
