@@ -647,6 +647,24 @@ def test_random_problems(seed):
     full_case(wl)
 
 
+# larger shapes: several row blocks per expert buffer, the 192-row tiles, every
+# column top-k variant, up to 256 experts (EC_RANDOM_LARGE_CASES widens it)
+@pytest.mark.parametrize("seed", range(int(os.environ.get("EC_RANDOM_LARGE_CASES", "2"))))
+def test_random_large_problems(seed):
+    rng = np.random.default_rng(5000 + seed)
+    G = int(rng.integers(1, 4))
+    lens = [int(x) for x in rng.integers(1, 4500, size=G)]
+    E = int(rng.choice([8, 33, 64, 128, 256]))
+    d = 64 * int(rng.integers(4, 17))
+    h = 64 * int(rng.integers(2, 13))
+    backward = bool(rng.random() < 0.5)
+    kw = dict(c_min=float(rng.uniform(0.5, 2.0)), c_max=float(rng.uniform(2.0, 8.0)))
+    wl = synth.small(f"rndL{seed}", lens, d, E, h, seed=6000 + seed, backward=backward,
+                     inv_temperature=float(rng.choice([0.5, 1.0, 2.0])), **kw)
+    print(f"[case] lens={lens} d={d} E={E} h={h} backward={backward} {kw}", flush=True)
+    full_case(wl)
+
+
 @pytest.mark.parametrize("seed", range(int(os.environ.get("EC_RANDOM_TC_CASES", "4"))))
 def test_random_token_choice(seed):
     rng = np.random.default_rng(3000 + seed)
