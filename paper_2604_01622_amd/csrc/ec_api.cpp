@@ -10,25 +10,23 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
-#include <mutex>
-#include <string>
+#include <atomic>
 
 #include "ec_kernels.h"
 
 
 namespace {
 
-thread_local std::string g_last_error;
+// fixed per-thread buffer: recording an error allocates nothing and cannot throw
+thread_local char g_last_error[512];
 thread_local hipEvent_t* g_events = nullptr;  // stage timing (ec_set_stage_events)
 thread_local int g_n_events = 0;
 
 int fail(int status, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return status;
 }
 
@@ -46,7 +44,7 @@ struct Plan {
 // ec_buffers: check the sizes of the [E, K_tot, .] expert buffers of expert
 // choice (token choice packs its pairs and checks its own bound).
 int validate(const ec_problem* p, Plan* out, bool ec_buffers = true) {
-  g_last_error.clear();
+  g_last_error[0] = '\0';
   if (!p) return fail(EC_ERR_ARG, "problem is NULL");
   if (p->dtype != EC_F32 && p->dtype != EC_BF16)
     return fail(EC_ERR_DTYPE, "unknown dtype %d", (int)p->dtype);
@@ -365,8 +363,9 @@ constexpr size_t kScratchBytes = EC_ROUTE_NOALLOC_MAX_BYTES;
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 constexpr int kMaxDevices = 64;
-std::mutex g_scratch_mu;
-void* g_scratch_ptr[kMaxDevices] = {};
+// hipGetSymbolAddress gives the same address every time on a device, so two
+// threads that both fill an empty entry store the same value: no lock needed.
+std::atomic<void*> g_scratch_ptr[kMaxDevices] = {};
 
 // Device address of the current device's scratch array.
 int scratch_of_current_device(void** out) {
@@ -374,14 +373,13 @@ int scratch_of_current_device(void** out) {
   EC_HIP(hipGetDevice(&dev));
   if (dev < 0 || dev >= kMaxDevices)
     return fail(EC_ERR_HIP, "device index %d outside [0, %d)", dev, kMaxDevices);
-  std::lock_guard<std::mutex> lock(g_scratch_mu);
-  if (!g_scratch_ptr[dev]) {
-    void* ptr = nullptr;
+  void* ptr = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!ptr) {
     EC_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
     if (!ptr) return fail(EC_ERR_HIP, "hipGetSymbolAddress returned a null address");
-    g_scratch_ptr[dev] = ptr;
+    g_scratch_ptr[dev].store(ptr, std::memory_order_release);
   }
-  *out = g_scratch_ptr[dev];
+  *out = ptr;
   return EC_OK;
 }
 
@@ -403,10 +401,10 @@ const char* ec_status_string(int status) {
   }
 }
 
-const char* ec_last_error(void) { return g_last_error.c_str(); }
+const char* ec_last_error(void) { return g_last_error; }
 
 int ec_set_stage_events(hipEvent_t* events, int n_events) {
-  g_last_error.clear();
+  g_last_error[0] = '\0';
   if (n_events < 0 || (n_events > 0 && !events)) return fail(EC_ERR_ARG, "bad event array");
   g_events = n_events > 0 ? events : nullptr;
   g_n_events = n_events;
@@ -464,7 +462,7 @@ int ec_saved_layout_of(const ec_problem* p, ec_saved_layout* out) {
 
 int ec_capacity(int32_t n_groups, const int32_t* group_lengths, int32_t n_experts, double c_fixed,
                 const double* t, double c_min, double c_max, int scheduler, int32_t* k_out) {
-  g_last_error.clear();
+  g_last_error[0] = '\0';
   if (n_groups < 0 || !group_lengths || !k_out) return fail(EC_ERR_ARG, "bad arguments");
   if (n_experts < 1) return fail(EC_ERR_SHAPE, "n_experts must be >= 1");
   if (t && (scheduler < EC_SCHED_LINEAR || scheduler > EC_SCHED_GAUSSIAN_REV))
@@ -744,7 +742,7 @@ int ec_moe_backward(const ec_problem* p, const void* X, const void* Wg, const vo
 
 int ec_tc_capacity(int32_t n_groups, const int32_t* group_lengths, int32_t n_experts,
                    int32_t top_k, double cf, int32_t* cap_out) {
-  g_last_error.clear();
+  g_last_error[0] = '\0';
   if (n_groups < 0 || !group_lengths || !cap_out) return fail(EC_ERR_ARG, "bad arguments");
   if (n_experts < 1 || top_k < 1 || top_k > n_experts)
     return fail(EC_ERR_ARG, "need 1 <= top_k <= n_experts");
