@@ -20,9 +20,16 @@ its Section 2.2 and its Section 4):
 Pins (tests/test_oracle.py): brute-force selection on tiny inputs, exactly k_g
 tokens per (group, expert), softmax closed forms, the dense soft mixture when
 every token is selected, the textbook SwiGLU FFN when E = 1, central finite
-differences of the backward, Table 5 of the paper for the capacity
-schedulers, and the drop statistic's closed cases (every token kept when
-k_g = L_g, every token dropped when k_g = 0, L_g - k_g dropped when E = 1).
+differences and torch autograd of the backward, Table 5 of the paper for the
+capacity schedulers and Figure 2's per-expert loads, the drop statistic's
+closed cases (every token kept when k_g = L_g, every token dropped when
+k_g = 0, L_g - k_g dropped when E = 1), and for token choice the rank
+definition of the row top-k with ties, first-come capacity, the arg-max expert
+at top-1, the expert-choice mixture at top-E without a cap, and the
+dropped-pair gate rule against a construction from torch's stable sort.
+Mutation tests plant plausible mistakes (tie direction, temperature, the
+activation, W1 and W3 swapped, a dropped softmax-Jacobian term) and check that
+a pin fails.
 """
 from __future__ import annotations
 
