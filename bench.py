@@ -399,6 +399,9 @@ def main():
                     help="token choice: capacity factor (<= 0: dropless)")
     ap.add_argument("--router-skew", type=float, default=0.0,
                     help="token choice: scale router rows by exp(N(0, s)) (uneven expert loads)")
+    ap.add_argument("--mask-ratio", type=float, default=None,
+                    help="every sequence's mask ratio t (workloads with c(t) = 12 - 8t capacities): "
+                         "the capacity, and so the expert work, of one point of the schedule")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forward-only", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
@@ -456,6 +459,10 @@ def main():
     log(f"[bench] drawing {wl.name}")
     inp = synth.draw(wl, with_dy=backward)
     L = np.asarray(wl.group_lengths)
+    if a.mask_ratio is not None:
+        if not wl.time_dependent:
+            raise SystemExit(f"--mask-ratio needs a workload with c(t) capacities, not {a.workload}")
+        inp.t = np.full_like(inp.t, a.mask_ratio)
     if wl.time_dependent:
         caps = ec.capacity(L, wl.n_experts, t=inp.t, c_min=wl.c_min, c_max=wl.c_max)
     else:
@@ -590,6 +597,8 @@ def main():
            "grouped_gemm": {"tflops": round(gemm_fl / (gemm_ms * 1e-3) / 1e12, 1),
                             "mfma_frac": round(gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}}
 
+    if a.mask_ratio is not None:
+        out["config"]["mask_ratio"] = a.mask_ratio
     # token drop statistic (Appendix D) of this batch, from the routing the step made
     if backward:
         slot = binding.saved_views(layer.saved, layer.P)["slot"]

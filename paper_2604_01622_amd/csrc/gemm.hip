@@ -6,8 +6,8 @@
 // bf16: one pipelined kernel (gemm_dma_kernel) for every product of the
 // forward and backward.  v_mfma_f32_32x32x16_bf16 with fp32 accumulation; a
 // 256 x 256 output tile per workgroup of 8 waves (2 per SIMD, 64 x 128 or
-// 128 x 64 each; the forward products take 192-row tiles of 96 x 64 per wave
-// when those pad short expert buffers less);
+// 128 x 64 each; the forward products take 192- or 128-row tiles, 96 x 64 or
+// 64 x 64 per wave, when those pad short expert buffers less);
 // K advances 64 at a time through a 2-stage LDS ring filled straight from
 // global memory by global_load_lds_dwordx4 (no VGPR staging).  K-contiguous
 // operands sit in LDS as 128-byte rows with XOR-swizzled 16-byte chunks
@@ -846,15 +846,18 @@ hipError_t run_dma_var(GemmParams p, long max_rows, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Row blocks of 192 for the forward expert products when they pad the expert
+// Row blocks of the forward expert products: 192 when they pad the expert
 // buffers enough less than blocks of 256 (one 2048-token sequence at c(t) =
-// 12 - 8t has 373 rows per expert: 384 computed instead of 512).  A 192-row
-// tile (96 x 64 per wave) does three quarters of the work in 0.875 of the time
-// (W1/W3 on that sequence), so a computed row costs 7/6 as much.  Both keep an
+// 12 - 8t has 373 rows per expert: 384 computed instead of 512), 128 for
+// buffers of at most 128 rows (that sequence at t = 1).  A 192-row tile (96 x 64
+// per wave) does three quarters of a 256-row tile's work in 0.875 of its time,
+// a 128-row tile (64 x 64 per wave) half the work in 0.74 of the time (W1/W3),
+// so a computed row costs 7/6 and 1.47 times as much.  Every choice keeps an
 // expert's row blocks side by side on one XCD, so its weights are fetched once.
-bool short_rows(int M) {
+int fwd_block_rows(int M) {
+  if (M <= 128) return 128;
   const long r256 = (M + 255) / 256 * 256L, r192 = (M + 191) / 192 * 192L;
-  return r192 * 7 < r256 * 6;
+  return r192 * 7 < r256 * 6 ? 192 : 256;
 }
 
 // ------------------------------------------------------------------ fp32 FMA
@@ -1039,8 +1042,11 @@ hipError_t launch_gemm_w13(int dtype, const void* Xe, const void* W1, const void
     if (rows) return hipErrorInvalidValue;   // the shared experts read X as is
     return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_SH_W13>(p, st);
   }
-  if (short_rows(M)) return run_dma<192, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
-  return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
+  switch (fwd_block_rows(M)) {
+    case 128: return run_dma<128, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
+    case 192: return run_dma<192, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
+    default: return run_dma<256, 256, 2, 4, 64, 2, true, true, EPI_SWIGLU, false, G_W13>(p, st);
+  }
 }
 
 hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int E, int M, int d,
@@ -1053,8 +1059,11 @@ hipError_t launch_gemm_w2(int dtype, const void* A, const void* W2, void* O, int
   if (M == 0) return hipSuccess;
   if (dtype == DT_F32) return run_f32<EPI_STORE>(p, 1, 1, st);
   if (shared) return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_SH_W2>(p, st);
-  if (short_rows(M)) return run_dma<192, 256, 2, 4, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
-  return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
+  switch (fwd_block_rows(M)) {
+    case 128: return run_dma<128, 256, 2, 4, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
+    case 192: return run_dma<192, 256, 2, 4, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
+    default: return run_dma<256, 256, 4, 2, 64, 2, true, true, EPI_STORE, false, G_W2>(p, st);
+  }
 }
 
 hipError_t launch_gemm_dA(int dtype, const void* dO, const void* W2, const void* H1,
