@@ -222,11 +222,14 @@ def cpu_baseline(inp, caps, inv_tau, backward, budget_s=10.0):
     time in order, until the budget is spent; each group is routed on its own, exactly as
     in the layer (routing never crosses a group)."""
     from oracle import ec_ref as ref
+    affinity = len(os.sched_getaffinity(0))
     try:
         from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        pools = [i for i in threadpool_info() if i.get("user_api") == "blas"] or threadpool_info()
+        blas_threads = max([i.get("num_threads", 1) for i in pools] or [1])
+        blas = ", ".join(sorted({str(i.get("internal_api", "?")) for i in pools})) or None
     except Exception:  # pragma: no cover
-        blas_threads = len(os.sched_getaffinity(0))
+        blas_threads, blas = affinity, None
     wl = inp.wl
     off = wl.group_offsets
     tokens, dt, groups = 0, 0.0, 0
@@ -246,6 +249,7 @@ def cpu_baseline(inp, caps, inv_tau, backward, budget_s=10.0):
         if dt >= budget_s:
             break
     return {"value": tokens / dt, "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
+            "affinity_cpus": affinity, "blas": blas,
             "sample": f"routing groups 0..{groups - 1} of {wl.n_groups} ({tokens} tokens, all "
                       f"{wl.n_experts} experts), {'fwd+bwd' if backward else 'fwd'}, numpy float64, "
                       f"{dt:.1f} s",
