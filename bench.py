@@ -457,6 +457,10 @@ def main():
     from paper_2604_01622_amd import binding, synth
 
     wl = WORKLOADS(synth)[a.workload]
+    if a.mask_ratio is not None and not (wl.time_dependent and 0.0 <= a.mask_ratio <= 1.0):
+        print(f"--mask-ratio needs a workload with c(t) capacities and t in [0, 1] "
+              f"(got {a.workload}, {a.mask_ratio})", file=sys.stderr)
+        sys.exit(2)
     backward = a.workload in ("train", "train_shared")
     inv_tau = wl.inv_temperatures[0]
     torch.cuda.set_device(0)
@@ -464,8 +468,6 @@ def main():
     inp = synth.draw(wl, with_dy=backward)
     L = np.asarray(wl.group_lengths)
     if a.mask_ratio is not None:
-        if not wl.time_dependent:
-            raise SystemExit(f"--mask-ratio needs a workload with c(t) capacities, not {a.workload}")
         inp.t = np.full_like(inp.t, a.mask_ratio)
     if wl.time_dependent:
         caps = ec.capacity(L, wl.n_experts, t=inp.t, c_min=wl.c_min, c_max=wl.c_max)

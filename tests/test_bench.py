@@ -100,3 +100,12 @@ def test_more_than_one_gpu_is_refused(extra):
     assert r.returncode == 2
     assert "exactly one GPU" in r.stderr
     assert r.stdout == ""
+
+
+@pytest.mark.parametrize("args", [["--workload", "static", "--mask-ratio", "0.5"],
+                                  ["--workload", "decode", "--mask-ratio", "1.5"]])
+def test_mask_ratio_needs_a_schedule_and_a_ratio_in_range(args):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py")] + args,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2
+    assert "--mask-ratio needs" in r.stderr
