@@ -223,6 +223,14 @@ def test_many_groups():
     full_case(wl)
 
 
+def test_many_tokens():
+    # 64 sequences of 4096 tokens: 4096 router workgroups of 64 tokens, a top-k
+    # grid of 16 x 64 columns, 32768 rows per expert buffer (128 row blocks)
+    wl = synth.small("many_tokens", [4096] * 64, 128, 16, 128, seed=18, capacity_factor=2.0,
+                     backward=True)
+    full_case(wl)
+
+
 def test_long_group_route_only():
     # a column longer than the LDS-cached top-k path
     wl = synth.small("long", [20000, 777], 64, 4, 64, seed=18, capacity_factor=1.5)
