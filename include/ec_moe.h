@@ -72,7 +72,8 @@ typedef enum {
 
 /* Problem description.  Limits: 1 <= E <= 256; d and h multiples of 64 with
  * 64 <= d, h <= 16384; 1 <= G; N = group_offsets[G] < 2^31; every expert
- * buffer E * K_tot * max(d, h) < 2^31 elements; N * 2 * max(d, hs) < 2^31.    */
+ * buffer within 2^31 elements: E * K_tot * 2 * max(d, h) < 2^31 (the backward's
+ * [E, K_tot, 2h] buffer); E * N < 2^31; N * 2 * max(d, hs) < 2^31.            */
 typedef struct {
   int64_t n_tokens;              /* N = sum of the group lengths                       */
   int32_t d_model;               /* d                                                  */

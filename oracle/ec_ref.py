@@ -545,6 +545,26 @@ def expert_grads_ref(X, Wg, W1, W3, W2, dY, sel_token, j: int, inv_tau: float = 
     return dh1.T @ x, dh3.T @ x, do.T @ a
 
 
+def expert_grads_units_ref(X, Wg, W1, W3, W2, dY, sel_token, j: int, units,
+                           inv_tau: float = 1.0):
+    """Rows `units` of dW1_j and dW3_j and columns `units` of dW2_j (hidden units of
+    expert j), selection given: each hidden unit needs only its own pre-activations
+    over the expert's rows."""
+    u = np.asarray(units, dtype=np.int64)
+    rows = np.asarray(sel_token)[j]
+    x = widen(np.asarray(X)[rows])
+    g = softmax_ref(x @ widen(Wg).T, inv_tau)[:, j]
+    h1 = x @ widen(np.asarray(W1[j])[u]).T
+    h3 = x @ widen(np.asarray(W3[j])[u]).T
+    sg = 1.0 / (1.0 + np.exp(-h1))
+    a = h1 * sg * h3
+    do = g[:, None] * widen(np.asarray(dY)[rows])
+    da = do @ widen(np.asarray(W2[j])[:, u])
+    dh3 = da * (h1 * sg)
+    dh1 = da * h3 * (sg * (1.0 + h1 * (1.0 - sg)))
+    return dh1.T @ x, dh3.T @ x, do.T @ a
+
+
 def router_grad_ref(X, Wg, W1, W3, W2, dY, sel_token, inv_tau: float = 1.0) -> np.ndarray:
     """dWg [E, d] with the selection given (needs every selected pair's output)."""
     Xf, dYf = widen(X), widen(dY)

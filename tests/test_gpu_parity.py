@@ -231,6 +231,35 @@ def test_many_tokens():
     full_case(wl)
 
 
+def test_near_the_size_limit():
+    # E K_tot 2 max(d, h) within 0.5% of the 2^31-element limit (the [E, K, 2h]
+    # buffer of the backward: 4.3 GB; H1, H3 and A 2.1 GB each): sampled rows of
+    # S, Y and dX, and sampled hidden units of every expert's weight gradients
+    wl = synth.small("near_limit", [262112], 512, 2, 2048, seed=19, capacity_factor=1.99,
+                     backward=True)
+    print(f"[case] {wl.name}", flush=True)
+    inp = synth.draw(wl, with_dy=True)
+    caps = caps_for(wl, inp)
+    K = int(np.sum(caps))
+    assert 2 * K * 2 * 2048 < 2 ** 31 and 2 * K * 2 * 2048 > 0.99 * 2 ** 31
+    rng = np.random.default_rng(19)
+    rows = np.sort(rng.choice(wl.n_tokens, 48, replace=False))
+    S_h, sel = check_route(inp, caps, 1.0, S_rows=rows)
+    out = run_layer(inp, caps, 1.0, backward=True)
+    assert np.array_equal(out["views"]["sel_token"].cpu().numpy(), sel)
+    args = (inp.X, inp.Wg, inp.W1, inp.W3, inp.W2)
+    errs = {"Y": rel_l2(out["Y"][rows], ref.forward_rows_ref(*args, sel, rows, 1.0)),
+            "dX": rel_l2(out["dX"][rows], ref.backward_rows_ref(*args, inp.dY, sel, rows, 1.0))}
+    units = [0, 777, 2047]
+    for j in range(2):
+        g1, g3, g2 = ref.expert_grads_units_ref(*args, inp.dY, sel, j, units, 1.0)
+        errs[f"dW1[{j}]"] = rel_l2(out["dW1"][j][units], g1)
+        errs[f"dW3[{j}]"] = rel_l2(out["dW3"][j][units], g3)
+        errs[f"dW2[{j}]"] = rel_l2(out["dW2"][j][:, units], g2)
+    print("[errs]", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    assert all(v <= out_tol("bf16") for v in errs.values()), errs
+
+
 def test_long_group_route_only():
     # a column longer than the LDS-cached top-k path
     wl = synth.small("long", [20000, 777], 64, 4, 64, seed=18, capacity_factor=1.5)

@@ -637,6 +637,12 @@ def test_restricted_forms_equal_full_definitions():
         assert np.max(np.abs(g1 - full["dW1"][j])) < 1e-12
         assert np.max(np.abs(g3 - full["dW3"][j])) < 1e-12
         assert np.max(np.abs(g2 - full["dW2"][j])) < 1e-12
+        units = [0, 7, 23]
+        u1, u3, u2 = ref.expert_grads_units_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY,
+                                                sel, j, units, inv_tau)
+        assert np.max(np.abs(u1 - full["dW1"][j][units])) < 1e-12
+        assert np.max(np.abs(u3 - full["dW3"][j][units])) < 1e-12
+        assert np.max(np.abs(u2 - full["dW2"][j][:, units])) < 1e-12
     dWg = ref.router_grad_ref(inp.X, inp.Wg, inp.W1, inp.W3, inp.W2, inp.dY, sel, inv_tau)
     assert np.max(np.abs(dWg - full["dWg"])) < 1e-12
     # the backward's Y and the per-expert outputs: the forward's terms, and their
